@@ -1,0 +1,283 @@
+"""SparsePR CPU oracle: ctypes wrapper over the plain C reference.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
+the benchmark's CPU-baseline leg; the GPU library never imports, links or
+runs it.  Every function works on one attention head given float32 numpy
+arrays and returns numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sparsepr_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libsparsepr_oracle.so")
+_lib = None
+
+# Portable x86-64-v3 code (the library travels to other hosts); no
+# floating-point contraction so every float expression is evaluated as written.
+CFLAGS = ["-O3", "-march=x86-64-v3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+          "-shared", "-fPIC", "-std=c11", "-Wall"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into oracle/libsparsepr_oracle.so."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        _lib = ctypes.CDLL(_LIB_PATH)
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _i64(a):
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def dense_rows(q, k, v, rows=None):
+    q, k, v = _f32(q), _f32(k), _f32(v)
+    n, d = q.shape
+    dv = v.shape[1]
+    rows = _i64(np.arange(n) if rows is None else rows)
+    out = np.zeros((len(rows), dv), np.float64)
+    lib().or_dense_rows(_p(q), _p(k), _p(v), k.shape[0], d, dv, _p(rows), len(rows), _p(out))
+    return out
+
+
+def sparse_rows(q, k, v, labels_q, labels_kv, z, rows=None):
+    q, k, v = _f32(q), _f32(k), _f32(v)
+    n, d = q.shape
+    dv = v.shape[1]
+    z = np.ascontiguousarray(z, dtype=np.uint8)
+    rows = _i64(np.arange(n) if rows is None else rows)
+    out = np.zeros((len(rows), dv), np.float64)
+    lib().or_sparse_rows(_p(q), _p(k), _p(v), k.shape[0], d, dv, _p(_i32(labels_q)),
+                         _p(_i32(labels_kv)), z.shape[1], _p(z), _p(rows), len(rows), _p(out))
+    return out
+
+
+def key_metric(q, m_s):
+    q = _f32(q)
+    n, d = q.shape
+    out = np.zeros((d, d), np.float64)
+    lib().or_key_metric(_p(q), n, d, m_s, _p(out))
+    return out
+
+
+def sym_eig(a):
+    a = _f64(a)
+    n = a.shape[0]
+    ev = np.zeros(n, np.float64)
+    u = np.zeros((n, n), np.float64)
+    lib().or_sym_eig(_p(a), n, _p(ev), _p(u))
+    return ev, u
+
+
+def response_basis(m, r, tau=1e-6):
+    m = _f64(m)
+    d = m.shape[0]
+    r = min(r, d)
+    f = np.zeros((d, r), np.float64)
+    ev = np.zeros(d, np.float64)
+    lib().or_response_basis(_p(m), d, r, ctypes.c_double(tau), _p(f), _p(ev))
+    return f, ev
+
+
+def project(x, f, rms=False, eps=1e-6):
+    x, f = _f32(x), _f64(f)
+    n, d = x.shape
+    r = f.shape[1]
+    phi = np.zeros((n, r), np.float32)
+    lib().or_project(_p(x), n, d, _p(f), r, int(rms), ctypes.c_double(eps), _p(phi))
+    return phi
+
+
+def kmeans(pts, c, iters):
+    pts = _f32(pts)
+    n, r = pts.shape
+    labels = np.zeros(n, np.int32)
+    cent = np.zeros((c, r), np.float32)
+    counts = np.zeros(c, np.int32)
+    it = lib().or_kmeans(_p(pts), n, r, c, iters, _p(labels), _p(cent), _p(counts))
+    return labels, cent, counts, it
+
+
+def kmeans_assign(pts, cent, want_scores=False):
+    pts, cent = _f32(pts), _f32(cent)
+    n, r = pts.shape
+    c = cent.shape[0]
+    labels = np.zeros(n, np.int32)
+    scores = np.zeros((n, c), np.float32) if want_scores else None
+    lib().or_kmeans_assign(_p(pts), n, r, _p(cent), c, _p(labels), _p(scores))
+    return (labels, scores) if want_scores else labels
+
+
+def group_mean(x, labels, c):
+    x = _f32(x)
+    n, d = x.shape
+    mean = np.zeros((c, d), np.float32)
+    counts = np.zeros(c, np.int32)
+    lib().or_group_mean(_p(x), n, d, _p(_i32(labels)), c, _p(mean), _p(counts))
+    return mean, counts
+
+
+def query_metric(kbar, counts):
+    kbar = _f32(kbar)
+    c, d = kbar.shape
+    out = np.zeros((d, d), np.float64)
+    lib().or_query_metric(_p(kbar), _p(_i32(counts)), c, d, _p(out))
+    return out
+
+
+def stable_perm(labels, c):
+    labels = _i32(labels)
+    n = len(labels)
+    perm = np.zeros(n, np.int32)
+    off = np.zeros(c + 1, np.int32)
+    lib().or_stable_perm(_p(labels), n, c, _p(perm), _p(off))
+    return perm, off
+
+
+def route_priorities(qbar, nq, kbar, nk):
+    qbar, kbar = _f32(qbar), _f32(kbar)
+    cq, d = qbar.shape
+    ck = kbar.shape[0]
+    prio = np.zeros((cq, ck), np.float32)
+    lib().or_route_priorities(_p(qbar), _p(_i32(nq)), cq, _p(kbar), _p(_i32(nk)), ck, d, _p(prio))
+    return prio
+
+
+def route_select(prio, nq, nk, budget):
+    prio = _f32(prio)
+    cq, ck = prio.shape
+    z = np.zeros((cq, ck), np.uint8)
+    out = np.zeros(4, np.int64)
+    lib().or_route_select(_p(prio), _p(_i32(nq)), cq, _p(_i32(nk)), ck, ctypes.c_int64(int(budget)),
+                          _p(z), _p(out))
+    return z, {"routed_pairs": int(out[0]), "forced_pairs": int(out[1]),
+               "routed_cells": int(out[2]), "forced_cells": int(out[3])}
+
+
+def probe_select(phi, labels, cent, m):
+    phi, cent = _f32(phi), _f32(cent)
+    n, r = phi.shape
+    c = cent.shape[0]
+    probes = np.zeros(max(m, 1), np.int32)
+    w = np.zeros(max(m, 1), np.float64)
+    np_ = lib().or_probe_select(_p(phi), n, r, _p(_i32(labels)), c, _p(cent), m, _p(probes), _p(w))
+    return probes[:np_], w[:np_]
+
+
+def fit(x, od, w, r, lam, eps=1e-6):
+    x, od, w = _f64(x), _f64(od), _f64(w)
+    m, dv = x.shape if x.ndim == 2 else (0, od.shape[-1])
+    mu_x = np.zeros(dv)
+    s_x = np.zeros(dv)
+    mu_r = np.zeros(dv)
+    b = np.zeros((dv, dv))
+    psi = np.zeros((dv, max(r, 1)))
+    g = np.zeros((dv, dv))
+    rank = ctypes.c_int(0)
+    st = lib().or_fit(_p(x), _p(od), _p(w), m, dv, r, ctypes.c_double(lam), ctypes.c_double(eps),
+                      _p(mu_x), _p(s_x), _p(mu_r), _p(b), _p(psi), _p(g), ctypes.byref(rank))
+    return {"status": st, "mu_x": mu_x, "s_x": s_x, "mu_r": mu_r, "b": b,
+            "psi": psi[:, :rank.value], "g": g, "rank": rank.value}
+
+
+def correct_rows(x, ft):
+    x = _f64(x)
+    n, dv = x.shape
+    out = np.zeros_like(x)
+    lib().or_correct_rows(_p(x), n, dv, _p(ft["mu_x"]), _p(ft["s_x"]), _p(ft["mu_r"]),
+                          _p(_f64(ft["g"])), _p(out))
+    return out
+
+
+def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_probes):
+    """Whole Response-Coupled Partitioning + routing + probe choice for one head."""
+    q, k = _f32(q), _f32(k)
+    n, d = q.shape
+    nv = n - n_text
+    rk, rq = min(r_k, d), min(r_q, d)
+    cq_t, ck_t = c_q + (n_text > 0), c_k + (n_text > 0)
+    out = {
+        "labels_q": np.zeros(n, np.int32), "labels_kv": np.zeros(n, np.int32),
+        "z": np.zeros((cq_t, ck_t), np.uint8),
+        "probes": np.zeros(max(n_probes, 1), np.int32), "w": np.zeros(max(n_probes, 1)),
+        "fk": np.zeros((d, rk)), "fq": np.zeros((d, rq)),
+        "phik": np.zeros((nv, rk), np.float32), "phiq": np.zeros((nv, rq), np.float32),
+        "kbar": np.zeros((c_k, d), np.float32), "qbar": np.zeros((c_q, d), np.float32),
+        "cqphi": np.zeros((c_q, rq), np.float32), "prio": np.zeros((c_q, c_k), np.float32),
+        "stats": np.zeros(7, np.int64),
+    }
+    lib().or_plan(_p(q), _p(k), n, d, n_text, n_sampled, r_k, r_q, c_k, c_q, iters,
+                  ctypes.c_double(density), n_probes, _p(out["labels_q"]), _p(out["labels_kv"]),
+                  _p(out["z"]), _p(out["probes"]), _p(out["w"]), _p(out["fk"]), _p(out["fq"]),
+                  _p(out["phik"]), _p(out["phiq"]), _p(out["kbar"]), _p(out["qbar"]),
+                  _p(out["cqphi"]), _p(out["prio"]), _p(out["stats"]))
+    npr = int(out["stats"][4])
+    out["probes"] = out["probes"][:npr]
+    out["w"] = out["w"][:npr]
+    s = out["stats"]
+    out["rho_route"] = s[0] / float(n) / float(n)
+    out["rho_exec"] = out["rho_route"] + npr / float(n)
+    return out
+
+
+def attend(q, k, v, labels_q, labels_kv, z, probes, w, *, n_text=0, r, lam, eps=1e-6):
+    """Sparse attention + exact probes + fit + correction for one head (double)."""
+    q, k, v = _f32(q), _f32(k), _f32(v)
+    n, d = q.shape
+    dv = v.shape[1]
+    z = np.ascontiguousarray(z, dtype=np.uint8)
+    probes = _i32(probes)
+    w = _f64(w)
+    m = len(probes)
+    out = np.zeros((n, dv), np.float64)
+    fo = np.zeros(3 * dv + dv * dv, np.float64)
+    st = lib().or_attend(_p(q), _p(k), _p(v), n, d, dv, n_text, _p(_i32(labels_q)),
+                         _p(_i32(labels_kv)), z.shape[0], z.shape[1], _p(z),
+                         _p(probes) if m else None, _p(w) if m else None, m, r,
+                         ctypes.c_double(lam), ctypes.c_double(eps), _p(out), _p(fo))
+    fit_out = {"status": st, "mu_x": fo[:dv], "s_x": fo[dv:2 * dv], "mu_r": fo[2 * dv:3 * dv],
+               "g": fo[3 * dv:].reshape(dv, dv)}
+    return out, fit_out
+
+
+def run(q, k, v, **params):
+    """plan + attend for one head; returns (output, plan)."""
+    pl = plan(q, k, n_text=params.get("n_text", 0), n_sampled=params["n_sampled"],
+              r_k=params["r_k"], r_q=params["r_q"], c_k=params["c_k"], c_q=params["c_q"],
+              iters=params["iters"], density=params["density"], n_probes=params["n_probes"])
+    out, ft = attend(q, k, v, pl["labels_q"], pl["labels_kv"], pl["z"], pl["probes"], pl["w"],
+                     n_text=params.get("n_text", 0), r=params["r"], lam=params["lam"])
+    pl["fit"] = ft
+    return out, pl
