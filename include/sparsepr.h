@@ -1,0 +1,220 @@
+/*
+ * sparsepr.h -- C ABI of the MI355X (gfx950) SparsePR sparse attention library.
+ *
+ * SparsePR ("Partition the Support, Reconstruct the Residual") replaces dense
+ * softmax attention of one head, O = softmax(Q K^T / sqrt(d)) V (Sec. 3,
+ * eq. dense_attention), by
+ *   1. Response-Coupled Partitioning (Sec. 4.1, App. B): paired K/V groups from
+ *      k-means on key-response coordinates phi_K = F_K^T k, then query groups
+ *      from k-means on the centroid-induced query coordinates phi_Q;
+ *   2. shared block routing of query-group x K/V-group cells under a pair
+ *      budget that charges each cell |G_a| |G_b| and reserves the probes' cost
+ *      first (Sec. 4.3, eq. pair_density);
+ *   3. renormalised hard-drop sparse attention over the routed cells, on
+ *      group-major permuted K/V (Sec. 3, eq. hard_drop; Sec. 4.3);
+ *   4. Probe-Fitted Residual Reconstruction (Sec. 4.2, App. A): exact rows for
+ *      M probe queries, a weighted ridge fit of the residual on the sparse
+ *      output restricted to the probes' residual subspace, and the affine
+ *      correction applied to every other row (eq. final_reconstructed_output).
+ *
+ * The work is split in two calls that follow that statement of the problem:
+ * sparsepr_plan (steps 1-2 and the probe choice of App. A.2) and
+ * sparsepr_attend (steps 3-4 and the restore to the original row order).
+ *
+ * Conventions (all entry points):
+ *  - Q, K, V and the output are DEVICE pointers to [batch, heads, n, d]
+ *    tensors addressed with element strides (stride_b, stride_h, stride_n);
+ *    the last dimension is contiguous.  dtype is float32 or bfloat16 for all
+ *    four; accumulation is always at least float32.
+ *  - Every batch x head pair is an independent SparsePR call with the same
+ *    parameters; all of them are processed by each launch.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued asynchronously on it; the caller keeps Q, K, V, the
+ *    output and the workspace alive until that work has completed.  Only
+ *    sparsepr_get_stats and sparsepr_plan_export synchronise the stream.
+ *  - The caller owns all memory.  The library never allocates device memory:
+ *    everything it needs lives in the caller's workspace.
+ *  - Every entry point returns a status; no C++ exception crosses the ABI.
+ *    Arguments are validated on the host before anything is enqueued, and a
+ *    call that fails validation has no side effects.  sparsepr_last_error()
+ *    describes the most recent failure of the calling thread.
+ */
+#ifndef SPARSEPR_H
+#define SPARSEPR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPARSEPR_OK = 0,
+  SPARSEPR_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size or parameter range */
+  SPARSEPR_ERR_UNSUPPORTED = 2,      /* valid but not implemented (e.g. d = 96) */
+  SPARSEPR_ERR_WORKSPACE_TOO_SMALL = 3,
+  SPARSEPR_ERR_HIP = 4,              /* a HIP runtime call failed */
+  SPARSEPR_ERR_NUMERICAL = 5         /* reported by sparsepr_get_stats only */
+} sparsepr_status;
+
+typedef enum { SPARSEPR_F32 = 0, SPARSEPR_BF16 = 1 } sparsepr_dtype;
+
+/* Tensor geometry.  Self-attention only: n_q == n_kv.  d == d_v in {64, 128}. */
+typedef struct {
+  int32_t batch, heads;
+  int32_t n_q, n_kv;
+  int32_t d, d_v;
+  int64_t stride_b, stride_h, stride_n; /* element strides shared by Q, K, V and O */
+  int32_t dtype;                        /* sparsepr_dtype */
+} sparsepr_shape;
+
+/* Per-call method parameters (paper defaults from App. C.2 where it gives them). */
+typedef struct {
+  int32_t n_sampled_queries;   /* M_s: strided query sample for M_K (App. B.1); 256 */
+  int32_t r_k, r_q;            /* response ranks r_K = 48, r_Q = 64 (clamped to d) */
+  int32_t n_kv_groups;         /* C_k, K/V groups over the video rows */
+  int32_t n_q_groups;          /* C_q, query groups over the video rows */
+  int32_t kmeans_iters;        /* T, Lloyd iterations (cold start); 8 */
+  float target_exec_density;   /* rho_exec target incl. probes (Sec. 4.3); 0.22 */
+  int32_t n_probes;            /* M exact probe rows per head (App. A.2); 64 */
+  int32_t resid_rank;          /* r, probe-residual output rank (Sec. 4.2); 16 */
+  float ridge;                 /* lambda (eq. probe_ridge_fit); 0.1 */
+  float eps_q;                 /* RMS floor of eq. query_response_feature; 1e-6 */
+  float eps_x;                 /* variance floor of eq. app_feature_scale; 1e-6 */
+  int32_t n_dense_prefix;      /* leading rows (e.g. text tokens) routed densely,
+                                  outside clustering, probes and the budget; 0 */
+} sparsepr_params;
+
+/* Realised accounting of one call (Sec. 4.3: rho_exec = rho_route + M/N_q). */
+typedef struct {
+  double rho_route;          /* routed pairs / (n_q n_kv), mean over heads */
+  double rho_exec;           /* rho_route + probes / n_q, mean over heads */
+  int64_t routed_pairs;      /* sum over heads (includes forced and dense-prefix cells) */
+  int64_t exec_pairs;        /* routed_pairs + probes * n_kv, sum over heads */
+  int64_t forced_pairs;      /* pairs of cells kept regardless of the budget */
+  int32_t routed_cells;      /* sum over heads (video x video cells) */
+  int32_t forced_cells;
+  int32_t nonempty_q_groups; /* sum over heads */
+  int32_t nonempty_kv_groups;
+  int32_t n_probes;          /* sum over heads */
+  int32_t kmeans_iters_kv;   /* max over heads of assignments performed */
+  int32_t kmeans_iters_q;
+  int32_t status_flags;      /* OR over heads of SPARSEPR_FLAG_* */
+} sparsepr_stats;
+
+#define SPARSEPR_FLAG_NONFINITE_INPUT 1 /* a NaN/Inf reached the partition features */
+#define SPARSEPR_FLAG_FIT_NOT_PD 2      /* ridge normal matrix not positive definite; correction
+                                           reduced to the mean residual */
+#define SPARSEPR_FLAG_BUDGET_BELOW_FORCED 4 /* forced cells alone exceed the pair budget */
+
+/* Host-side view of one head's plan, for export (diagnostics, oracle replay)
+ * and import (running attend on a plan made elsewhere).  All arrays are HOST
+ * memory owned by the caller; a NULL pointer skips that array.  Sizes use
+ * n = n_q, n_v = n - n_dense_prefix, C_q/C_k = the group counts, and
+ * Cq_t = C_q + (n_dense_prefix > 0), Ck_t = C_k + (n_dense_prefix > 0) (the
+ * dense prefix forms the extra last group on each side). */
+typedef struct {
+  /* plan content: exported, and read by import */
+  int32_t* labels_q;     /* [n]  query group of each row, in [0, Cq_t) */
+  int32_t* labels_kv;    /* [n]  K/V group of each row, in [0, Ck_t) */
+  uint8_t* routes;       /* [Cq_t * Ck_t] 1 = cell evaluated */
+  int32_t* probes;       /* [n_probes] probe rows in selection order */
+  int32_t n_probes;      /* export: written; import: number of entries in probes */
+  /* derived data: export only */
+  float* probe_weights;  /* [n_probes] coverage weights w_p = |G_a| / m_a */
+  int32_t* perm_q;       /* [n]  group-major order of the query rows */
+  int32_t* off_q;        /* [Cq_t + 1] */
+  int32_t* perm_kv;      /* [n] */
+  int32_t* off_kv;       /* [Ck_t + 1] */
+  float* m_k;            /* [d*d] key-response metric */
+  float* m_q;            /* [d*d] query-response metric */
+  float* f_k;            /* [d * r_k] eigen-scaled key basis */
+  float* f_q;            /* [d * r_q] */
+  float* phi_k;          /* [n_v * r_k] key-response coordinates */
+  float* phi_q;          /* [n_v * r_q] query-response coordinates */
+  float* cent_k;         /* [C_k * r_k] final K/V k-means centroids */
+  float* cent_q;         /* [C_q * r_q] final query k-means centroids (probe means) */
+  float* kbar;           /* [C_k * d] key-space group means */
+  float* qbar;           /* [C_q * d] query-space group means */
+  float* route_prio;     /* [C_q * C_k] route priorities (0 for empty groups) */
+  /* after sparsepr_attend: */
+  float* o_sparse;       /* [n * d_v] hard-drop output, original row order */
+  float* o_dense_probes; /* [n_probes * d_v] exact probe rows */
+  float* fit_mu_x;       /* [d_v] */
+  float* fit_s_x;        /* [d_v] */
+  float* fit_mu_r;       /* [d_v] */
+  float* fit_bpsi;       /* [d_v * r] B_lambda Psi_r (the ridge map times the basis) */
+  float* fit_psi;        /* [d_v * r] Psi_r (columns beyond fit_rank are 0) */
+  int32_t fit_rank;      /* export: retained residual rank */
+} sparsepr_plan_host;
+
+typedef struct sparsepr_plan_s* sparsepr_plan_t;
+
+/* Fill `p` with the paper's defaults (App. C.2) and C_k = C_q = 0, which
+ * sparsepr_plan_create replaces by ceil(n_v / 64). */
+void sparsepr_params_default(sparsepr_params* p);
+
+/* Bytes of device workspace one plan needs for this shape and parameters.
+ * Errors: INVALID_ARGUMENT / UNSUPPORTED as for sparsepr_plan_create. */
+sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const sparsepr_params* params,
+                                        size_t* bytes);
+
+/* Validate shape and parameters and bind a device workspace of `bytes`
+ * bytes (256-byte aligned) to a new plan handle.  The handle owns only host
+ * metadata; the workspace remains the caller's.  Constraints
+ * (INVALID_ARGUMENT otherwise): batch, heads >= 1; n_q == n_kv >= 1;
+ * 0 <= n_dense_prefix < n_q; 1 <= C_k, C_q <= n_v; 1 <= r_k, r_q;
+ * 1 <= M_s; 0 <= M; 1 <= r <= d_v; 0 < rho <= 1; ridge >= 0; eps >= 0;
+ * stride_n >= d.  UNSUPPORTED: d != d_v, d not in {64, 128}, C_k or C_q
+ * above 8191, n_q above 2^24. */
+sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr_params* params,
+                                     void* workspace, size_t bytes, sparsepr_plan_t* out);
+
+/* Response-Coupled Partitioning, routing and probe choice for every head
+ * (Sec. 4.1, Sec. 4.3, App. A.2, App. B).  Reads Q and K only (values never
+ * enter the partition, App. B.1). */
+sparsepr_status sparsepr_plan(sparsepr_plan_t plan, const void* q, const void* k, void* stream);
+
+/* Sparse attention over the routed cells, exact probe rows, residual fit and
+ * correction (Sec. 4.2-4.3, App. A); writes the output [batch, heads, n, d_v]
+ * in the original row order.  Uses the plan made by the last sparsepr_plan or
+ * sparsepr_plan_import on this handle; `q`, `k` must be the tensors it was
+ * made from. */
+sparsepr_status sparsepr_attend(sparsepr_plan_t plan, const void* q, const void* k,
+                                const void* v, void* out, void* stream);
+
+/* Dense attention of Sec. 3 (eq. dense_attention) for every head, on the same
+ * kernels the probes use; for error reporting.  Needs no plan, allocates
+ * nothing; `workspace` must hold sparsepr_dense_workspace_size bytes. */
+sparsepr_status sparsepr_dense_workspace_size(const sparsepr_shape* shape, size_t* bytes);
+sparsepr_status sparsepr_dense_attend(const sparsepr_shape* shape, const void* q, const void* k,
+                                      const void* v, void* out, void* workspace, size_t bytes,
+                                      void* stream);
+
+/* Synchronise `stream` and read the realised accounting of the last call. */
+sparsepr_status sparsepr_get_stats(sparsepr_plan_t plan, sparsepr_stats* out, void* stream);
+
+/* Copy head `bh` (= b * heads + h) of the current plan (and, after attend,
+ * of its outputs) into caller host buffers.  Synchronises `stream`. */
+sparsepr_status sparsepr_plan_export(sparsepr_plan_t plan, int32_t bh, sparsepr_plan_host* out,
+                                     void* stream);
+
+/* Replace head `bh` of the plan by labels_q, labels_kv, routes and probes
+ * from host memory (all four required).  Group-major permutations, offsets,
+ * route lists and coverage weights are rebuilt on the device.  Errors:
+ * INVALID_ARGUMENT for out-of-range labels or probes. */
+sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const sparsepr_plan_host* in,
+                                     void* stream);
+
+/* Release the handle (not the workspace).  NULL is ignored. */
+void sparsepr_plan_destroy(sparsepr_plan_t plan);
+
+/* Text of the calling thread's most recent failure ("" if none); valid until
+ * that thread's next call into the library. */
+const char* sparsepr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPARSEPR_H */

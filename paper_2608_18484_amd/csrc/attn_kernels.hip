@@ -1,0 +1,869 @@
+// Attention-side kernels of the SparsePR operator for gfx950:
+//  * renormalised hard-drop block-sparse attention over the routed cells
+//    (Sec. 3 eq. hard_drop; Sec. 4.3), bf16 MFMA with fp32 accumulation, or
+//    an fp32 VALU variant;
+//  * exact probe rows against all keys (Sec. 4.3; App. A.2 eq.
+//    app_probe_residual), split over keys and merged by log-sum-exp;
+//  * the probe-fitted residual fit (Sec. 4.2; App. A.3) and the correction +
+//    restore to the original row order (eq. final_reconstructed_output).
+//
+// Layout of the bf16 attention kernel.  A block of 128 threads (2 waves)
+// owns up to 64 query rows of one query group; each wave owns 32 of them.
+// The scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
+// (A = 32 keys x 16 dims from LDS, B = 16 dims x 32 queries held in
+// registers), so every lane holds scores of ONE query and the online softmax
+// needs a single cross-lane exchange (lanes l and l+32).  The probabilities
+// stay in registers and feed O^T = V^T P^T directly as the B operand; V is
+// stored transposed in LDS with its keys permuted inside each 16-key chunk to
+// match the accumulator layout, so the A operand is one 16-byte LDS read.
+// K/V rows are gathered on load through the group-major permutation, so the
+// routed K/V groups are contiguous key ranges without a physical copy.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include <type_traits>
+
+#include "device_utils.hpp"
+#include "sparsepr_internal.hpp"
+
+namespace sparsepr {
+
+enum { MODE_SPARSE = 0, MODE_PROBE = 1, MODE_DENSE = 2 };
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;          // MODE_DENSE: user output tensor
+  float* osp;         // MODE_SPARSE: [BH][N][D] fp32
+  float* part;        // MODE_PROBE: [BH][M][nsplit][D+2]
+  const int4* chunks;
+  const int32_t* nchunks;
+  const int32_t* permq;
+  const int32_t* offq;
+  const int32_t* permk;
+  const int2* rng;
+  const int32_t* rng_cnt;
+  const int32_t* probes;
+  const int32_t* nprobes;
+};
+
+// Where the rows and keys of one block come from.
+struct Work1 {
+  int nrows;      // valid query rows (<= 64)
+  int nkeys;      // keys in the flat key list
+  int k0;         // MODE_PROBE/DENSE: first key row
+  int a;          // MODE_SPARSE: query group
+  int rbase;      // MODE_SPARSE: first permutation slot of the rows
+  int split;      // MODE_PROBE: split index
+  int tile;       // MODE_PROBE/DENSE: row tile
+};
+
+template <int MODE>
+__device__ __forceinline__ bool get_work(const Geom& g, const AttnArgs& A, int bh, Work1& w) {
+  if (MODE == MODE_SPARSE) {
+    const int cx = blockIdx.x;
+    if (cx >= A.nchunks[bh]) return false;
+    const int4 c = A.chunks[(size_t)bh * g.nchunk_max + cx];
+    w.a = c.x;
+    w.rbase = A.offq[(size_t)bh * (g.CQt + 1) + c.x] + c.y;
+    w.nrows = c.z;
+    w.nkeys = c.w;
+    w.k0 = 0;
+    return w.nrows > 0 && w.nkeys > 0;
+  } else if (MODE == MODE_PROBE) {
+    const int np = A.nprobes[bh];
+    w.tile = blockIdx.x;
+    w.split = blockIdx.y;
+    if (w.tile * 64 >= np) return false;
+    w.nrows = min(64, np - w.tile * 64);
+    w.k0 = w.split * kProbeSplit;
+    w.nkeys = min(g.N - w.k0, kProbeSplit);
+    return w.nkeys > 0;
+  } else {
+    w.tile = blockIdx.x;
+    w.nrows = min(64, g.N - w.tile * 64);
+    w.k0 = 0;
+    w.nkeys = g.N;
+    return w.nrows > 0;
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ int row_of(const Geom& g, const AttnArgs& A, int bh, const Work1& w,
+                                      int r) {
+  if (MODE == MODE_SPARSE) return A.permq[(size_t)bh * g.N + w.rbase + r];
+  if (MODE == MODE_PROBE) return A.probes[(size_t)bh * g.M + w.tile * 64 + r];
+  return w.tile * 64 + r;
+}
+
+// Source row of flat key f (f < nkeys).  MODE_SPARSE walks the routed ranges
+// with a per-thread cursor that only moves forward.
+struct KeyCursor {
+  int j, cum;
+};
+
+template <int MODE>
+__device__ __forceinline__ int key_row(const Geom& g, const AttnArgs& A, int bh, const Work1& w,
+                                       int f, KeyCursor& cur, const int2* rg, int nr) {
+  if (MODE != MODE_SPARSE) return w.k0 + f;
+  while (cur.j < nr && f >= cur.cum + rg[cur.j].y) {
+    cur.cum += rg[cur.j].y;
+    ++cur.j;
+  }
+  return A.permk[(size_t)bh * g.N + rg[cur.j].x + (f - cur.cum)];
+}
+
+// Slot of key k (0..15) inside its 16-key chunk of the transposed V tile:
+// the accumulator of a 32x32 MFMA holds keys (i/4)*8 + h*4 + i%4 in lane half
+// h, register i; registers 0..7 of half h become operand slots h*8 + 0..7.
+__device__ __forceinline__ int vslot(int k) { return ((k >> 2) & 1) * 8 + (k >> 3) * 4 + (k & 3); }
+
+template <int D, int MODE>
+__global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
+  constexpr int KT = 64;
+  constexpr int KLD = D + 8;   // K tile row stride (bf16 elements)
+  constexpr int VLD = KT + 8;  // V^T tile row stride
+  constexpr int NKS = D / 16;  // k-steps of the QK^T contraction
+  constexpr int NDB = D / 32;  // 32-wide output blocks of O^T
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KLD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VLD];
+  __shared__ int srcrow[KT];
+  const int bh = (MODE == MODE_PROBE) ? blockIdx.z : blockIdx.y;
+  Work1 w;
+  if (!get_work<MODE>(g, A, bh, w)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const int64_t base = head_base(g, bh);
+  const uint16_t* Kp = (const uint16_t*)A.k + base;
+  const uint16_t* Vp = (const uint16_t*)A.v + base;
+  const uint16_t* Qp = (const uint16_t*)A.q + base;
+
+  // this lane's query row and its B operands (16 dims per k-step)
+  const int qr = wv * 32 + n;
+  const bool qvalid = qr < w.nrows;
+  const int qrow = qvalid ? row_of<MODE>(g, A, bh, w, qr) : 0;
+  bf16x8 qreg[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    uint4 u = make_uint4(0, 0, 0, 0);
+    if (qvalid) u = *(const uint4*)(Qp + (int64_t)qrow * g.sn + ks * 16 + h * 8);
+    qreg[ks] = __builtin_bit_cast(bf16x8, u);
+  }
+  const bool wave_active = wv * 32 < w.nrows;
+
+  const int2* rg = nullptr;
+  int nr = 0;
+  if (MODE == MODE_SPARSE) {
+    rg = A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt;
+    nr = A.rng_cnt[(size_t)bh * g.CQt + w.a];
+  }
+  KeyCursor cur{0, 0};
+
+  const float sl2 = 1.4426950408889634f / sqrtf((float)D);
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 O[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) O[db][i] = 0.f;
+
+  const int ntile = (w.nkeys + KT - 1) / KT;
+  for (int t = 0; t < ntile; ++t) {
+    if (tid < KT) {
+      const int f = t * KT + tid;
+      srcrow[tid] = (f < w.nkeys) ? key_row<MODE>(g, A, bh, w, f, cur, rg, nr) : -1;
+    }
+    __syncthreads();
+    // K tile: 16-byte pieces, rows contiguous across lanes
+#pragma unroll
+    for (int u = 0; u < KT * D / 8 / 128; ++u) {
+      const int p = tid + 128 * u;
+      const int row = p / (D / 8), c8 = p % (D / 8);
+      const int src = srcrow[row];
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (src >= 0) val = *(const uint4*)(Kp + (int64_t)src * g.sn + c8 * 8);
+      *(uint4*)(Ks + row * KLD + c8 * 8) = val;
+    }
+    // V tile, transposed: a thread takes two adjacent keys (same 16-key chunk
+    // slots s, s+1) and 8 dims, and stores 8 packed key pairs
+#pragma unroll
+    for (int u = 0; u < KT * D / 16 / 128; ++u) {
+      const int p = tid + 128 * u;
+      const int pp = p % (KT / 2), c8 = p / (KT / 2);
+      const int k0 = 2 * pp;
+      const int s0 = srcrow[k0], s1 = srcrow[k0 + 1];
+      uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+      if (s0 >= 0) v0 = *(const uint4*)(Vp + (int64_t)s0 * g.sn + c8 * 8);
+      if (s1 >= 0) v1 = *(const uint4*)(Vp + (int64_t)s1 * g.sn + c8 * 8);
+      const int pos = (k0 & ~15) + vslot(k0 & 15);
+      const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
+      const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t lo = (a0[e] & 0xffffu) | (a1[e] << 16);
+        const uint32_t hi = (a0[e] >> 16) | (a1[e] & 0xffff0000u);
+        *(uint32_t*)(Vt + (c8 * 8 + 2 * e) * VLD + pos) = lo;
+        *(uint32_t*)(Vt + (c8 * 8 + 2 * e + 1) * VLD + pos) = hi;
+      }
+    }
+    __syncthreads();
+    if (wave_active) {
+      // S^T for 64 keys x 32 queries: two 32-key blocks
+      f32x16 S[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) S[kb][i] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          const bf16x8 av =
+              __builtin_bit_cast(bf16x8, *(const uint4*)(Ks + (kb * 32 + n) * KLD + ks * 16 + h * 8));
+          S[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], S[kb], 0, 0, 0);
+        }
+      }
+      // online softmax (base 2); key of register i: kb*32 + (i/4)*8 + h*4 + i%4
+      const bool tail = (t + 1) * KT > w.nkeys;
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float s = S[kb][i] * sl2;
+          if (tail) {
+            const int key = t * KT + kb * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
+            if (key >= w.nkeys) s = -INFINITY;
+          }
+          S[kb][i] = s;
+          mt = fmaxf(mt, s);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      float ls = 0.f;
+      bf16x8 P[4];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float p = __builtin_amdgcn_exp2f(S[kb][hh * 8 + e] - m_new);
+            ls += p;
+            P[kb * 2 + hh][e] = (__bf16)p;
+          }
+      l_run = l_run * alpha + ls;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) O[db][i] *= alpha;
+      // O^T += V^T P^T over four 16-key chunks
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const bf16x8 av =
+              __builtin_bit_cast(bf16x8, *(const uint4*)(Vt + (db * 32 + n) * VLD + c * 16 + h * 8));
+          O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, P[c], O[db], 0, 0, 0);
+        }
+    }
+    __syncthreads();
+  }
+  if (!qvalid) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (MODE == MODE_PROBE) {
+    float* dst = A.part + (((size_t)bh * g.M + w.tile * 64 + qr) * g.nsplit + w.split) * (D + 2);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int dv = db * 32 + i4 * 8 + h * 4;
+        *(float4*)(dst + dv) =
+            make_float4(O[db][i4 * 4], O[db][i4 * 4 + 1], O[db][i4 * 4 + 2], O[db][i4 * 4 + 3]);
+      }
+    if (h == 0) {
+      dst[D] = m_run;
+      dst[D + 1] = l_tot;
+    }
+  } else {
+    const float inv = 1.f / l_tot;
+    if (MODE == MODE_SPARSE) {
+      float* dst = A.osp + ((size_t)bh * g.N + qrow) * D;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int dv = db * 32 + i4 * 8 + h * 4;
+          *(float4*)(dst + dv) = make_float4(O[db][i4 * 4] * inv, O[db][i4 * 4 + 1] * inv,
+                                             O[db][i4 * 4 + 2] * inv, O[db][i4 * 4 + 3] * inv);
+        }
+    } else {
+      uint16_t* dst = (uint16_t*)A.out + base + (int64_t)qrow * g.sn;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int dv = db * 32 + i4 * 8 + h * 4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const __bf16 b = (__bf16)(O[db][i4 * 4 + e] * inv);
+            dst[dv + e] = __builtin_bit_cast(uint16_t, b);
+          }
+        }
+    }
+  }
+}
+
+// fp32 variant (VALU): one thread per query row, 32-key tiles staged in LDS.
+template <int D, int MODE>
+__global__ __launch_bounds__(64) void k_attn_f32(Geom g, AttnArgs A) {
+  constexpr int KT = 32;
+  __shared__ float Ks[KT][D + 1];
+  __shared__ float Vs[KT][D + 1];
+  __shared__ int srcrow[KT];
+  const int bh = (MODE == MODE_PROBE) ? blockIdx.z : blockIdx.y;
+  Work1 w;
+  if (!get_work<MODE>(g, A, bh, w)) return;
+  const int tid = threadIdx.x;
+  const int64_t base = head_base(g, bh);
+  const float* Kp = (const float*)A.k + base;
+  const float* Vp = (const float*)A.v + base;
+  const float* Qp = (const float*)A.q + base;
+  const bool qvalid = tid < w.nrows;
+  const int qrow = qvalid ? row_of<MODE>(g, A, bh, w, tid) : 0;
+  float qv[D], o[D];
+#pragma unroll
+  for (int c = 0; c < D; ++c) {
+    qv[c] = qvalid ? Qp[(int64_t)qrow * g.sn + c] : 0.f;
+    o[c] = 0.f;
+  }
+  const int2* rg = nullptr;
+  int nr = 0;
+  if (MODE == MODE_SPARSE) {
+    rg = A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt;
+    nr = A.rng_cnt[(size_t)bh * g.CQt + w.a];
+  }
+  KeyCursor cur{0, 0};
+  const float scale = 1.f / sqrtf((float)D);
+  const float l2e = 1.4426950408889634f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const int ntile = (w.nkeys + KT - 1) / KT;
+  for (int t = 0; t < ntile; ++t) {
+    if (tid < KT) {
+      const int f = t * KT + tid;
+      srcrow[tid] = (f < w.nkeys) ? key_row<MODE>(g, A, bh, w, f, cur, rg, nr) : -1;
+    }
+    __syncthreads();
+    for (int i = tid; i < KT * D; i += 64) {
+      const int r = i / D, c = i % D;
+      const int src = srcrow[r];
+      Ks[r][c] = src >= 0 ? Kp[(int64_t)src * g.sn + c] : 0.f;
+      Vs[r][c] = src >= 0 ? Vp[(int64_t)src * g.sn + c] : 0.f;
+    }
+    __syncthreads();
+    const int kn = min(KT, w.nkeys - t * KT);
+    float s[KT];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      float acc = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc = fmaf(qv[c], Ks[j][c], acc);
+      s[j] = (j < kn) ? acc * scale * l2e : -INFINITY;
+      mt = fmaxf(mt, s[j]);
+    }
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int c = 0; c < D; ++c) o[c] *= alpha;
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      const float p = exp2f(s[j] - m_new);
+      l_run += p;
+#pragma unroll
+      for (int c = 0; c < D; ++c) o[c] = fmaf(p, Vs[j][c], o[c]);
+    }
+    __syncthreads();
+  }
+  if (!qvalid) return;
+  if (MODE == MODE_PROBE) {
+    float* dst = A.part + (((size_t)bh * g.M + w.tile * 64 + tid) * g.nsplit + w.split) * (D + 2);
+    for (int c = 0; c < D; ++c) dst[c] = o[c];
+    dst[D] = m_run;
+    dst[D + 1] = l_run;
+  } else if (MODE == MODE_SPARSE) {
+    float* dst = A.osp + ((size_t)bh * g.N + qrow) * D;
+    for (int c = 0; c < D; ++c) dst[c] = o[c] / l_run;
+  } else {
+    float* dst = (float*)A.out + base + (int64_t)qrow * g.sn;
+    for (int c = 0; c < D; ++c) dst[c] = o[c] / l_run;
+  }
+}
+
+// Merge the key splits of the probe rows: O = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
+__global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
+                                                     const int32_t* nprobes, float* odp) {
+  const int p = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  if (p >= nprobes[bh] || c >= g.dv) return;
+  const int D = g.dv;
+  const float* src = part + ((size_t)bh * g.M + p) * g.nsplit * (D + 2);
+  float m = -INFINITY;
+  for (int s = 0; s < g.nsplit; ++s) m = fmaxf(m, src[(size_t)s * (D + 2) + D]);
+  float l = 0.f, o = 0.f;
+  for (int s = 0; s < g.nsplit; ++s) {
+    const float* e = src + (size_t)s * (D + 2);
+    const float f = exp2f(e[D] - m);
+    l += e[D + 1] * f;
+    o += e[c] * f;
+  }
+  odp[((size_t)bh * g.M + p) * D + c] = o / l;
+}
+
+// ---------------------------------------------------------------------------
+// Probe-fitted residual fit (Sec. 4.2; App. A.3), one block of 1024 threads
+// per head:
+//   alpha_p = w_p / sum w;  mu_x, mu_R weighted means;
+//   s_x = sqrt(sum alpha (x - mu_x)^2 + eps);  xbar = (x - mu_x)/s_x;
+//   Rbar = R - mu_R;  w~_p = M w_p / sum w;
+//   Psi = leading r eigenvectors of Rbar^T W Rbar (right singular vectors of
+//         W^1/2 Rbar), keeping sigma > 1e-6 sigma_1;
+//   (xbar^T W xbar + lambda I) Y = xbar^T W (Rbar Psi)   (Cholesky),
+// so Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
+// ---------------------------------------------------------------------------
+
+template <int D, typename T>
+__device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag);
+
+template <int D>
+__global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
+  using T = typename std::conditional<D <= 64, double, float>::type;
+  constexpr int LD = D + 1;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * D * LD * sizeof(T)];
+  __shared__ T rc[D / 2], rs[D / 2];
+  __shared__ int order[D];
+  __shared__ double red[2];
+  __shared__ int flag, rank_s, fail;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int np = w.nprobes[bh];
+  const int r = g.r;
+  float* fv = w.fitv + (size_t)bh * 3 * D;
+  float* Y = w.fity + (size_t)bh * D * r;
+  float* Psi = w.fitpsi + (size_t)bh * D * r;
+  double* xb = w.fitscr + (size_t)bh * ((size_t)2 * g.M * D + (size_t)g.M * r + (size_t)D * r);  // [M][D]
+  double* rb = xb + (size_t)g.M * D;                            // [M][D]
+  double* rp = rb + (size_t)g.M * D;                            // [M][r]   Rbar Psi
+  double* rhs = rp + (size_t)g.M * r;                           // [D][r]
+  for (int i = tid; i < D * r; i += 1024) {
+    Y[i] = 0.f;
+    Psi[i] = 0.f;
+  }
+  if (np == 0) {
+    for (int c = tid; c < D; c += 1024) {
+      fv[c] = 0.f;
+      fv[D + c] = 1.f;
+      fv[2 * D + c] = 0.f;
+    }
+    if (tid == 0) w.stats[(size_t)bh * 16 + ST_FIT_RANK] = 0;
+    return;
+  }
+  const int32_t* pr = w.probes + (size_t)bh * g.M;
+  const float* pwt = w.pw + (size_t)bh * g.M;
+  const float* osp = w.osp + (size_t)bh * g.N * D;
+  const float* odp = w.odp + (size_t)bh * g.M * D;
+  if (tid == 0) {
+    double s = 0.0;
+    for (int p = 0; p < np; ++p) s += (double)pwt[p];
+    red[0] = s;
+  }
+  __syncthreads();
+  const double sw = red[0];
+  // weighted statistics, one thread per output dimension
+  if (tid < D) {
+    const int c = tid;
+    double mx = 0.0, mr = 0.0;
+    for (int p = 0; p < np; ++p) {
+      const double al = (double)pwt[p] / sw;
+      const double x = osp[(size_t)pr[p] * D + c];
+      mx += al * x;
+      mr += al * ((double)odp[(size_t)p * D + c] - x);
+    }
+    double vx = 0.0;
+    for (int p = 0; p < np; ++p) {
+      const double al = (double)pwt[p] / sw;
+      const double t = (double)osp[(size_t)pr[p] * D + c] - mx;
+      vx += al * t * t;
+    }
+    const double sx = sqrt(vx + (double)g.eps_x);
+    for (int p = 0; p < np; ++p) {
+      const double x = osp[(size_t)pr[p] * D + c];
+      xb[(size_t)p * D + c] = (x - mx) / sx;
+      rb[(size_t)p * D + c] = ((double)odp[(size_t)p * D + c] - x) - mr;
+    }
+    fv[c] = (float)mx;
+    fv[D + c] = (float)sx;
+    fv[2 * D + c] = (float)mr;
+  }
+  __syncthreads();
+  // H = Rbar^T W Rbar into the Jacobi matrix
+  T* Am = (T*)smem;
+  T* Vm = Am + D * LD;
+  const double wscale = (double)np / sw;
+  for (int e = tid; e < D * D; e += 1024) {
+    const int i = e / D, j = e % D;
+    double acc = 0.0;
+    for (int p = 0; p < np; ++p) acc += wscale * (double)pwt[p] * rb[(size_t)p * D + i] * rb[(size_t)p * D + j];
+    Am[i * LD + j] = (T)acc;
+  }
+  __syncthreads();
+  jacobi_eig_lds_fit<D, T>(Am, Vm, rc, rs, &flag);
+  if (tid < D) {
+    const T li = Am[tid * LD + tid];
+    int rank = 0;
+    for (int j = 0; j < D; ++j) {
+      const T lj = Am[j * LD + j];
+      rank += (lj > li) || (lj == li && j < tid);
+    }
+    order[rank] = tid;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const double l1 = Am[order[0] * LD + order[0]];
+    const double s1 = l1 > 0.0 ? sqrt(l1) : 0.0;
+    int rk = 0;
+    for (int t = 0; t < r && t < D; ++t) {
+      const double lt = Am[order[t] * LD + order[t]];
+      const double st = lt > 0.0 ? sqrt(lt) : 0.0;
+      if (s1 > 0.0 && st > 1e-6 * s1)
+        ++rk;
+      else
+        break;
+    }
+    rank_s = rk;
+    fail = 0;
+  }
+  __syncthreads();
+  const int rk = rank_s;
+  for (int i = tid; i < D * rk; i += 1024) {
+    const int row = i / rk, t = i % rk;
+    Psi[row * r + t] = (float)Vm[row * LD + order[t]];
+  }
+  __syncthreads();
+  // Rbar Psi (M x rk) and rhs = xbar^T W (Rbar Psi) (D x rk)
+  for (int i = tid; i < np * rk; i += 1024) {
+    const int p = i / rk, t = i % rk;
+    double acc = 0.0;
+    for (int c = 0; c < D; ++c) acc += rb[(size_t)p * D + c] * (double)Vm[c * LD + order[t]];
+    rp[(size_t)p * r + t] = acc;
+  }
+  __syncthreads();
+  for (int i = tid; i < D * rk; i += 1024) {
+    const int c = i / rk, t = i % rk;
+    double acc = 0.0;
+    for (int p = 0; p < np; ++p)
+      acc += wscale * (double)pwt[p] * xb[(size_t)p * D + c] * rp[(size_t)p * r + t];
+    rhs[(size_t)c * r + t] = acc;
+  }
+  // S = xbar^T W xbar + lambda I in LDS (double), then Cholesky S = L L^T
+  double* S = (double*)smem;
+  __syncthreads();
+  for (int e = tid; e < D * D; e += 1024) {
+    const int i = e / D, j = e % D;
+    double acc = 0.0;
+    for (int p = 0; p < np; ++p) acc += wscale * (double)pwt[p] * xb[(size_t)p * D + i] * xb[(size_t)p * D + j];
+    S[i * D + j] = acc + (i == j ? (double)g.ridge : 0.0);
+  }
+  __syncthreads();
+  for (int j = 0; j < D; ++j) {
+    if (tid == 0) {
+      const double dj = S[j * D + j];
+      if (!(dj > 0.0)) fail = 1;
+      S[j * D + j] = dj > 0.0 ? sqrt(dj) : 1.0;
+    }
+    __syncthreads();
+    const double ljj = S[j * D + j];
+    for (int i = j + 1 + tid; i < D; i += 1024) S[i * D + j] /= ljj;
+    __syncthreads();
+    const int rem = D - j - 1;
+    for (int e = tid; e < rem * rem; e += 1024) {
+      const int i = j + 1 + e / rem, k = j + 1 + e % rem;
+      if (k <= i) S[i * D + k] -= S[i * D + j] * S[k * D + j];
+    }
+    __syncthreads();
+  }
+  // L L^T Y = rhs, one right-hand side per thread
+  if (tid < rk && !fail) {
+    const int t = tid;
+    for (int i = 0; i < D; ++i) {
+      double acc = rhs[(size_t)i * r + t];
+      for (int k = 0; k < i; ++k) acc -= S[i * D + k] * rhs[(size_t)k * r + t];
+      rhs[(size_t)i * r + t] = acc / S[i * D + i];
+    }
+    for (int i = D - 1; i >= 0; --i) {
+      double acc = rhs[(size_t)i * r + t];
+      for (int k = i + 1; k < D; ++k) acc -= S[k * D + i] * rhs[(size_t)k * r + t];
+      rhs[(size_t)i * r + t] = acc / S[i * D + i];
+    }
+    for (int i = 0; i < D; ++i) Y[i * r + t] = (float)rhs[(size_t)i * r + t];
+  }
+  if (tid == 0) {
+    int64_t* st = w.stats + (size_t)bh * 16;
+    st[ST_FIT_RANK] = rk;
+    if (fail) st[ST_FLAGS] |= SPARSEPR_FLAG_FIT_NOT_PD;
+  }
+}
+
+// Correction and restore (eq. probe_residual_estimate and
+// final_reconstructed_output): out_i = x_i + mu_R + ((x_i - mu_x)/s_x) Y Psi^T
+// for the video rows; dense-prefix rows keep their (exact) sparse output.
+// Probe rows are overwritten afterwards by k_probe_scatter.
+template <int D>
+__global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
+  constexpr int ROWS = 64;
+  __shared__ float xs[ROWS][D + 1];
+  __shared__ float ts[ROWS][33];
+  __shared__ float fy[D][33], fp[D][33];
+  __shared__ float mux[D], sx[D], mur[D];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int r0 = blockIdx.x * ROWS;
+  const int r = g.r;
+  const int rr = min(r, 32);
+  const float* fv = w.fitv + (size_t)bh * 3 * D;
+  for (int c = tid; c < D; c += 256) {
+    mux[c] = fv[c];
+    sx[c] = fv[D + c];
+    mur[c] = fv[2 * D + c];
+  }
+  const float* Y = w.fity + (size_t)bh * D * r;
+  const float* Psi = w.fitpsi + (size_t)bh * D * r;
+  const float* osp = w.osp + (size_t)bh * g.N * D;
+  for (int i = tid; i < ROWS * D; i += 256) {
+    const int rr2 = i / D, c = i % D;
+    const int row = r0 + rr2;
+    xs[rr2][c] = row < g.N ? osp[(size_t)row * D + c] : 0.f;
+  }
+  __syncthreads();
+  const int64_t base = head_base(g, bh);
+  // the residual rank is processed in slices of up to 32 directions
+  float accs[ROWS * D / 256];
+#pragma unroll
+  for (int u = 0; u < ROWS * D / 256; ++u) accs[u] = 0.f;
+  for (int t0 = 0; t0 < r; t0 += 32) {
+    const int tn = min(32, r - t0);
+    __syncthreads();
+    for (int i = tid; i < D * tn; i += 256) {
+      const int c = i / tn, t = i % tn;
+      fy[c][t] = Y[c * r + t0 + t];
+      fp[c][t] = Psi[c * r + t0 + t];
+    }
+    __syncthreads();
+    for (int i = tid; i < ROWS * tn; i += 256) {
+      const int rw = i / tn, t = i % tn;
+      float acc = 0.f;
+      for (int c = 0; c < D; ++c) acc = fmaf((xs[rw][c] - mux[c]) / sx[c], fy[c][t], acc);
+      ts[rw][t] = acc;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < ROWS * D / 256; ++u) {
+      const int i = tid + 256 * u;
+      const int rw = i / D, c = i % D;
+      float acc = accs[u];
+      for (int t = 0; t < tn; ++t) acc = fmaf(ts[rw][t], fp[c][t], acc);
+      accs[u] = acc;
+    }
+  }
+  (void)rr;
+#pragma unroll
+  for (int u = 0; u < ROWS * D / 256; ++u) {
+    const int i = tid + 256 * u;
+    const int rw = i / D, c = i % D;
+    const int row = r0 + rw;
+    if (row >= g.N) continue;
+    const float x = xs[rw][c];
+    const float v = (row < g.ntext) ? x : x + mur[c] + accs[u];
+    const int64_t idx = base + (int64_t)row * g.sn + c;
+    if (g.bf16) {
+      const __bf16 b = (__bf16)v;
+      ((uint16_t*)out)[idx] = __builtin_bit_cast(uint16_t, b);
+    } else {
+      ((float*)out)[idx] = v;
+    }
+  }
+}
+
+// Probe rows take their exact dense rows (eq. final_reconstructed_output).
+__global__ __launch_bounds__(128) void k_probe_scatter(Geom g, Work w, void* out) {
+  const int p = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  if (p >= w.nprobes[bh] || c >= g.dv) return;
+  const int row = w.probes[(size_t)bh * g.M + p];
+  const float v = w.odp[((size_t)bh * g.M + p) * g.dv + c];
+  const int64_t idx = head_base(g, bh) + (int64_t)row * g.sn + c;
+  if (g.bf16) {
+    const __bf16 b = (__bf16)v;
+    ((uint16_t*)out)[idx] = __builtin_bit_cast(uint16_t, b);
+  } else {
+    ((float*)out)[idx] = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Jacobi eigensolver for the fit (same method as the planner's, duplicated
+// here so each translation unit stands alone).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void rr_pair2(int step, int i, int n, int& p, int& q) {
+  if (i == 0) {
+    p = step;
+    q = n - 1;
+  } else {
+    p = (step + i) % (n - 1);
+    q = (step - i + n - 1) % (n - 1);
+  }
+}
+
+template <int D, typename T>
+__device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
+  constexpr int LD = D + 1, P = D / 2;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int i = tid; i < D * D; i += nt) {
+    const int rr = i / D, c = i % D;
+    V[rr * LD + c] = (rr == c) ? T(1) : T(0);
+  }
+  __syncthreads();
+  for (int sweep = 0; sweep < 20; ++sweep) {
+    if (tid == 0) *flag = 0;
+    __syncthreads();
+    for (int step = 0; step < D - 1; ++step) {
+      if (tid < P) {
+        int p, q;
+        rr_pair2(step, tid, D, p, q);
+        const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
+        T c = 1, s = 0;
+        const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
+        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
+          const T theta = (aqq - app) / (T(2) * apq);
+          const T at = fabs(theta);
+          const T t = (at > T(1e10)) ? T(0.5) / theta
+                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
+          c = T(1) / sqrt(t * t + T(1));
+          s = t * c;
+          *flag = 1;
+        }
+        rc[tid] = c;
+        rs[tid] = s;
+      }
+      __syncthreads();
+      for (int idx = tid; idx < P * P; idx += nt) {
+        const int i = idx / P, j = idx % P;
+        const T si = rs[i], sj = rs[j];
+        if (si == T(0) && sj == T(0)) continue;
+        const T ci = rc[i], cj = rc[j];
+        int p, q, p2, q2;
+        rr_pair2(step, i, D, p, q);
+        rr_pair2(step, j, D, p2, q2);
+        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
+        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
+        const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
+        const T y10 = x10 * cj - x11 * sj, y11 = x10 * sj + x11 * cj;
+        T z00 = ci * y00 - si * y10, z01 = ci * y01 - si * y11;
+        T z10 = si * y00 + ci * y10, z11 = si * y01 + ci * y11;
+        if (i == j) z01 = z10 = T(0);
+        A[p * LD + p2] = z00;
+        A[p * LD + q2] = z01;
+        A[q * LD + p2] = z10;
+        A[q * LD + q2] = z11;
+      }
+      for (int idx = tid; idx < D * P; idx += nt) {
+        const int row = idx / P, j = idx % P;
+        const T sj = rs[j];
+        if (sj == T(0)) continue;
+        const T cj = rc[j];
+        int p, q;
+        rr_pair2(step, j, D, p, q);
+        const T vp = V[row * LD + p], vq = V[row * LD + q];
+        V[row * LD + p] = cj * vp - sj * vq;
+        V[row * LD + q] = sj * vp + cj * vq;
+      }
+      __syncthreads();
+    }
+    const int more = *flag;
+    __syncthreads();
+    if (!more) break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host launchers
+// ---------------------------------------------------------------------------
+
+static AttnArgs make_args(const Work* w, const void* q, const void* k, const void* v, void* out) {
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  if (w) {
+    a.osp = w->osp;
+    a.part = w->part;
+    a.chunks = w->chunks;
+    a.nchunks = w->nchunks;
+    a.permq = w->permq;
+    a.offq = w->offq;
+    a.permk = w->permk;
+    a.rng = w->rng;
+    a.rng_cnt = w->rng_cnt;
+    a.probes = w->probes;
+    a.nprobes = w->nprobes;
+  }
+  return a;
+}
+
+template <int D>
+static void attend_d(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+                     void* out, hipStream_t s) {
+  const AttnArgs a = make_args(&w, q, k, v, out);
+  const dim3 gs(g.nchunk_max, g.BH);
+  const dim3 gp((g.M + 63) / 64, g.nsplit, g.BH);
+  if (g.bf16) {
+    k_attn_bf16<D, MODE_SPARSE><<<gs, 128, 0, s>>>(g, a);
+    if (g.M > 0) k_attn_bf16<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
+  } else {
+    k_attn_f32<D, MODE_SPARSE><<<gs, 64, 0, s>>>(g, a);
+    if (g.M > 0) k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(g, a);
+  }
+  if (g.M > 0) k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
+  k_fit<D><<<g.BH, 1024, 0, s>>>(g, w);
+  k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(g, w, out);
+  if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w, out);
+}
+
+void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+                   void* out, hipStream_t s) {
+  if (g.d == 64)
+    attend_d<64>(g, w, q, k, v, out, s);
+  else
+    attend_d<128>(g, w, q, k, v, out, s);
+}
+
+void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
+                  float* part, hipStream_t s) {
+  (void)part;
+  const AttnArgs a = make_args(nullptr, q, k, v, out);
+  const dim3 gd((g.N + 63) / 64, g.BH);
+  if (g.d == 64) {
+    if (g.bf16)
+      k_attn_bf16<64, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
+    else
+      k_attn_f32<64, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
+  } else {
+    if (g.bf16)
+      k_attn_bf16<128, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
+    else
+      k_attn_f32<128, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
+  }
+}
+
+}  // namespace sparsepr

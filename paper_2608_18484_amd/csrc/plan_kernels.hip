@@ -1,0 +1,1144 @@
+// Planner kernels of the SparsePR operator for gfx950: Response-Coupled
+// Partitioning (Sec. 4.1, App. B), budgeted shared block routing (Sec. 4.3)
+// and query-group-stratified probe selection (App. A.2).
+//
+// Decisions that must be reproducible bit for bit (k-means labels, group
+// order, route set, probe set) are taken on float values computed in a fixed
+// operation order, with the lowest index winning ties:
+//  * k-means score of point x and centroid c: t = fmaf chain of x_k c_k over
+//    k in index order, u = fmaf chain of c_k c_k, score = fmaf(-2, t, u);
+//  * centroids: double sums over members in ascending row order / count;
+//  * probe radial key: fmaf chain of (phi_k - c_k)^2 in index order.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "device_utils.hpp"
+#include "sparsepr_internal.hpp"
+
+namespace sparsepr {
+
+// ---------------------------------------------------------------------------
+// Per-call initialisation
+// ---------------------------------------------------------------------------
+
+__global__ void k_plan_init(Geom g, Work w) {
+  const int bh = blockIdx.x;
+  for (int i = threadIdx.x; i < 16; i += blockDim.x) w.stats[bh * 16 + i] = 0;
+  for (int i = threadIdx.x; i < 2 * (g.T + 1); i += blockDim.x)
+    w.kmstate[bh * 2 * (g.T + 1) + i] = (i % (g.T + 1) == 0) ? 1 : 0;
+}
+
+// ---------------------------------------------------------------------------
+// Key-response metric M_K = Q_s^T Q_s / M_s over the strided query sample
+// s_i = floor(i * n_v / M_s) (Sec. 4.1; App. B.1 eq. app_key_metric).
+// ---------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, double* gram) {
+  constexpr int ENT = D * D / 256;
+  constexpr int SB = 32;
+  __shared__ float qs[SB][D];
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int64_t base = head_base(g, bh);
+  const int e0 = tid * ENT, ra = e0 / D, cb = e0 % D;
+  double acc[ENT];
+#pragma unroll
+  for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
+  for (int s0 = 0; s0 < g.Ms; s0 += SB) {
+    for (int t = tid; t < SB * D; t += 256) {
+      const int i = s0 + t / D, c = t % D;
+      float v = 0.f;
+      if (i < g.Ms) {
+        const int64_t row = g.ntext + ((int64_t)i * g.NV) / g.Ms;
+        v = load_x(q, g.bf16, base + row * g.sn + c);
+      }
+      qs[t / D][c] = v;
+    }
+    __syncthreads();
+    const int cnt = min(SB, g.Ms - s0);
+    for (int i = 0; i < cnt; ++i) {
+      const double a = qs[i][ra];
+#pragma unroll
+      for (int e = 0; e < ENT; ++e) acc[e] += a * (double)qs[i][cb + e];
+    }
+    __syncthreads();
+  }
+  double* out = gram + (size_t)bh * D * D;
+#pragma unroll
+  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / (double)g.Ms;
+}
+
+// ---------------------------------------------------------------------------
+// Symmetric eigensolver: parallel cyclic Jacobi in LDS, one block of 1024
+// threads per matrix (double for d = 64, float for d = 128, whose two d x d
+// matrices would not fit in LDS in double).  Each step applies D/2 disjoint rotations chosen by
+// the round-robin (circle) ordering; A <- J^T A J on 2x2 blocks, V <- V J.
+// On return the eigenvalues are on A's diagonal and V's columns hold the
+// eigenvectors.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void rr_pair(int step, int i, int n, int& p, int& q) {
+  if (i == 0) {
+    p = step;
+    q = n - 1;
+  } else {
+    p = (step + i) % (n - 1);
+    q = (step - i + n - 1) % (n - 1);
+  }
+}
+
+template <int D, typename T>
+__device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
+  constexpr int LD = D + 1, P = D / 2;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int i = tid; i < D * D; i += nt) {
+    const int r = i / D, c = i % D;
+    V[r * LD + c] = (r == c) ? T(1) : T(0);
+  }
+  __syncthreads();
+  for (int sweep = 0; sweep < 20; ++sweep) {
+    if (tid == 0) *flag = 0;
+    __syncthreads();
+    for (int step = 0; step < D - 1; ++step) {
+      if (tid < P) {
+        int p, q;
+        rr_pair(step, tid, D, p, q);
+        const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
+        T c = 1, s = 0;
+        const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
+        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
+          const T theta = (aqq - app) / (T(2) * apq);
+          const T at = fabs(theta);
+          const T t = (at > T(1e10)) ? T(0.5) / theta
+                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
+          c = T(1) / sqrt(t * t + T(1));
+          s = t * c;
+          *flag = 1;
+        }
+        rc[tid] = c;
+        rs[tid] = s;
+      }
+      __syncthreads();
+      for (int idx = tid; idx < P * P; idx += nt) {
+        const int i = idx / P, j = idx % P;
+        const T si = rs[i], sj = rs[j];
+        if (si == T(0) && sj == T(0)) continue;
+        const T ci = rc[i], cj = rc[j];
+        int p, q, p2, q2;
+        rr_pair(step, i, D, p, q);
+        rr_pair(step, j, D, p2, q2);
+        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
+        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
+        const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
+        const T y10 = x10 * cj - x11 * sj, y11 = x10 * sj + x11 * cj;
+        T z00 = ci * y00 - si * y10, z01 = ci * y01 - si * y11;
+        T z10 = si * y00 + ci * y10, z11 = si * y01 + ci * y11;
+        if (i == j) z01 = z10 = T(0);
+        A[p * LD + p2] = z00;
+        A[p * LD + q2] = z01;
+        A[q * LD + p2] = z10;
+        A[q * LD + q2] = z11;
+      }
+      for (int idx = tid; idx < D * P; idx += nt) {
+        const int row = idx / P, j = idx % P;
+        const T sj = rs[j];
+        if (sj == T(0)) continue;
+        const T cj = rc[j];
+        int p, q;
+        rr_pair(step, j, D, p, q);
+        const T vp = V[row * LD + p], vq = V[row * LD + q];
+        V[row * LD + p] = cj * vp - sj * vq;
+        V[row * LD + q] = sj * vp + cj * vq;
+      }
+      __syncthreads();
+    }
+    const int more = *flag;
+    __syncthreads();
+    if (!more) break;
+  }
+}
+
+// Sort the eigenvalues on A's diagonal in descending order (ties by index):
+// order[t] = index of the t-th largest.  Needs D threads.
+template <int D, typename T>
+__device__ void eig_order(const T* A, int* order) {
+  constexpr int LD = D + 1;
+  const int i = threadIdx.x;
+  if (i < D) {
+    const T li = A[i * LD + i];
+    int rank = 0;
+    for (int j = 0; j < D; ++j) {
+      const T lj = A[j * LD + j];
+      rank += (lj > li) || (lj == li && j < i);
+    }
+    order[rank] = i;
+  }
+  __syncthreads();
+}
+
+// Eigen-scaled response basis (Sec. 4.1; App. B.1, B.2): the leading r
+// eigendirections, each scaled by sqrt(lambda / mean of the r retained
+// lambdas); eigenvalues below tau * lambda_1 are clamped to 0 first.
+template <int D>
+__global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, float tau, float* F,
+                                                    float* evals) {
+  using T = typename std::conditional<D <= 64, double, float>::type;
+  constexpr int LD = D + 1;
+  __shared__ T A[D * LD];
+  __shared__ T V[D * LD];
+  __shared__ T rc[D / 2], rs[D / 2];
+  __shared__ int order[D];
+  __shared__ double lam[D];
+  __shared__ int flag;
+  __shared__ double meanv;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const double* G = gram + (size_t)bh * D * D;
+  for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
+  __syncthreads();
+  jacobi_eig_lds<D, T>(A, V, rc, rs, &flag);
+  eig_order<D, T>(A, order);
+  const double l1 = A[order[0] * LD + order[0]];
+  if (tid < D) {
+    const double l = A[order[tid] * LD + order[tid]];
+    lam[tid] = (l1 > 0.0 && l >= (double)tau * l1) ? l : 0.0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double s = 0.0;
+    for (int t = 0; t < r; ++t) s += lam[t];
+    meanv = s / r;
+  }
+  __syncthreads();
+  float* Fo = F + (size_t)bh * D * r;
+  for (int i = tid; i < D * r; i += blockDim.x) {
+    const int row = i / r, t = i % r;
+    const double wgt = meanv > 0.0 ? sqrt(lam[t] / meanv) : 0.0;
+    Fo[i] = (float)((double)V[row * LD + order[t]] * wgt);
+  }
+  if (tid < D) evals[(size_t)bh * D + tid] = (float)lam[tid];
+}
+
+// ---------------------------------------------------------------------------
+// Response coordinates phi = F^T x (eq. key_response_feature), optionally
+// divided by max(RMS, eps) (eq. query_response_feature).  64 rows per block,
+// four threads per row.
+// ---------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
+                                                 int rms, float eps, float* phi, int64_t* stats) {
+  constexpr int ROWS = 64, MAXC = 32;
+  __shared__ float xs[ROWS][D + 1];
+  __shared__ float fs[D * 128];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int r0 = blockIdx.x * ROWS;
+  const int64_t base = head_base(g, bh);
+  const float* Fh = F + (size_t)bh * D * R;
+  for (int i = tid; i < D * R; i += 256) fs[i] = Fh[i];
+  for (int i = tid; i < ROWS * D; i += 256) {
+    const int rr = i / D, c = i % D;
+    const int row = r0 + rr;
+    xs[rr][c] = (row < g.NV) ? load_x(x, g.bf16, base + (int64_t)(g.ntext + row) * g.sn + c) : 0.f;
+  }
+  __syncthreads();
+  const int rr = tid >> 2, part = tid & 3;
+  float acc[MAXC];
+#pragma unroll
+  for (int u = 0; u < MAXC; ++u) acc[u] = 0.f;
+  for (int k = 0; k < D; ++k) {
+    const float xk = xs[rr][k];
+#pragma unroll
+    for (int u = 0; u < MAXC; ++u) {
+      const int c = part + 4 * u;
+      if (c < R) acc[u] = fmaf(xk, fs[k * R + c], acc[u]);
+    }
+  }
+  float den = 1.f;
+  if (rms) {
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < MAXC; ++u)
+      if (part + 4 * u < R) ss = fmaf(acc[u], acc[u], ss);
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    den = fmaxf(sqrtf(ss / (float)R), eps);
+  }
+  const int row = r0 + rr;
+  if (row < g.NV) {
+    float* out = phi + ((size_t)bh * g.NV + row) * R;
+    bool bad = false;
+#pragma unroll
+    for (int u = 0; u < MAXC; ++u) {
+      const int c = part + 4 * u;
+      if (c < R) {
+        const float v = acc[u] / den;
+        bad |= !isfinite(v);
+        out[c] = v;
+      }
+    }
+    if (bad)
+      atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
+               (unsigned long long)SPARSEPR_FLAG_NONFINITE_INPUT);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k-means (Sec. 4.1: paired K/V groups from phi_K, query groups from phi_Q)
+// and the stable group-major counting sort (Sec. 4.3) it maintains.
+// ---------------------------------------------------------------------------
+
+struct KmArgs {
+  const float* pts;   // [BH][n][R] (k-means only)
+  float* cent;        // [BH][C][R] (k-means only)
+  int32_t* labels;    // [BH][N] in row order; the sorted rows start at row0
+  int32_t* perm;      // [BH][N]
+  int32_t* off;       // [BH][offstride]
+  int32_t* blkhist;   // [BH][nblk][cmax]
+  int32_t* changed;   // [BH][2][T+1]
+  int n;              // rows taking part (sorted rows are row0 .. row0+n-1)
+  int row0, N;
+  int R, C;           // coordinate rank, groups
+  int offstride, nblk, cmax, sel, T;
+};
+
+__device__ __forceinline__ int32_t* km_changed(const KmArgs& a, int bh) {
+  return a.changed + (size_t)bh * 2 * (a.T + 1) + a.sel * (a.T + 1);
+}
+
+__device__ __forceinline__ bool km_skip(const KmArgs& a, int bh, int it) {
+  return it >= 0 && km_changed(a, bh)[it] == 0;
+}
+
+__global__ void k_km_init(KmArgs a) {
+  const int bh = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.C * a.R) return;
+  const int b = i / a.R, c = i % a.R;
+  // cold start from the strided points floor(b * n / C)
+  const int src = (int)(((int64_t)b * a.n) / a.C);
+  a.cent[(size_t)bh * a.C * a.R + i] = a.pts[((size_t)bh * a.n + src) * a.R + c];
+}
+
+// Exact assignment: one point per thread, centroids staged through LDS.
+template <int MAXR>
+__global__ __launch_bounds__(256) void k_km_assign(KmArgs a, int it) {
+  constexpr int CB = 64;
+  __shared__ float cs[CB][MAXR + 1];
+  __shared__ float cu[CB];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  int32_t* chg = km_changed(a, bh);
+  if (it > 0 && chg[it - 1] == 0) return;  // converged: labels and centroids are final
+  const int j = blockIdx.x * 256 + tid;
+  const int R = a.R;
+  float x[MAXR];
+  const float* pj = a.pts + ((size_t)bh * a.n + min(j, a.n - 1)) * R;
+#pragma unroll
+  for (int k = 0; k < MAXR; ++k) x[k] = (k < R) ? pj[k] : 0.f;
+  const float* cent = a.cent + (size_t)bh * a.C * R;
+  float best = 0.f;
+  int bi = -1;
+  for (int c0 = 0; c0 < a.C; c0 += CB) {
+    const int cn = min(CB, a.C - c0);
+    __syncthreads();
+    for (int i = tid; i < cn * R; i += 256) cs[i / R][i % R] = cent[(size_t)c0 * R + i];
+    __syncthreads();
+    if (tid < cn) {
+      float u = 0.f;
+      for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
+      cu[tid] = u;
+    }
+    __syncthreads();
+    for (int b = 0; b < cn; ++b) {
+      float t = 0.f;
+#pragma unroll
+      for (int k = 0; k < MAXR; ++k)
+        if (k < R) t = fmaf(x[k], cs[b][k], t);
+      const float s = fmaf(-2.f, t, cu[b]);
+      if (bi < 0 || s < best) {
+        best = s;
+        bi = c0 + b;
+      }
+    }
+  }
+  if (j < a.n) {
+    int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+    const int old = lab[j];
+    lab[j] = bi;
+    if (it > 0 && old != bi) atomicAdd(&chg[it], 1);
+  }
+}
+
+// Counting sort, pass 1: per-block label histograms.
+__global__ __launch_bounds__(256) void k_sort_hist(KmArgs a, int it) {
+  extern __shared__ int hs[];
+  const int bh = blockIdx.y, blk = blockIdx.x, tid = threadIdx.x;
+  if (km_skip(a, bh, it)) return;
+  for (int b = tid; b < a.C; b += 256) hs[b] = 0;
+  __syncthreads();
+  const int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  const int j0 = blk * kSortBlock, j1 = min(a.n, j0 + kSortBlock);
+  for (int j = j0 + tid; j < j1; j += 256) atomicAdd(&hs[lab[j]], 1);
+  __syncthreads();
+  int32_t* out = a.blkhist + ((size_t)bh * a.nblk + blk) * a.cmax;
+  for (int b = tid; b < a.C; b += 256) out[b] = hs[b];
+}
+
+// Counting sort, pass 2: per-label running offsets over the blocks, then the
+// exclusive scan over labels gives the group offsets.
+__global__ __launch_bounds__(1024) void k_sort_scan(KmArgs a, int it) {
+  extern __shared__ int cnt[];  // C + 1 ints, then 17 ints of scan scratch
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  if (km_skip(a, bh, it)) return;
+  int32_t* hist = a.blkhist + (size_t)bh * a.nblk * a.cmax;
+  for (int b = tid; b < a.C; b += 1024) {
+    int run = 0;
+    for (int k = 0; k < a.nblk; ++k) {
+      const int v = hist[(size_t)k * a.cmax + b];
+      hist[(size_t)k * a.cmax + b] = run;
+      run += v;
+    }
+    cnt[b] = run;
+  }
+  __syncthreads();
+  const int total = block_exclusive_scan(cnt, a.C, cnt + a.C + 1);
+  int32_t* off = a.off + (size_t)bh * a.offstride;
+  for (int b = tid; b < a.C; b += 1024) off[b] = cnt[b];
+  if (tid == 0) off[a.C] = total;
+}
+
+// Counting sort, pass 3: stable scatter.  One wave per block of rows walks its
+// rows in order; rows with equal labels inside a 64-row slice get their
+// stable rank from a ballot over the lanes holding that label.
+__global__ __launch_bounds__(64) void k_sort_scatter(KmArgs a, int it) {
+  extern __shared__ int pos[];
+  const int bh = blockIdx.y, blk = blockIdx.x, lane = threadIdx.x;
+  if (km_skip(a, bh, it)) return;
+  const int32_t* hist = a.blkhist + ((size_t)bh * a.nblk + blk) * a.cmax;
+  const int32_t* off = a.off + (size_t)bh * a.offstride;
+  for (int b = lane; b < a.C; b += 64) pos[b] = off[b] + hist[b];
+  __syncthreads();
+  const int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  int32_t* perm = a.perm + (size_t)bh * a.N;
+  const int j0 = blk * kSortBlock, j1 = min(a.n, j0 + kSortBlock);
+  for (int s = j0; s < j1; s += 64) {
+    const int j = s + lane;
+    const bool valid = j < j1;
+    const int L = valid ? lab[j] : -1;
+    uint64_t active = __ballot(valid);
+    while (active) {
+      const int first = __ffsll((unsigned long long)active) - 1;
+      const int Lf = __shfl(L, first);
+      const uint64_t m = __ballot(L == Lf) & active;
+      if (L == Lf) {
+        const uint64_t below = m & ((1ull << lane) - 1ull);
+        perm[pos[Lf] + __popcll(below)] = a.row0 + j;
+      }
+      __syncthreads();
+      if (lane == first) pos[Lf] += __popcll(m);
+      __syncthreads();
+      active &= ~m;
+    }
+  }
+}
+
+// Centroid update: per group, double sums of the members' coordinates in
+// ascending row order (the stable permutation order) / count, rounded to
+// float; an empty group keeps its centroid.  One wave per group.
+__global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
+  const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (km_changed(a, bh)[it] == 0) return;
+  const int b = blockIdx.x * 4 + wv;
+  if (b >= a.C) return;
+  const int32_t* off = a.off + (size_t)bh * a.offstride;
+  const int32_t* perm = a.perm + (size_t)bh * a.N;
+  const int s0 = off[b], s1 = off[b + 1];
+  if (s1 == s0) return;
+  const float* pts = a.pts + (size_t)bh * a.n * a.R;
+  for (int k = lane; k < a.R; k += 64) {
+    double sum = 0.0;
+    for (int m = s0; m < s1; ++m) sum += (double)pts[(size_t)(perm[m] - a.row0) * a.R + k];
+    a.cent[((size_t)bh * a.C + b) * a.R + k] = (float)(sum / (double)(s1 - s0));
+  }
+}
+
+// The dense-prefix rows (before row0) form the extra last group: label C and
+// the last permutation slots, in row order.
+__global__ void k_prefix_group(KmArgs a) {
+  const int bh = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < a.row0) {
+    a.labels[(size_t)bh * a.N + i] = a.C;
+    a.perm[(size_t)bh * a.N + a.n + i] = i;
+  }
+  if (i == 0 && a.row0 > 0) a.off[(size_t)bh * a.offstride + a.C + 1] = a.N;
+}
+
+// ---------------------------------------------------------------------------
+// Group means in the input space (kbar, qbar): double sums in ascending row
+// order / count, rounded to float; empty groups get 0.  One wave per group.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const int32_t* perm,
+                                                    const int32_t* off, int C, int offstride,
+                                                    float* mean) {
+  const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + wv;
+  if (b >= C) return;
+  const int64_t base = head_base(g, bh);
+  const int32_t* o = off + (size_t)bh * offstride;
+  const int32_t* p = perm + (size_t)bh * g.N;
+  const int s0 = o[b], s1 = o[b + 1];
+  for (int c = lane; c < g.d; c += 64) {
+    double sum = 0.0;
+    for (int m = s0; m < s1; ++m) sum += (double)load_x(x, g.bf16, base + (int64_t)p[m] * g.sn + c);
+    mean[((size_t)bh * C + b) * g.d + c] = (s1 > s0) ? (float)(sum / (double)(s1 - s0)) : 0.f;
+  }
+}
+
+// Query-response metric M_Q = Kt^T Kt / (C_k^+ d) from the nonempty key-space
+// group means centred by their uniform mean, equal weights
+// (App. B.2 eq. app_query_metric).
+template <int D>
+__global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const int32_t* offk,
+                                                      Geom g, double* gram) {
+  constexpr int ENT = D * D / 256;
+  constexpr int GB = 16;
+  __shared__ double mu[D];
+  __shared__ double ks[GB][D];
+  __shared__ int cplus;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int C = g.CK;
+  const int32_t* o = offk + (size_t)bh * (g.CKt + 1);
+  const float* kb = kbar + (size_t)bh * C * D;
+  if (tid < D) {
+    double s = 0.0;
+    int cp = 0;
+    for (int b = 0; b < C; ++b)
+      if (o[b + 1] > o[b]) {
+        s += (double)kb[(size_t)b * D + tid];
+        ++cp;
+      }
+    mu[tid] = cp ? s / cp : 0.0;
+    if (tid == 0) cplus = cp;
+  }
+  __syncthreads();
+  const int e0 = tid * ENT, ra = e0 / D, cb = e0 % D;
+  double acc[ENT];
+#pragma unroll
+  for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
+  for (int b0 = 0; b0 < C; b0 += GB) {
+    for (int t = tid; t < GB * D; t += 256) {
+      const int b = b0 + t / D, c = t % D;
+      double v = 0.0;
+      if (b < C && o[b + 1] > o[b]) v = (double)kb[(size_t)b * D + c] - mu[c];
+      ks[t / D][c] = v;
+    }
+    __syncthreads();
+    for (int i = 0; i < GB; ++i) {
+      const double a = ks[i][ra];
+#pragma unroll
+      for (int e = 0; e < ENT; ++e) acc[e] += a * ks[i][cb + e];
+    }
+    __syncthreads();
+  }
+  const double den = (double)max(cplus, 1) * (double)D;
+  double* out = gram + (size_t)bh * D * D;
+#pragma unroll
+  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / den;
+}
+
+// ---------------------------------------------------------------------------
+// Routing under a pair budget (Sec. 4.3).  Priority of cell (a, b): the
+// centroid estimate of the log attention probability of one of its pairs,
+//   s_ab = (float fmaf chain of qbar_a . kbar_b) * (float)(1/sqrt(d)),
+//   pi_ab = s_ab - (float)log(sum_b |G_b| exp(s_ab)).
+// Every nonempty query group keeps its best cell (forced); the other cells are
+// taken in (pi desc, a*C_k + b asc) order while the cumulative pair cost
+// |G_a||G_b| fits in the budget, which already excludes the probes' cost.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const float* kbar, Geom g,
+                                                    const int32_t* offq, const int32_t* offk,
+                                                    float* prio, int32_t* forced) {
+  extern __shared__ float sm[];  // qrow[d] | s[CK]
+  __shared__ double red[4];
+  __shared__ float redf[4];
+  __shared__ int redi[4];
+  const int a = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, wv = tid >> 6;
+  const int CK = g.CK, D = g.d;
+  const int32_t* oq = offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = offk + (size_t)bh * (g.CKt + 1);
+  float* pr = prio + ((size_t)bh * g.CQ + a) * CK;
+  const int na = oq[a + 1] - oq[a];
+  if (na == 0) {
+    for (int b = tid; b < CK; b += 256) pr[b] = 0.f;
+    if (tid == 0) forced[(size_t)bh * g.CQ + a] = -1;
+    return;
+  }
+  float* qrow = sm;
+  float* s = sm + D;
+  for (int c = tid; c < D; c += 256) qrow[c] = qbar[((size_t)bh * g.CQ + a) * D + c];
+  __syncthreads();
+  const float scale = (float)(1.0 / sqrt((double)D));
+  const float* kb = kbar + (size_t)bh * CK * D;
+  float mx = -INFINITY;
+  for (int b = tid; b < CK; b += 256) {
+    float v = -INFINITY;
+    if (ok[b + 1] > ok[b]) {
+      float t = 0.f;
+      for (int c = 0; c < D; ++c) t = fmaf(qrow[c], kb[(size_t)b * D + c], t);
+      v = t * scale;
+    }
+    s[b] = v;
+    mx = fmaxf(mx, v);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) redf[wv] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  double z = 0.0;
+  for (int b = tid; b < CK; b += 256) {
+    const int nb = ok[b + 1] - ok[b];
+    if (nb > 0) z += (double)nb * exp((double)s[b] - (double)mx);
+  }
+  z = wave_sum_d(z);
+  if (lane == 0) red[wv] = z;
+  __syncthreads();
+  const float lse = (float)((double)mx + log(red[0] + red[1] + red[2] + red[3]));
+  float bestv = -INFINITY;
+  int besti = 0x7fffffff;
+  for (int b = tid; b < CK; b += 256) {
+    float p = 0.f;
+    if (ok[b + 1] > ok[b]) {
+      p = s[b] - lse;
+      if (besti == 0x7fffffff || p > bestv || (p == bestv && b < besti)) {
+        bestv = p;
+        besti = b;
+      }
+    }
+    pr[b] = p;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bestv, o);
+    const int oi = __shfl_xor(besti, o);
+    if (oi != 0x7fffffff && (besti == 0x7fffffff || ov > bestv || (ov == bestv && oi < besti))) {
+      bestv = ov;
+      besti = oi;
+    }
+  }
+  __syncthreads();
+  if (lane == 0) {
+    redf[wv] = bestv;
+    redi[wv] = besti;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float bv = redf[0];
+    int bi = redi[0];
+    for (int k = 1; k < 4; ++k)
+      if (redi[k] != 0x7fffffff &&
+          (bi == 0x7fffffff || redf[k] > bv || (redf[k] == bv && redi[k] < bi))) {
+        bv = redf[k];
+        bi = redi[k];
+      }
+    forced[(size_t)bh * g.CQ + a] = (bi == 0x7fffffff) ? -1 : bi;
+  }
+}
+
+// selstate slots.  SS_DONE: 0 searching, 1 every eligible cell fits,
+// 2 boundary key found (cells with larger keys are taken), 3 nothing beyond
+// the forced cells fits.
+enum { SS_REM = 0, SS_PREFIX = 1, SS_ABOVE = 2, SS_DONE = 3, SS_BOUND = 4 };
+
+// Total order of the walk: larger key first = priority descending, then flat
+// index ascending.
+__device__ __forceinline__ uint64_t cell_key(float p, int64_t idx) {
+  return ((uint64_t)float_order_bits(p) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx);
+}
+
+__global__ __launch_bounds__(256) void k_sel_init(Geom g, Work w) {
+  __shared__ long long red[4];
+  __shared__ int redc[4];
+  const int bh = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  const int32_t* fo = w.forced + (size_t)bh * g.CQ;
+  long long fc = 0;
+  int ncell = 0;
+  for (int a = tid; a < g.CQ; a += 256) {
+    const int b = fo[a];
+    if (b >= 0) {
+      fc += (long long)(oq[a + 1] - oq[a]) * (ok[b + 1] - ok[b]);
+      ++ncell;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    fc += __shfl_xor(fc, o);
+    ncell += __shfl_xor(ncell, o);
+  }
+  if (lane == 0) {
+    red[wv] = fc;
+    redc[wv] = ncell;
+  }
+  uint64_t* hist = w.selhist + (size_t)bh * kSelPasses * kSelBins;
+  for (int i = tid; i < kSelPasses * kSelBins; i += 256) hist[i] = 0;
+  __syncthreads();
+  if (tid == 0) {
+    const long long forced = red[0] + red[1] + red[2] + red[3];
+    const int fcells = redc[0] + redc[1] + redc[2] + redc[3];
+    int64_t* st = w.selstate + (size_t)bh * 8;
+    const long long rem = (long long)g.budget - forced;
+    const long long all = (long long)g.NV * (long long)g.NV - forced;
+    st[SS_REM] = rem;
+    st[SS_PREFIX] = 0;
+    st[SS_ABOVE] = 0;
+    st[SS_BOUND] = 0;
+    st[SS_DONE] = (rem < 0) ? 3 : (all <= rem ? 1 : 0);
+    int64_t* stats = w.stats + (size_t)bh * 16;
+    stats[ST_FORCED_PAIRS] = forced;
+    stats[ST_FORCED_CELLS] = fcells;
+    if (rem < 0) stats[ST_FLAGS] |= SPARSEPR_FLAG_BUDGET_BELOW_FORCED;
+  }
+}
+
+// Weighted radix select, one 8-bit digit of the 64-bit cell key per pass:
+// histogram of pair cost per digit over the cells still in the bucket.
+__global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
+  __shared__ unsigned long long hs[kSelBins];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int64_t* st = w.selstate + (size_t)bh * 8;
+  if (st[SS_DONE] != 0) return;
+  for (int i = tid; i < kSelBins; i += 256) hs[i] = 0;
+  __syncthreads();
+  const int shift = 56 - 8 * p;
+  const uint64_t prefix = (uint64_t)st[SS_PREFIX];
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  const int32_t* fo = w.forced + (size_t)bh * g.CQ;
+  const float* pr = w.prio + (size_t)bh * g.CQ * g.CK;
+  const int64_t ncell = (int64_t)g.CQ * g.CK;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + tid; idx < ncell; idx += (int64_t)gridDim.x * 256) {
+    const int a = (int)(idx / g.CK), b = (int)(idx - (int64_t)a * g.CK);
+    const int na = oq[a + 1] - oq[a], nb = ok[b + 1] - ok[b];
+    if (na == 0 || nb == 0 || fo[a] == b) continue;
+    const uint64_t key = cell_key(pr[idx], idx);
+    if (p > 0 && (key >> (shift + 8)) != (prefix >> (shift + 8))) continue;
+    atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb);
+  }
+  __syncthreads();
+  uint64_t* gh = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
+  for (int i = tid; i < kSelBins; i += 256)
+    if (hs[i]) atomicAdd((unsigned long long*)&gh[i], hs[i]);
+}
+
+// Pick the digit bucket where the cumulative cost (from the largest keys
+// down) first exceeds the remaining budget.
+__global__ void k_sel_choose(Geom g, Work w, int p) {
+  const int bh = blockIdx.x;
+  int64_t* st = w.selstate + (size_t)bh * 8;
+  if (threadIdx.x != 0 || st[SS_DONE] != 0) return;
+  const int shift = 56 - 8 * p;
+  const uint64_t* gh = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
+  const long long rem = st[SS_REM];
+  long long run = st[SS_ABOVE];
+  for (int dg = kSelBins - 1; dg >= 0; --dg) {
+    const long long h = (long long)gh[dg];
+    if (run + h > rem) {
+      const uint64_t prefix = (uint64_t)st[SS_PREFIX] | ((uint64_t)dg << shift);
+      st[SS_PREFIX] = (int64_t)prefix;
+      st[SS_ABOVE] = run;
+      if (shift == 0) {
+        st[SS_BOUND] = (int64_t)prefix;
+        st[SS_DONE] = 2;
+      }
+      return;
+    }
+    run += h;
+  }
+  st[SS_DONE] = 1;
+}
+
+// Route matrix over all cells (dense-prefix group included): forced cells,
+// cells above the boundary key, and every cell of the dense-prefix group.
+__global__ __launch_bounds__(256) void k_sel_mark(Geom g, Work w) {
+  __shared__ int red[4];
+  const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t* st = w.selstate + (size_t)bh * 8;
+  const int done = (int)st[SS_DONE];
+  const uint64_t bound = (uint64_t)st[SS_BOUND];
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  const int32_t* fo = w.forced + (size_t)bh * g.CQ;
+  const float* pr = w.prio + (size_t)bh * g.CQ * g.CK;
+  uint8_t* z = w.z + (size_t)bh * g.CQt * g.CKt;
+  const int64_t ncell = (int64_t)g.CQt * g.CKt;
+  int cnt = 0;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + tid; idx < ncell; idx += (int64_t)gridDim.x * 256) {
+    const int a = (int)(idx / g.CKt), b = (int)(idx - (int64_t)a * g.CKt);
+    uint8_t sel = 0;
+    if (a < g.CQ && b < g.CK) {
+      const int na = oq[a + 1] - oq[a], nb = ok[b + 1] - ok[b];
+      if (na > 0 && nb > 0) {
+        if (fo[a] == b) {
+          sel = 1;
+        } else if (done == 1) {
+          sel = 1;
+        } else if (done == 2) {
+          const int64_t vidx = (int64_t)a * g.CK + b;
+          sel = cell_key(pr[vidx], vidx) > bound;
+        }
+        cnt += sel;
+      }
+    } else {
+      sel = 1;  // dense-prefix query group or K/V group
+    }
+    z[idx] = sel;
+  }
+  cnt = wave_sum_i(cnt);
+  if (lane == 0) red[wv] = cnt;
+  __syncthreads();
+  if (tid == 0) {
+    const int c = red[0] + red[1] + red[2] + red[3];
+    if (c) atomicAdd((unsigned long long*)&w.stats[(size_t)bh * 16 + ST_ROUTED_CELLS],
+                     (unsigned long long)c);
+  }
+}
+
+// Per query group, the routed K/V groups as maximal contiguous ranges of the
+// group-major K/V order, and their total length.
+__global__ __launch_bounds__(64) void k_ranges(Geom g, Work w) {
+  const int bh = blockIdx.y;
+  const int a = blockIdx.x * 64 + threadIdx.x;
+  if (a >= g.CQt) return;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  const uint8_t* z = w.z + ((size_t)bh * g.CQt + a) * g.CKt;
+  int2* rg = w.rng + ((size_t)bh * g.CQt + a) * g.CKt;
+  const int na = oq[a + 1] - oq[a];
+  int cnt = 0, tot = 0, cs = -1, ce = -1;
+  if (na > 0) {
+    for (int b = 0; b < g.CKt; ++b) {
+      if (!z[b]) continue;
+      const int s = ok[b], e = ok[b + 1];
+      if (e == s) continue;
+      if (s == ce) {
+        ce = e;
+      } else {
+        if (cs >= 0) rg[cnt++] = make_int2(cs, ce - cs);
+        cs = s;
+        ce = e;
+      }
+      tot += e - s;
+    }
+    if (cs >= 0) rg[cnt++] = make_int2(cs, ce - cs);
+  }
+  w.rng_cnt[(size_t)bh * g.CQt + a] = cnt;
+  w.keytot[(size_t)bh * g.CQt + a] = tot;
+  if (na > 0)
+    atomicAdd((unsigned long long*)&w.stats[(size_t)bh * 16 + ST_ROUTED_PAIRS],
+              (unsigned long long)((long long)na * tot));
+}
+
+// Attention work items: each query group split into tiles of kQTile rows.
+__global__ __launch_bounds__(1024) void k_chunks(Geom g, Work w) {
+  extern __shared__ int nch[];  // CQt + 1 + 17
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  for (int a = tid; a < g.CQt; a += 1024) nch[a] = (oq[a + 1] - oq[a] + kQTile - 1) / kQTile;
+  __syncthreads();
+  const int total = block_exclusive_scan(nch, g.CQt, nch + g.CQt + 1);
+  int4* ch = w.chunks + (size_t)bh * g.nchunk_max;
+  const int32_t* kt = w.keytot + (size_t)bh * g.CQt;
+  for (int a = tid; a < g.CQt; a += 1024) {
+    const int na = oq[a + 1] - oq[a];
+    int c = nch[a];
+    for (int r0 = 0; r0 < na; r0 += kQTile) ch[c++] = make_int4(a, r0, min(kQTile, na - r0), kt[a]);
+  }
+  if (tid == 0) w.nchunks[bh] = total;
+}
+
+// ---------------------------------------------------------------------------
+// Probe selection (App. A.2, Algorithm "Query-Group-Stratified Exact Probe
+// Selection") and coverage weights w_p = |G_a| / m_a (eq. app_probe_weight).
+// ---------------------------------------------------------------------------
+
+// Radial key of every video row: squared distance to its group mean in phi_Q
+// space (ordering by it is ordering by the distance).
+__global__ void k_probe_d2(Geom g, Work w) {
+  const int bh = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= g.NV) return;
+  const int a = w.labq[(size_t)bh * g.N + g.ntext + i];
+  const float* ph = w.phiq + ((size_t)bh * g.NV + i) * g.rq;
+  const float* c = w.centq + ((size_t)bh * g.CQ + a) * g.rq;
+  float acc = 0.f;
+  for (int k = 0; k < g.rq; ++k) {
+    const float diff = ph[k] - c[k];
+    acc = fmaf(diff, diff, acc);
+  }
+  w.d2[(size_t)bh * g.NV + i] = acc;
+}
+
+__device__ __forceinline__ uint64_t probe_key(float d2, int row) {
+  return ((uint64_t)float_order_bits(d2) << 32) | (uint32_t)row;
+}
+
+// One block per head.  Groups are visited in a deterministic order (ascending
+// id when there are at most M nonempty groups, otherwise the stride-s
+// interleave (rank mod s, rank), s = ceil(G / M)); each visit takes the
+// group's next row by (distance, row index).
+__global__ __launch_bounds__(256) void k_probe_select(Geom g, Work w) {
+  extern __shared__ int sh[];  // cnt[CQ] | ne[CQ] | mcount[CQ] | base[CQ + 1 + 5]
+  int* cnt = sh;
+  int* ne = cnt + g.CQ;
+  int* mcount = ne + g.CQ;
+  int* base = mcount + g.CQ;
+  __shared__ int G;
+  const int bh = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int M = g.M;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* perm = w.permq + (size_t)bh * g.N;
+  int32_t* probes = w.probes + (size_t)bh * M;
+  int32_t* picks = w.picks + (size_t)bh * M;
+  float* pw = w.pw + (size_t)bh * M;
+  const float* d2 = w.d2 + (size_t)bh * g.NV;
+  for (int a = tid; a < g.CQ; a += 256) {
+    cnt[a] = oq[a + 1] - oq[a];
+    mcount[a] = 0;
+    base[a] = (cnt[a] > 0);
+  }
+  __syncthreads();
+  const int ng = block_exclusive_scan(base, g.CQ, base + g.CQ + 1);
+  for (int a = tid; a < g.CQ; a += 256)
+    if (cnt[a] > 0) ne[base[a]] = a;
+  if (tid == 0) G = ng;
+  __syncthreads();
+  // probes per group
+  if (G > M) {
+    const int s = (G + M - 1) / M, qs = G / s, rem = G % s;
+    for (int k = tid; k < G; k += 256) {
+      const int res = k % s;
+      const int pos = res * qs + min(res, rem) + k / s;
+      if (pos < M) mcount[ne[k]] = 1;
+    }
+  } else if (tid == 0) {
+    int taken = 0;
+    for (int t = 0; taken < M; ++t)
+      for (int o = 0; o < G && taken < M; ++o)
+        if (cnt[ne[o]] > t) {
+          mcount[ne[o]]++;
+          ++taken;
+        }
+  }
+  __syncthreads();
+  for (int a = tid; a < g.CQ; a += 256) base[a] = mcount[a];
+  __syncthreads();
+  block_exclusive_scan(base, g.CQ, base + g.CQ + 1);
+  // each wave selects the mcount smallest (d2, row) rows of its groups
+  for (int a = wv; a < g.CQ; a += 4) {
+    const int m = mcount[a];
+    if (m == 0) continue;
+    const int s0 = oq[a], s1 = oq[a + 1];
+    uint64_t last = 0;
+    for (int t = 0; t < m; ++t) {
+      uint64_t best = ~0ull;
+      for (int i = s0 + lane; i < s1; i += 64) {
+        const int row = perm[i];
+        const uint64_t key = probe_key(d2[row - g.ntext], row);
+        if ((t == 0 || key > last) && key < best) best = key;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t ob = __shfl_xor(best, o);
+        best = ob < best ? ob : best;
+      }
+      if (lane == 0) picks[base[a] + t] = (int)(best & 0xffffffffu);
+      last = best;
+    }
+  }
+  __syncthreads();
+  // emit in visit order
+  if (tid == 0) {
+    int taken = 0;
+    if (G > M) {
+      const int s = (G + M - 1) / M;
+      for (int res = 0; res < s && taken < M; ++res)
+        for (int k = res; k < G && taken < M; k += s) {
+          const int a = ne[k];
+          probes[taken] = picks[base[a]];
+          pw[taken] = (float)cnt[a];
+          ++taken;
+        }
+    } else {
+      for (int t = 0; taken < M; ++t)
+        for (int o = 0; o < G && taken < M; ++o) {
+          const int a = ne[o];
+          if (cnt[a] > t) {
+            probes[taken] = picks[base[a] + t];
+            pw[taken] = (float)cnt[a] / (float)mcount[a];
+            ++taken;
+          }
+        }
+    }
+    w.nprobes[bh] = taken;
+    w.stats[(size_t)bh * 16 + ST_NPROBES] = taken;
+  }
+}
+
+// Coverage weights of imported probes: w_p = |G_a| / m_a.
+__global__ __launch_bounds__(256) void k_probe_weights(Geom g, Work w) {
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int np = w.nprobes[bh];
+  const int32_t* lab = w.labq + (size_t)bh * g.N;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  for (int p = tid; p < np; p += 256) {
+    const int a = lab[w.probes[(size_t)bh * g.M + p]];
+    int m = 0;
+    for (int t = 0; t < np; ++t) m += (lab[w.probes[(size_t)bh * g.M + t]] == a);
+    w.pw[(size_t)bh * g.M + p] = (float)(oq[a + 1] - oq[a]) / (float)m;
+  }
+  if (tid == 0) w.stats[(size_t)bh * 16 + ST_NPROBES] = np;
+}
+
+// Final per-head counters: k-means assignments performed, nonempty groups.
+__global__ __launch_bounds__(256) void k_plan_stats(Geom g, Work w, int with_kmeans) {
+  __shared__ int red[2][4];
+  const int bh = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  int nq = 0, nk = 0;
+  for (int a = tid; a < g.CQt; a += 256) nq += oq[a + 1] > oq[a];
+  for (int b = tid; b < g.CKt; b += 256) nk += ok[b + 1] > ok[b];
+  nq = wave_sum_i(nq);
+  nk = wave_sum_i(nk);
+  if (lane == 0) {
+    red[0][wv] = nq;
+    red[1][wv] = nk;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t* st = w.stats + (size_t)bh * 16;
+    st[ST_NE_Q] = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+    st[ST_NE_K] = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+    if (with_kmeans) {
+      for (int sel = 0; sel < 2; ++sel) {
+        const int32_t* chg = w.kmstate + (size_t)bh * 2 * (g.T + 1) + sel * (g.T + 1);
+        int n = 1;
+        for (int it = 1; it < g.T && chg[it - 1] != 0; ++it) ++n;
+        st[sel == 0 ? ST_ITK : ST_ITQ] = n;
+      }
+    }
+  }
+}
+
+__global__ void k_zero_routed(Geom g, Work w) {
+  const int bh = blockIdx.x;
+  if (threadIdx.x == 0) {
+    w.stats[(size_t)bh * 16 + ST_ROUTED_PAIRS] = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host launchers
+// ---------------------------------------------------------------------------
+
+static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
+  const int shm = (a.C + 1 + 17) * (int)sizeof(int);
+  k_sort_hist<<<dim3(a.nblk, BH), 256, a.C * sizeof(int), s>>>(a, it);
+  k_sort_scan<<<BH, 1024, shm, s>>>(a, it);
+  k_sort_scatter<<<dim3(a.nblk, BH), 64, a.C * sizeof(int), s>>>(a, it);
+}
+
+static void run_kmeans(const Geom& g, const KmArgs& a, hipStream_t s) {
+  const int BH = g.BH;
+  k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
+  for (int it = 0; it < g.T; ++it) {
+    dim3 grid((a.n + 255) / 256, BH);
+    if (a.R <= 32)
+      k_km_assign<32><<<grid, 256, 0, s>>>(a, it);
+    else if (a.R <= 64)
+      k_km_assign<64><<<grid, 256, 0, s>>>(a, it);
+    else
+      k_km_assign<128><<<grid, 256, 0, s>>>(a, it);
+    run_sort(a, BH, it, s);
+    k_km_update<<<dim3((a.C + 3) / 4, BH), 256, 0, s>>>(a, it);
+  }
+  if (a.row0 > 0) k_prefix_group<<<dim3((a.row0 + 255) / 256, BH), 256, 0, s>>>(a);
+}
+
+template <int D>
+static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s) {
+  const int BH = g.BH;
+  k_plan_init<<<BH, 64, 0, s>>>(g, w);
+  // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1)
+  k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
+  k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
+  k_project<D><<<dim3((g.NV + 63) / 64, BH), 256, 0, s>>>(k, g, w.fk, g.rk, 0, 0.f, w.phik,
+                                                         w.stats);
+  KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
+            g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T};
+  run_kmeans(g, ak, s);
+  // Query-response coordinates from the K/V groups (App. B.2)
+  k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
+                                                         w.kbar);
+  k_query_metric<D><<<BH, 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
+  k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
+  k_project<D><<<dim3((g.NV + 63) / 64, BH), 256, 0, s>>>(q, g, w.fq, g.rq, 1, g.eps_q, w.phiq,
+                                                         w.stats);
+  KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
+            g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T};
+  run_kmeans(g, aq, s);
+  k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
+                                                         w.qbar);
+  // Routing (Sec. 4.3)
+  k_route_prio<<<dim3(g.CQ, BH), 256, (g.d + g.CK) * sizeof(float), s>>>(
+      w.qbar, w.kbar, g, w.offq, w.offk, w.prio, w.forced);
+  k_sel_init<<<BH, 256, 0, s>>>(g, w);
+  const int64_t ncell = (int64_t)g.CQ * g.CK;
+  const int gsel = (int)std::min<int64_t>(std::max<int64_t>((ncell + 4095) / 4096, 1), 512);
+  for (int p = 0; p < kSelPasses; ++p) {
+    k_sel_hist<<<dim3(gsel, BH), 256, 0, s>>>(g, w, p);
+    k_sel_choose<<<BH, 64, 0, s>>>(g, w, p);
+  }
+  const int64_t ncell_t = (int64_t)g.CQt * g.CKt;
+  const int gmark = (int)std::min<int64_t>(std::max<int64_t>((ncell_t + 4095) / 4096, 1), 512);
+  k_sel_mark<<<dim3(gmark, BH), 256, 0, s>>>(g, w);
+  k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);
+  k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
+  // Probes (App. A.2)
+  if (g.M > 0) {
+    k_probe_d2<<<dim3((g.NV + 255) / 256, BH), 256, 0, s>>>(g, w);
+    k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
+  }
+  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 1);
+}
+
+void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s) {
+  if (g.d == 64)
+    plan_d<64>(g, w, q, k, s);
+  else
+    plan_d<128>(g, w, q, k, s);
+}
+
+void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s) {
+  (void)bh;  // every head is rebuilt; heads not imported reproduce their own data
+  const int BH = g.BH;
+  KmArgs ak{nullptr, nullptr, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.N, 0, g.N,
+            0, g.CKt, g.CKt + 1, g.nsort_blk_full, g.cmax, 0, g.T};
+  run_sort(ak, BH, -1, s);
+  KmArgs aq{nullptr, nullptr, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.N, 0, g.N,
+            0, g.CQt, g.CQt + 1, g.nsort_blk_full, g.cmax, 1, g.T};
+  run_sort(aq, BH, -1, s);
+  k_zero_routed<<<BH, 64, 0, s>>>(g, w);
+  k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);
+  k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
+  if (g.M > 0) k_probe_weights<<<BH, 256, 0, s>>>(g, w);
+  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 0);
+}
+
+}  // namespace sparsepr

@@ -1,0 +1,121 @@
+// Internal declarations shared by the HIP translation units of the SparsePR
+// library: problem geometry, the device workspace layout and the host-side
+// launchers of every kernel.  Nothing here is part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sparsepr.h"
+
+namespace sparsepr {
+
+// Attention-kernel query tile: rows of one query group handled by a block.
+constexpr int kQTile = 64;
+// Key tile of the attention kernels.
+constexpr int kKTile = 64;
+// Probe-row dense attention: keys per split.
+constexpr int kProbeSplit = 2048;
+// Tokens per block of the counting sort.
+constexpr int kSortBlock = 1024;
+// Bins of one radix-select pass (8-bit digits over 64-bit keys).
+constexpr int kSelBins = 256;
+constexpr int kSelPasses = 8;
+
+struct Geom {
+  int B, H, BH;           // batch, heads, batch*heads
+  int N, NV, ntext;       // rows, video rows, dense-prefix rows
+  int d, dv;              // head dims (equal)
+  int rk, rq;             // response ranks, clamped to d
+  int CK, CQ;             // video groups
+  int CKt, CQt;           // + the dense-prefix group when ntext > 0
+  int Ms;                 // sampled queries (clamped to NV)
+  int T;                  // k-means iterations
+  int M;                  // probes per head, min(n_probes, NV)
+  int r;                  // residual rank
+  int bf16;               // 1: bf16 tensors, 0: fp32
+  int64_t sb, sh, sn;     // element strides of Q, K, V, O
+  float rho, ridge, eps_q, eps_x;
+  int64_t budget;         // video x video pair budget after the probe reservation
+  int nchunk_max;         // attention work items per head (upper bound)
+  int nsplit;             // probe attention key splits
+  int nsort_blk;          // counting-sort blocks over NV rows
+  int nsort_blk_full;     // counting-sort blocks over N rows
+  int cmax;               // max(CKt, CQt)
+};
+
+// Device workspace: every array is [BH][...] contiguous.
+struct Work {
+  double* gram_k;   // [BH][d][d]
+  double* gram_q;   // [BH][d][d]
+  float* evals_k;   // [BH][d]
+  float* evals_q;   // [BH][d]
+  float* fk;        // [BH][d][rk]
+  float* fq;        // [BH][d][rq]
+  float* phik;      // [BH][NV][rk]
+  float* phiq;      // [BH][NV][rq]
+  float* centk;     // [BH][CK][rk]
+  float* centq;     // [BH][CQ][rq]
+  int32_t* labk;    // [BH][N]  (row order; dense prefix -> CK)
+  int32_t* labq;    // [BH][N]
+  int32_t* permk;   // [BH][N]
+  int32_t* permq;   // [BH][N]
+  int32_t* offk;    // [BH][CKt+1]
+  int32_t* offq;    // [BH][CQt+1]
+  int32_t* blkhist; // [BH][nsort_blk_full][cmax]
+  int32_t* kmstate; // [BH][2][T+1]: labels changed per assignment (kv, q)
+  float* kbar;      // [BH][CK][d]
+  float* qbar;      // [BH][CQ][d]
+  float* prio;      // [BH][CQ][CK]
+  int32_t* forced;  // [BH][CQ]
+  uint64_t* selhist;  // [BH][kSelPasses][kSelBins]
+  int64_t* selstate;  // [BH][8]
+  uint8_t* z;         // [BH][CQt][CKt]
+  int32_t* rng_cnt;   // [BH][CQt]
+  int2* rng;          // [BH][CQt][CKt]: (start position in perm_kv, length)
+  int32_t* keytot;    // [BH][CQt]
+  int4* chunks;       // [BH][nchunk_max]: (a, row start in group, rows, keys)
+  int32_t* nchunks;   // [BH]
+  float* d2;          // [BH][NV] probe radial distances
+  int32_t* probes;    // [BH][M]
+  float* pw;          // [BH][M]
+  int32_t* nprobes;   // [BH]
+  int32_t* picks;     // [BH][M] probe-selection scratch
+  float* osp;         // [BH][N][dv]
+  float* odp;         // [BH][M][dv]
+  float* part;        // [BH][M][nsplit][dv+2] split partials (o, m, l)
+  float* fitv;        // [BH][3*dv] mu_x, s_x, mu_r
+  float* fity;        // [BH][dv][r] B Psi
+  float* fitpsi;      // [BH][dv][r]
+  double* fitscr;     // [BH][2*M*dv + M*r + dv*r] fit scratch
+  int64_t* stats;     // [BH][16]
+};
+
+// stats slots
+enum {
+  ST_ROUTED_PAIRS = 0,
+  ST_FORCED_PAIRS = 1,
+  ST_ROUTED_CELLS = 2,
+  ST_FORCED_CELLS = 3,
+  ST_NPROBES = 4,
+  ST_ITK = 5,
+  ST_ITQ = 6,
+  ST_FLAGS = 7,
+  ST_NE_Q = 8,
+  ST_NE_K = 9,
+  ST_FIT_RANK = 10,
+};
+
+// ---- plan kernels -------------------------------------------------------
+void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s);
+// Rebuild permutations, route lists, chunks and probe weights from labels,
+// z and probes already placed in the workspace for head bh (import path).
+void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s);
+// ---- attend kernels -----------------------------------------------------
+void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+                   void* out, hipStream_t s);
+void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
+                  float* part, hipStream_t s);
+
+}  // namespace sparsepr

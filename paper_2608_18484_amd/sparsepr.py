@@ -1,0 +1,257 @@
+"""Thin ctypes binding of the SparsePR C ABI (include/sparsepr.h).
+
+Argument marshalling only: every step of the operator runs in the HIP
+library.  torch supplies device memory (inputs, outputs, the workspace) and
+the stream.  Loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsparsepr.so")
+
+F32, BF16 = 0, 1
+FLAG_NONFINITE_INPUT, FLAG_FIT_NOT_PD, FLAG_BUDGET_BELOW_FORCED = 1, 2, 4
+STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP",
+          5: "NUMERICAL"}
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("n_q", ctypes.c_int32),
+                ("n_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("stride_n", ctypes.c_int64), ("dtype", ctypes.c_int32)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("n_sampled_queries", ctypes.c_int32), ("r_k", ctypes.c_int32),
+                ("r_q", ctypes.c_int32), ("n_kv_groups", ctypes.c_int32),
+                ("n_q_groups", ctypes.c_int32), ("kmeans_iters", ctypes.c_int32),
+                ("target_exec_density", ctypes.c_float), ("n_probes", ctypes.c_int32),
+                ("resid_rank", ctypes.c_int32), ("ridge", ctypes.c_float),
+                ("eps_q", ctypes.c_float), ("eps_x", ctypes.c_float),
+                ("n_dense_prefix", ctypes.c_int32)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("rho_route", ctypes.c_double), ("rho_exec", ctypes.c_double),
+                ("routed_pairs", ctypes.c_int64), ("exec_pairs", ctypes.c_int64),
+                ("forced_pairs", ctypes.c_int64), ("routed_cells", ctypes.c_int32),
+                ("forced_cells", ctypes.c_int32), ("nonempty_q_groups", ctypes.c_int32),
+                ("nonempty_kv_groups", ctypes.c_int32), ("n_probes", ctypes.c_int32),
+                ("kmeans_iters_kv", ctypes.c_int32), ("kmeans_iters_q", ctypes.c_int32),
+                ("status_flags", ctypes.c_int32)]
+
+
+_P = ctypes.c_void_p
+HOST_FIELDS = [
+    ("labels_q", "i4"), ("labels_kv", "i4"), ("routes", "u1"), ("probes", "i4"),
+    ("n_probes", None),
+    ("probe_weights", "f4"), ("perm_q", "i4"), ("off_q", "i4"), ("perm_kv", "i4"),
+    ("off_kv", "i4"), ("m_k", "f4"), ("m_q", "f4"), ("f_k", "f4"), ("f_q", "f4"),
+    ("phi_k", "f4"), ("phi_q", "f4"), ("cent_k", "f4"), ("cent_q", "f4"), ("kbar", "f4"),
+    ("qbar", "f4"), ("route_prio", "f4"), ("o_sparse", "f4"), ("o_dense_probes", "f4"),
+    ("fit_mu_x", "f4"), ("fit_s_x", "f4"), ("fit_mu_r", "f4"), ("fit_bpsi", "f4"),
+    ("fit_psi", "f4"), ("fit_rank", None),
+]
+
+
+class PlanHost(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32 if kind is None else _P) for name, kind in HOST_FIELDS]
+
+
+EXPORTED = ["sparsepr_params_default", "sparsepr_workspace_size", "sparsepr_plan_create",
+            "sparsepr_plan", "sparsepr_attend", "sparsepr_dense_workspace_size",
+            "sparsepr_dense_attend", "sparsepr_get_stats", "sparsepr_plan_export",
+            "sparsepr_plan_import", "sparsepr_plan_destroy", "sparsepr_last_error"]
+
+_lib = None
+
+
+def lib():
+    """Load libsparsepr.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"SparsePR HIP library not built: {LIB_PATH} is missing "
+                               "(run __graft_entry__.build() or paper_2608_18484_amd/build.py)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.sparsepr_last_error.restype = ctypes.c_char_p
+        for name in EXPORTED:
+            if name not in ("sparsepr_last_error", "sparsepr_params_default", "sparsepr_plan_destroy"):
+                getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+class SparsePRError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _check(st):
+    if st != 0:
+        raise SparsePRError(st, lib().sparsepr_last_error().decode())
+
+
+def default_params(**kw) -> Params:
+    p = Params()
+    lib().sparsepr_params_default(ctypes.byref(p))
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def shape_of(t, dtype=None) -> Shape:
+    """Shape struct for a [B, H, N, d] torch tensor (last dim contiguous)."""
+    import torch
+    b, h, n, d = t.shape
+    sb, sh, sn, sd = t.stride()
+    if sd != 1:
+        raise ValueError("last dimension must be contiguous")
+    dt = dtype if dtype is not None else (BF16 if t.dtype == torch.bfloat16 else F32)
+    return Shape(b, h, n, n, d, d, sb, sh, sn, dt)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class SparsePR:
+    """One SparsePR operator instance bound to a shape, parameters and a workspace."""
+
+    def __init__(self, shape: Shape, params: Params, device="cuda"):
+        import torch
+        self.shape, self.params = shape, params
+        nbytes = ctypes.c_size_t(0)
+        _check(lib().sparsepr_workspace_size(ctypes.byref(shape), ctypes.byref(params),
+                                             ctypes.byref(nbytes)))
+        self.workspace_bytes = nbytes.value
+        self.workspace = torch.empty(max(nbytes.value, 256), dtype=torch.uint8, device=device)
+        self.handle = ctypes.c_void_p()
+        _check(lib().sparsepr_plan_create(ctypes.byref(shape), ctypes.byref(params),
+                                          _ptr(self.workspace), ctypes.c_size_t(self.workspace.numel()),
+                                          ctypes.byref(self.handle)))
+        n = shape.n_q
+        ntext = params.n_dense_prefix
+        nv = n - ntext
+        self.ck = params.n_kv_groups or -(-nv // 64)
+        self.cq = params.n_q_groups or -(-nv // 64)
+        self.ck_t = self.ck + (ntext > 0)
+        self.cq_t = self.cq + (ntext > 0)
+        self.m = min(params.n_probes, nv)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.sparsepr_plan_destroy(h)
+            self.handle = None
+
+    def plan(self, q, k, stream=None):
+        _check(lib().sparsepr_plan(self.handle, _ptr(q), _ptr(k), _stream(stream)))
+
+    def attend(self, q, k, v, out, stream=None):
+        _check(lib().sparsepr_attend(self.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                     _stream(stream)))
+
+    def __call__(self, q, k, v, out=None, stream=None):
+        import torch
+        if out is None:
+            out = torch.empty_like(q)
+        self.plan(q, k, stream)
+        self.attend(q, k, v, out, stream)
+        return out
+
+    def stats(self, stream=None) -> dict:
+        s = Stats()
+        _check(lib().sparsepr_get_stats(self.handle, ctypes.byref(s), _stream(stream)))
+        return {name: getattr(s, name) for name, _ in Stats._fields_}
+
+    def _sizes(self):
+        sh, p = self.shape, self.params
+        n, d, dv = sh.n_q, sh.d, sh.d_v
+        nv = n - p.n_dense_prefix
+        rk, rq, r = min(p.r_k, d), min(p.r_q, d), p.resid_rank
+        m = max(self.m, 1)
+        return {
+            "labels_q": n, "labels_kv": n, "routes": self.cq_t * self.ck_t, "probes": m,
+            "probe_weights": m, "perm_q": n, "off_q": self.cq_t + 1, "perm_kv": n,
+            "off_kv": self.ck_t + 1, "m_k": d * d, "m_q": d * d, "f_k": d * rk, "f_q": d * rq,
+            "phi_k": nv * rk, "phi_q": nv * rq, "cent_k": self.ck * rk, "cent_q": self.cq * rq,
+            "kbar": self.ck * d, "qbar": self.cq * d, "route_prio": self.cq * self.ck,
+            "o_sparse": n * dv, "o_dense_probes": m * dv, "fit_mu_x": dv, "fit_s_x": dv,
+            "fit_mu_r": dv, "fit_bpsi": dv * r, "fit_psi": dv * r,
+        }
+
+    def export(self, bh: int = 0, fields=None, stream=None) -> dict:
+        """Copy head bh of the plan (and attend outputs) to numpy arrays."""
+        sizes = self._sizes()
+        want = [name for name, kind in HOST_FIELDS if kind is not None and
+                (fields is None or name in fields)]
+        bufs = {}
+        ph = PlanHost()
+        for name, kind in HOST_FIELDS:
+            if kind is None or name not in want:
+                continue
+            arr = np.zeros(sizes[name], dtype=np.dtype(kind))
+            bufs[name] = arr
+            setattr(ph, name, arr.ctypes.data_as(ctypes.c_void_p))
+        _check(lib().sparsepr_plan_export(self.handle, ctypes.c_int32(bh), ctypes.byref(ph),
+                                          _stream(stream)))
+        sh, p = self.shape, self.params
+        d, dv, r = sh.d, sh.d_v, p.resid_rank
+        rk, rq = min(p.r_k, d), min(p.r_q, d)
+        npr = ph.n_probes
+        shapes = {"routes": (self.cq_t, self.ck_t), "m_k": (d, d), "m_q": (d, d),
+                  "f_k": (d, rk), "f_q": (d, rq), "phi_k": (-1, rk), "phi_q": (-1, rq),
+                  "cent_k": (self.ck, rk), "cent_q": (self.cq, rq), "kbar": (self.ck, d),
+                  "qbar": (self.cq, d), "route_prio": (self.cq, self.ck), "o_sparse": (-1, dv),
+                  "o_dense_probes": (-1, dv), "fit_bpsi": (dv, r), "fit_psi": (dv, r)}
+        out = {}
+        for name, arr in bufs.items():
+            if name in ("probes", "probe_weights"):
+                arr = arr[:npr]
+            if name == "o_dense_probes":
+                arr = arr[:npr * dv]
+            out[name] = arr.reshape(shapes[name]) if name in shapes else arr
+        out["n_probes"] = npr
+        out["fit_rank"] = ph.fit_rank
+        return out
+
+    def import_plan(self, bh: int, labels_q, labels_kv, routes, probes, stream=None):
+        """Replace head bh's plan by host arrays (labels, route matrix, probes)."""
+        lq = np.ascontiguousarray(labels_q, np.int32)
+        lk = np.ascontiguousarray(labels_kv, np.int32)
+        z = np.ascontiguousarray(routes, np.uint8)
+        pr = np.ascontiguousarray(probes, np.int32)
+        ph = PlanHost()
+        ph.labels_q = lq.ctypes.data_as(ctypes.c_void_p)
+        ph.labels_kv = lk.ctypes.data_as(ctypes.c_void_p)
+        ph.routes = z.ctypes.data_as(ctypes.c_void_p)
+        ph.probes = pr.ctypes.data_as(ctypes.c_void_p) if len(pr) else None
+        ph.n_probes = len(pr)
+        _check(lib().sparsepr_plan_import(self.handle, ctypes.c_int32(bh), ctypes.byref(ph),
+                                          _stream(stream)))
+
+
+def dense_attention(q, k, v, out=None, stream=None):
+    """Dense attention (Sec. 3) for every head on the probe kernels."""
+    import torch
+    if out is None:
+        out = torch.empty_like(q)
+    sh = shape_of(q)
+    _check(lib().sparsepr_dense_attend(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                       None, ctypes.c_size_t(0), _stream(stream)))
+    return out

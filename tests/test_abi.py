@@ -1,0 +1,124 @@
+"""Host-side checks of the C ABI: the library loads, exports exactly what
+include/sparsepr.h declares, and validates arguments before any HIP call."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_18484_amd import sparsepr as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparsepr.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sparsepr_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_names():
+    assert declared_functions() == sorted(S.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = S.lib()
+    out = subprocess.check_output(["nm", "-D", "--defined-only", S.LIB_PATH], text=True)
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_struct_layout_matches_c_compiler(tmp_path):
+    # the binding's structs must have the C layout the header gives them
+    structs = {"sparsepr_shape": S.Shape, "sparsepr_params": S.Params,
+               "sparsepr_stats": S.Stats, "sparsepr_plan_host": S.PlanHost}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', 'int main(void) {']
+    for cname, cls in structs.items():
+        lines.append(f'printf("{cname} %zu\\n", sizeof({cname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'printf("{cname}.{fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-o", str(exe), str(src)])
+    got = dict(l.split() for l in subprocess.check_output([str(exe)], text=True).splitlines())
+    for cname, cls in structs.items():
+        assert int(got[cname]) == ctypes.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert int(got[f"{cname}.{fname}"]) == getattr(cls, fname).offset, (cname, fname)
+
+
+def _ws(shape, params):
+    n = ctypes.c_size_t(0)
+    st = S.lib().sparsepr_workspace_size(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(n))
+    return st, n.value, S.lib().sparsepr_last_error().decode()
+
+
+def tiny_shape(**kw):
+    base = dict(batch=1, heads=1, n_q=1024, n_kv=1024, d=64, d_v=64, stride_b=65536,
+                stride_h=65536, stride_n=64, dtype=S.F32)
+    base.update(kw)
+    return S.Shape(**base)
+
+
+def test_defaults_follow_paper_table():
+    p = S.default_params()
+    assert (p.r_k, p.r_q, p.n_probes, p.resid_rank) == (48, 64, 64, 16)
+    assert abs(p.ridge - 0.1) < 1e-7 and abs(p.target_exec_density - 0.22) < 1e-7
+    assert abs(p.eps_q - 1e-6) < 1e-12
+
+
+def test_workspace_size_ok_and_monotone():
+    st, n1, _ = _ws(tiny_shape(), S.default_params(n_probes=32))
+    assert st == 0 and n1 > 0
+    st, n2, _ = _ws(tiny_shape(heads=4, stride_b=4 * 65536), S.default_params(n_probes=32))
+    assert st == 0 and n2 > 3 * n1
+
+
+@pytest.mark.parametrize("shape_kw,param_kw,status,needle", [
+    (dict(d=96, d_v=96, stride_n=96), {}, 2, "d must be 64 or 128"),
+    (dict(d_v=128), {}, 2, "d must equal d_v"),
+    (dict(n_kv=512), {}, 2, "self-attention"),
+    (dict(batch=0), {}, 1, "batch"),
+    (dict(dtype=7), {}, 1, "dtype"),
+    (dict(stride_n=32), {}, 1, "stride"),
+    ({}, dict(target_exec_density=0.0), 1, "target_exec_density"),
+    ({}, dict(target_exec_density=1.5), 1, "target_exec_density"),
+    ({}, dict(resid_rank=0), 1, "resid_rank"),
+    ({}, dict(resid_rank=65), 1, "resid_rank"),
+    ({}, dict(n_kv_groups=2000), 1, "group counts"),
+    ({}, dict(n_probes=-1), 1, "n_probes"),
+    ({}, dict(ridge=-1.0), 1, "ridge"),
+    ({}, dict(n_dense_prefix=1024), 1, "n_dense_prefix"),
+    ({}, dict(kmeans_iters=0), 1, "kmeans_iters"),
+])
+def test_validation_errors(shape_kw, param_kw, status, needle):
+    st, _, msg = _ws(tiny_shape(**shape_kw), S.default_params(**param_kw))
+    assert st == status and needle in msg
+
+
+def test_null_arguments_rejected():
+    lib = S.lib()
+    assert lib.sparsepr_workspace_size(None, None, None) == 1
+    assert lib.sparsepr_plan(None, None, None, None) == 1
+    assert lib.sparsepr_attend(None, None, None, None, None, None) == 1
+    assert lib.sparsepr_get_stats(None, None, None) == 1
+    assert lib.sparsepr_plan_export(None, 0, None, None) == 1
+    assert lib.sparsepr_plan_import(None, 0, None, None) == 1
+    lib.sparsepr_plan_destroy(None)
+    sh = tiny_shape()
+    p = S.default_params()
+    h = ctypes.c_void_p()
+    # NULL / misaligned workspace fail before touching the device
+    assert lib.sparsepr_plan_create(ctypes.byref(sh), ctypes.byref(p), None, 0, ctypes.byref(h)) == 1
+    assert lib.sparsepr_plan_create(ctypes.byref(sh), ctypes.byref(p), ctypes.c_void_p(16), 1 << 30,
+                                    ctypes.byref(h)) == 1
+    # too small a workspace
+    assert lib.sparsepr_plan_create(ctypes.byref(sh), ctypes.byref(p), ctypes.c_void_p(1 << 20), 256,
+                                    ctypes.byref(h)) == 3
+    assert "needs" in lib.sparsepr_last_error().decode()
