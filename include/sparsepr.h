@@ -207,6 +207,28 @@ sparsepr_status sparsepr_plan_export(sparsepr_plan_t plan, int32_t bh, sparsepr_
 sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const sparsepr_plan_host* in,
                                      void* stream);
 
+/* Device time per phase, measured with HIP events recorded on the call's
+ * stream around each phase (Sec. 4.3 lists what a call's latency covers).
+ * Accumulated over the calls made while profiling was enabled. */
+typedef struct {
+  double plan_ms;         /* partitioning, routing and probe choice */
+  double sparse_attn_ms;  /* the block-sparse attention kernel alone */
+  double probe_ms;        /* exact probe rows and their merge */
+  double fit_ms;          /* residual fit */
+  double correct_ms;      /* correction, restore and probe rows */
+  int32_t plan_calls;
+  int32_t attend_calls;
+} sparsepr_timings;
+
+/* Enable (1) or disable (0) event timing on this handle.  Creating the events
+ * is the only thing it does; no device memory is allocated. */
+sparsepr_status sparsepr_set_profiling(sparsepr_plan_t plan, int32_t enable);
+
+/* Synchronise `stream`, write the accumulated timings, and reset them when
+ * `reset` is nonzero.  INVALID_ARGUMENT when profiling is not enabled. */
+sparsepr_status sparsepr_get_timings(sparsepr_plan_t plan, sparsepr_timings* out, int32_t reset,
+                                     void* stream);
+
 /* Release the handle (not the workspace).  NULL is ignored. */
 void sparsepr_plan_destroy(sparsepr_plan_t plan);
 

@@ -62,6 +62,10 @@ def _f64(a):
     return np.ascontiguousarray(a, dtype=np.float64)
 
 
+def num_threads() -> int:
+    return int(lib().or_num_threads())
+
+
 def dense_rows(q, k, v, rows=None):
     q, k, v = _f32(q), _f32(k), _f32(v)
     n, d = q.shape

@@ -21,6 +21,9 @@
 extern "C" {
 #endif
 
+/* OpenMP threads the oracle runs on. */
+int or_num_threads(void);
+
 /* Dense attention rows (Sec. 3, eq. dense_attention). out: n_rows x dv. */
 void or_dense_rows(const float* q, const float* k, const float* v, int n_k, int d, int dv,
                    const int64_t* rows, int n_rows, double* out);

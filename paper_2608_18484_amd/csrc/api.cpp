@@ -200,7 +200,46 @@ struct sparsepr_plan_s {
   char* base;
   size_t bytes;
   bool planned;
+  // event timing (sparsepr_set_profiling): a ring of event sets, so timed
+  // loops of up to kRing calls need no host synchronisation
+  static constexpr int kRing = 64;
+  bool profiling = false;
+  hipEvent_t ev_plan[kRing][2] = {};
+  hipEvent_t ev_att[kRing][5] = {};
+  int n_plan = 0, n_att = 0;  // pending (recorded, not yet harvested) calls
+  sparsepr_timings acc{};
 };
+
+namespace {
+
+void destroy_events(sparsepr_plan_s* p) {
+  for (auto& set : p->ev_plan)
+    for (auto& e : set)
+      if (e) (void)hipEventDestroy(e), e = nullptr;
+  for (auto& set : p->ev_att)
+    for (auto& e : set)
+      if (e) (void)hipEventDestroy(e), e = nullptr;
+  p->profiling = false;
+}
+
+// Fold the pending events into the totals (the stream has been synchronised).
+void harvest(sparsepr_plan_s* p) {
+  float ms = 0.f;
+  for (int i = 0; i < p->n_plan; ++i)
+    if (hipEventElapsedTime(&ms, p->ev_plan[i][0], p->ev_plan[i][1]) == hipSuccess) {
+      p->acc.plan_ms += ms;
+      p->acc.plan_calls += 1;
+    }
+  double* dst[4] = {&p->acc.sparse_attn_ms, &p->acc.probe_ms, &p->acc.fit_ms, &p->acc.correct_ms};
+  for (int i = 0; i < p->n_att; ++i) {
+    for (int k = 0; k < 4; ++k)
+      if (hipEventElapsedTime(&ms, p->ev_att[i][k], p->ev_att[i][k + 1]) == hipSuccess) *dst[k] += ms;
+    p->acc.attend_calls += 1;
+  }
+  p->n_plan = p->n_att = 0;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -272,7 +311,17 @@ sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr
 sparsepr_status sparsepr_plan(sparsepr_plan_t plan, const void* q, const void* k, void* stream) {
   if (!plan || !q || !k) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan, q and k must not be NULL");
   (void)hipGetLastError();  // report only this call's launch errors
+  hipEvent_t* ev = nullptr;
+  if (plan->profiling) {
+    if (plan->n_plan == sparsepr_plan_s::kRing) {
+      (void)hipStreamSynchronize((hipStream_t)stream);
+      harvest(plan);
+    }
+    ev = plan->ev_plan[plan->n_plan++];
+    (void)hipEventRecord(ev[0], (hipStream_t)stream);
+  }
   launch_plan(plan->g, plan->w, q, k, (hipStream_t)stream);
+  if (ev) (void)hipEventRecord(ev[1], (hipStream_t)stream);
   const sparsepr_status st = hip_check(hipGetLastError(), "sparsepr_plan launch");
   if (st != SPARSEPR_OK) return st;
   plan->planned = true;
@@ -285,7 +334,15 @@ sparsepr_status sparsepr_attend(sparsepr_plan_t plan, const void* q, const void*
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan, q, k, v and out must not be NULL");
   if (!plan->planned) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "no plan: call sparsepr_plan or sparsepr_plan_import first");
   (void)hipGetLastError();
-  launch_attend(plan->g, plan->w, q, k, v, out, (hipStream_t)stream);
+  hipEvent_t* ev = nullptr;
+  if (plan->profiling) {
+    if (plan->n_att == sparsepr_plan_s::kRing) {
+      (void)hipStreamSynchronize((hipStream_t)stream);
+      harvest(plan);
+    }
+    ev = plan->ev_att[plan->n_att++];
+  }
+  launch_attend(plan->g, plan->w, q, k, v, out, (hipStream_t)stream, ev);
   const sparsepr_status st = hip_check(hipGetLastError(), "sparsepr_attend launch");
   if (st != SPARSEPR_OK) return st;
   return ok();
@@ -495,7 +552,52 @@ sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const spa
   return ok();
 }
 
-void sparsepr_plan_destroy(sparsepr_plan_t plan) { delete plan; }
+sparsepr_status sparsepr_set_profiling(sparsepr_plan_t plan, int32_t enable) {
+  if (!plan) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan must not be NULL");
+  if (!enable) {
+    destroy_events(plan);
+    return ok();
+  }
+  if (plan->profiling) return ok();
+  for (auto& set : plan->ev_plan)
+    for (auto& e : set) {
+      const sparsepr_status st = hip_check(hipEventCreate(&e), "hipEventCreate");
+      if (st != SPARSEPR_OK) {
+        destroy_events(plan);
+        return st;
+      }
+    }
+  for (auto& set : plan->ev_att)
+    for (auto& e : set) {
+      const sparsepr_status st = hip_check(hipEventCreate(&e), "hipEventCreate");
+      if (st != SPARSEPR_OK) {
+        destroy_events(plan);
+        return st;
+      }
+    }
+  plan->acc = sparsepr_timings{};
+  plan->n_plan = plan->n_att = 0;
+  plan->profiling = true;
+  return ok();
+}
+
+sparsepr_status sparsepr_get_timings(sparsepr_plan_t plan, sparsepr_timings* out, int32_t reset,
+                                     void* stream) {
+  if (!plan || !out) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan and out must not be NULL");
+  if (!plan->profiling) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "profiling is not enabled");
+  const sparsepr_status st = hip_check(hipStreamSynchronize((hipStream_t)stream), "hipStreamSynchronize");
+  if (st != SPARSEPR_OK) return st;
+  harvest(plan);
+  *out = plan->acc;
+  if (reset) plan->acc = sparsepr_timings{};
+  return ok();
+}
+
+void sparsepr_plan_destroy(sparsepr_plan_t plan) {
+  if (!plan) return;
+  destroy_events(plan);
+  delete plan;
+}
 
 const char* sparsepr_last_error(void) { return g_last_error.c_str(); }
 

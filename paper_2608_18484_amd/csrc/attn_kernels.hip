@@ -823,29 +823,37 @@ static AttnArgs make_args(const Work* w, const void* q, const void* k, const voi
 
 template <int D>
 static void attend_d(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
-                     void* out, hipStream_t s) {
+                     void* out, hipStream_t s, hipEvent_t* ev) {
   const AttnArgs a = make_args(&w, q, k, v, out);
   const dim3 gs(g.nchunk_max, g.BH);
   const dim3 gp((g.M + 63) / 64, g.nsplit, g.BH);
-  if (g.bf16) {
+  if (ev) (void)hipEventRecord(ev[0], s);
+  if (g.bf16)
     k_attn_bf16<D, MODE_SPARSE><<<gs, 128, 0, s>>>(g, a);
-    if (g.M > 0) k_attn_bf16<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
-  } else {
+  else
     k_attn_f32<D, MODE_SPARSE><<<gs, 64, 0, s>>>(g, a);
-    if (g.M > 0) k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(g, a);
+  if (ev) (void)hipEventRecord(ev[1], s);
+  if (g.M > 0) {
+    if (g.bf16)
+      k_attn_bf16<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
+    else
+      k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(g, a);
+    k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
   }
-  if (g.M > 0) k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
+  if (ev) (void)hipEventRecord(ev[2], s);
   k_fit<D><<<g.BH, 1024, 0, s>>>(g, w);
+  if (ev) (void)hipEventRecord(ev[3], s);
   k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(g, w, out);
   if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w, out);
+  if (ev) (void)hipEventRecord(ev[4], s);
 }
 
 void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
-                   void* out, hipStream_t s) {
+                   void* out, hipStream_t s, hipEvent_t* ev) {
   if (g.d == 64)
-    attend_d<64>(g, w, q, k, v, out, s);
+    attend_d<64>(g, w, q, k, v, out, s, ev);
   else
-    attend_d<128>(g, w, q, k, v, out, s);
+    attend_d<128>(g, w, q, k, v, out, s, ev);
 }
 
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,

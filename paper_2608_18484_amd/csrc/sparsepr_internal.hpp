@@ -113,8 +113,11 @@ void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hip
 // z and probes already placed in the workspace for head bh (import path).
 void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s);
 // ---- attend kernels -----------------------------------------------------
+// Optional events recorded between the phases of attend (null = none):
+// ev[0] before the sparse attention, ev[1] after it, ev[2] after the probe
+// rows, ev[3] after the fit, ev[4] after the correction.
 void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
-                   void* out, hipStream_t s);
+                   void* out, hipStream_t s, hipEvent_t* ev = nullptr);
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
                   float* part, hipStream_t s);
 

@@ -48,6 +48,13 @@ class Stats(ctypes.Structure):
                 ("status_flags", ctypes.c_int32)]
 
 
+class Timings(ctypes.Structure):
+    _fields_ = [("plan_ms", ctypes.c_double), ("sparse_attn_ms", ctypes.c_double),
+                ("probe_ms", ctypes.c_double), ("fit_ms", ctypes.c_double),
+                ("correct_ms", ctypes.c_double), ("plan_calls", ctypes.c_int32),
+                ("attend_calls", ctypes.c_int32)]
+
+
 _P = ctypes.c_void_p
 HOST_FIELDS = [
     ("labels_q", "i4"), ("labels_kv", "i4"), ("routes", "u1"), ("probes", "i4"),
@@ -68,7 +75,8 @@ class PlanHost(ctypes.Structure):
 EXPORTED = ["sparsepr_params_default", "sparsepr_workspace_size", "sparsepr_plan_create",
             "sparsepr_plan", "sparsepr_attend", "sparsepr_dense_workspace_size",
             "sparsepr_dense_attend", "sparsepr_get_stats", "sparsepr_plan_export",
-            "sparsepr_plan_import", "sparsepr_plan_destroy", "sparsepr_last_error"]
+            "sparsepr_plan_import", "sparsepr_set_profiling", "sparsepr_get_timings",
+            "sparsepr_plan_destroy", "sparsepr_last_error"]
 
 _lib = None
 
@@ -178,6 +186,15 @@ class SparsePR:
         s = Stats()
         _check(lib().sparsepr_get_stats(self.handle, ctypes.byref(s), _stream(stream)))
         return {name: getattr(s, name) for name, _ in Stats._fields_}
+
+    def set_profiling(self, enable=True):
+        _check(lib().sparsepr_set_profiling(self.handle, ctypes.c_int32(int(enable))))
+
+    def timings(self, reset=True, stream=None) -> dict:
+        t = Timings()
+        _check(lib().sparsepr_get_timings(self.handle, ctypes.byref(t), ctypes.c_int32(int(reset)),
+                                          _stream(stream)))
+        return {name: getattr(t, name) for name, _ in Timings._fields_}
 
     def _sizes(self):
         sh, p = self.shape, self.params

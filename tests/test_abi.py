@@ -35,7 +35,8 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layout_matches_c_compiler(tmp_path):
     # the binding's structs must have the C layout the header gives them
     structs = {"sparsepr_shape": S.Shape, "sparsepr_params": S.Params,
-               "sparsepr_stats": S.Stats, "sparsepr_plan_host": S.PlanHost}
+               "sparsepr_stats": S.Stats, "sparsepr_plan_host": S.PlanHost,
+               "sparsepr_timings": S.Timings}
     lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', 'int main(void) {']
     for cname, cls in structs.items():
         lines.append(f'printf("{cname} %zu\\n", sizeof({cname}));')
@@ -110,6 +111,8 @@ def test_null_arguments_rejected():
     assert lib.sparsepr_get_stats(None, None, None) == 1
     assert lib.sparsepr_plan_export(None, 0, None, None) == 1
     assert lib.sparsepr_plan_import(None, 0, None, None) == 1
+    assert lib.sparsepr_set_profiling(None, 1) == 1
+    assert lib.sparsepr_get_timings(None, None, 0, None) == 1
     lib.sparsepr_plan_destroy(None)
     sh = tiny_shape()
     p = S.default_params()
