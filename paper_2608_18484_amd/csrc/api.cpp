@@ -78,6 +78,14 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->offq, (size_t)(g.CQt + 1) * 4);
   add(&w->blkhist, (size_t)g.nsort_blk_full * g.cmax * 4);
   add(&w->kmstate, (size_t)2 * (g.T + 1) * 4);
+  add(&w->km_xhi, NV * g.rpad * 2);
+  add(&w->km_xlo, NV * g.rpad * 2);
+  add(&w->km_xn, NV * 4);
+  add(&w->km_chi, (size_t)g.cpad * g.rpad * 2);
+  add(&w->km_clo, (size_t)g.cpad * g.rpad * 2);
+  add(&w->km_cu, (size_t)g.cpad * 4);
+  add(&w->km_fb, NV * 4);
+  add(&w->km_fbcnt, (size_t)2 * g.T * 4);
   add(&w->kbar, (size_t)g.CK * d * 4);
   add(&w->qbar, (size_t)g.CQ * d * 4);
   add(&w->prio, (size_t)g.CQ * g.CK * 4);
@@ -95,6 +103,8 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->pw, M * 4);
   add(&w->nprobes, 4);
   add(&w->picks, M * 4);
+  add(&w->kperm, g.bf16 ? N * d * 2 : 0);
+  add(&w->vperm, g.bf16 ? N * dv * 2 : 0);
   add(&w->osp, N * dv * 4);
   add(&w->odp, M * dv * 4);
   add(&w->part, M * g.nsplit * (dv + 2) * 4);
@@ -184,10 +194,13 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.budget = (int64_t)std::floor((double)p->target_exec_density * (double)NV * (double)NV) -
              (int64_t)g.M * (int64_t)N;
   g.nchunk_max = (N + kQTile - 1) / kQTile + g.CQt;
+  g.nchunk_per_xcd = (g.nchunk_max + 7) / 8;
   g.nsplit = (N + kProbeSplit - 1) / kProbeSplit;
   g.nsort_blk = (NV + kSortBlock - 1) / kSortBlock;
   g.nsort_blk_full = (N + kSortBlock - 1) / kSortBlock;
   g.cmax = std::max(g.CKt, g.CQt);
+  g.rpad = (std::max(g.rk, g.rq) + 15) / 16 * 16;
+  g.cpad = (std::max(g.CK, g.CQ) + 31) / 32 * 32;
   return SPARSEPR_OK;
 }
 

@@ -46,6 +46,8 @@ struct AttnArgs {
   const int32_t* rng_cnt;
   const int32_t* probes;
   const int32_t* nprobes;
+  const uint16_t* kperm;
+  const uint16_t* vperm;
 };
 
 // Where the rows and keys of one block come from.
@@ -114,32 +116,101 @@ __device__ __forceinline__ int key_row(const Geom& g, const AttnArgs& A, int bh,
   return A.permk[(size_t)bh * g.N + rg[cur.j].x + (f - cur.cum)];
 }
 
-// Slot of key k (0..15) inside its 16-key chunk of the transposed V tile:
-// the accumulator of a 32x32 MFMA holds keys (i/4)*8 + h*4 + i%4 in lane half
-// h, register i; registers 0..7 of half h become operand slots h*8 + 0..7.
-__device__ __forceinline__ int vslot(int k) { return ((k >> 2) & 1) * 8 + (k >> 3) * 4 + (k & 3); }
+// Bank swizzle of the 16-byte chunks of a K/V tile row in LDS: chunk c of
+// key r sits at position c ^ swz(r) (low three bits), so 8 consecutive keys
+// reading one chunk (the K operand) and 4 consecutive keys reading two
+// neighbouring chunks (the transposed V reads) hit distinct banks.
+__device__ __forceinline__ int kv_swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
 
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// LDS transposing read of four 16-bit values.  In every group of 16 lanes,
+// lane j receives element j%4 of the 8-byte rows addressed by lanes
+// j/4, j/4+4, j/4+8, j/4+12 of its group.
+__device__ __forceinline__ v4i16 lds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16*)(__attribute__((address_space(3))) uint16_t*)(p));
+}
+
+// Direct global->LDS copy of 16 bytes per lane: lane l's bytes land at
+// lds_base + 16*l (lds_base must be the same for the whole wave).  Issued as
+// inline assembly so that the compiler adds no waits for it; callers order it
+// with explicit s_waitcnt vmcnt.  Nothing else in these kernels uses M0.
+__device__ __forceinline__ void g2lds16(const void* src, const void* lds_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)lds_base);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds)
+               : "memory");
+}
+
+// Block-sparse flash attention, bf16 MFMA, fp32 accumulation.
+//  * 128 threads = 2 waves; a block owns up to 64 query rows (32 per wave)
+//    that share one key list: the routed ranges of their query group in the
+//    group-major K/V copy (MODE_SPARSE), or a contiguous slice of the original
+//    K/V rows (MODE_PROBE, MODE_DENSE).
+//  * 32-key tiles, double-buffered in LDS and filled by direct global->LDS
+//    16-byte loads issued one tile ahead; the key positions of a tile are
+//    computed two tiles ahead into a ring of three slots.
+//  * S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_32x32x16_bf16; V^T
+//    fragments come from the row-major V tile through transposing LDS reads.
+//  * Online softmax in base 2 with lazy rescaling: the running maximum only
+//    moves (and O, l are rescaled) when a tile's maximum exceeds it by 2^8.
 template <int D, int MODE>
-__global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
-  constexpr int KT = 64;
-  constexpr int KLD = D + 8;   // K tile row stride (bf16 elements)
-  constexpr int VLD = KT + 8;  // V^T tile row stride
-  constexpr int NKS = D / 16;  // k-steps of the QK^T contraction
-  constexpr int NDB = D / 32;  // 32-wide output blocks of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KLD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VLD];
-  __shared__ int srcrow[KT];
-  const int bh = (MODE == MODE_PROBE) ? blockIdx.z : blockIdx.y;
-  Work1 w;
-  if (!get_work<MODE>(g, A, bh, w)) return;
+__global__ __launch_bounds__(128) void k_attn_mfma(Geom g, AttnArgs A) {
+  constexpr int KT = 32;
+  constexpr int CH = D / 8;                    // 16-byte chunks per row
+  constexpr int NKS = D / 16;                  // k-steps of Q K^T
+  constexpr int NDB = D / 32;                  // 32-wide blocks of O^T
+  constexpr int LPT = KT * CH / 128;           // 16-byte loads per thread per tensor per tile
+  constexpr int MAXR = 1024;                   // routed ranges staged in LDS
+  __shared__ __attribute__((aligned(1024))) uint16_t Kb0[KT * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t Kb1[KT * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t Vb0[KT * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t Vb1[KT * D];
+  __shared__ int spos[3][KT];
+  __shared__ int2 srng[MODE == MODE_SPARSE ? MAXR : 1];
+
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
-  const int64_t base = head_base(g, bh);
-  const uint16_t* Kp = (const uint16_t*)A.k + base;
-  const uint16_t* Vp = (const uint16_t*)A.v + base;
-  const uint16_t* Qp = (const uint16_t*)A.q + base;
+  Work1 w;
+  int bh;
+  const uint16_t* Kp;
+  const uint16_t* Vp;
+  if (MODE == MODE_SPARSE) {
+    // XCD-aware order: hardware block b runs on XCD b % 8; XCD x takes the
+    // contiguous slice [x*per, (x+1)*per) of the head's chunks, so spatially
+    // adjacent query groups (which route to overlapping K/V groups) share an
+    // L2, and all XCDs work on the same head at a time.
+    bh = blockIdx.y;
+    const int nch = A.nchunks[bh];
+    const int per = (nch + 7) / 8;
+    const int x = blockIdx.x & 7, y = blockIdx.x >> 3;
+    const int cx = x * per + y;
+    if (y >= per || cx >= nch) return;
+    const int4 c = A.chunks[(size_t)bh * g.nchunk_max + cx];
+    w.a = c.x;
+    w.rbase = A.offq[(size_t)bh * (g.CQt + 1) + c.x] + c.y;
+    w.nrows = c.z;
+    w.nkeys = c.w;
+    w.k0 = 0;
+    if (w.nrows <= 0 || w.nkeys <= 0) return;
+    Kp = A.kperm + (size_t)bh * g.N * D;
+    Vp = A.vperm + (size_t)bh * g.N * D;
+  } else {
+    bh = (MODE == MODE_PROBE) ? blockIdx.z : blockIdx.y;
+    if (!get_work<MODE>(g, A, bh, w)) return;
+    const int64_t base = head_base(g, bh);
+    Kp = (const uint16_t*)A.k + base;
+    Vp = (const uint16_t*)A.v + base;
+  }
+  const int64_t ksn = (MODE == MODE_SPARSE) ? D : g.sn;  // row stride of Kp/Vp
+  const int64_t qbase = head_base(g, bh);
+  const uint16_t* Qp = (const uint16_t*)A.q + qbase;
 
-  // this lane's query row and its B operands (16 dims per k-step)
+  // query row of this lane and its B operands
   const int qr = wv * 32 + n;
   const bool qvalid = qr < w.nrows;
   const int qrow = qvalid ? row_of<MODE>(g, A, bh, w, qr) : 0;
@@ -152,13 +223,57 @@ __global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
   }
   const bool wave_active = wv * 32 < w.nrows;
 
-  const int2* rg = nullptr;
+  // routed ranges of the query group (positions in the group-major K/V),
+  // staged in LDS when they fit; never read through generic pointers (flat
+  // accesses would make the compiler wait for the in-flight tile loads)
+  typedef const __attribute__((address_space(1))) int* gptr_int;
+  gptr_int grng = nullptr;
   int nr = 0;
   if (MODE == MODE_SPARSE) {
-    rg = A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt;
+    grng = (gptr_int)(A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt);
     nr = A.rng_cnt[(size_t)bh * g.CQt + w.a];
+    for (int i = tid; i < min(nr, MAXR); i += 128) srng[i] = make_int2(grng[2 * i], grng[2 * i + 1]);
+    __syncthreads();
   }
+  const bool rng_in_lds = nr <= MAXR;
+  auto range_at = [&](int j) -> int2 {
+    if (rng_in_lds) return srng[j];
+    return make_int2(grng[2 * j], grng[2 * j + 1]);
+  };
+  const int safe_pos = (MODE == MODE_SPARSE) ? range_at(0).x : w.k0;
   KeyCursor cur{0, 0};
+  auto fill_pos = [&](int tt) {  // key positions of tile tt -> ring slot tt % 3
+    if (tid < KT) {
+      const int f = tt * KT + tid;
+      int pos = safe_pos;
+      if (f < w.nkeys) {
+        if (MODE == MODE_SPARSE) {
+          int2 r = range_at(cur.j);
+          while (f >= cur.cum + r.y && cur.j + 1 < nr) {
+            cur.cum += r.y;
+            ++cur.j;
+            r = range_at(cur.j);
+          }
+          pos = r.x + (f - cur.cum);
+        } else {
+          pos = w.k0 + f;
+        }
+      }
+      spos[tt % 3][tid] = pos;
+    }
+  };
+  auto issue_loads = [&](int tt, uint16_t* kb, uint16_t* vb) {  // tile tt -> (kb, vb)
+#pragma unroll
+    for (int u = 0; u < LPT; ++u) {
+      const int inst = wv * LPT + u;
+      const int s = inst * 64 + lane;
+      const int key = s / CH, p = s % CH;
+      const int c8 = p ^ kv_swz(key);
+      const int64_t off = (int64_t)spos[tt % 3][key] * ksn + c8 * 8;
+      g2lds16(Kp + off, kb + inst * 512);
+      g2lds16(Vp + off, vb + inst * 512);
+    }
+  };
 
   const float sl2 = 1.4426950408889634f / sqrtf((float)D);
   float m_run = -INFINITY, l_run = 0.f;
@@ -167,108 +282,95 @@ __global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) O[db][i] = 0.f;
+  // s_waitcnt immediate (gfx9 encoding) waiting for lgkmcnt(0) only
+  constexpr int kWaitLgkm0 = 0xC07F;
 
   const int ntile = (w.nkeys + KT - 1) / KT;
-  for (int t = 0; t < ntile; ++t) {
-    if (tid < KT) {
-      const int f = t * KT + tid;
-      srcrow[tid] = (f < w.nkeys) ? key_row<MODE>(g, A, bh, w, f, cur, rg, nr) : -1;
-    }
-    __syncthreads();
-    // K tile: 16-byte pieces, rows contiguous across lanes
-#pragma unroll
-    for (int u = 0; u < KT * D / 8 / 128; ++u) {
-      const int p = tid + 128 * u;
-      const int row = p / (D / 8), c8 = p % (D / 8);
-      const int src = srcrow[row];
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (src >= 0) val = *(const uint4*)(Kp + (int64_t)src * g.sn + c8 * 8);
-      *(uint4*)(Ks + row * KLD + c8 * 8) = val;
-    }
-    // V tile, transposed: a thread takes two adjacent keys (same 16-key chunk
-    // slots s, s+1) and 8 dims, and stores 8 packed key pairs
-#pragma unroll
-    for (int u = 0; u < KT * D / 16 / 128; ++u) {
-      const int p = tid + 128 * u;
-      const int pp = p % (KT / 2), c8 = p / (KT / 2);
-      const int k0 = 2 * pp;
-      const int s0 = srcrow[k0], s1 = srcrow[k0 + 1];
-      uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-      if (s0 >= 0) v0 = *(const uint4*)(Vp + (int64_t)s0 * g.sn + c8 * 8);
-      if (s1 >= 0) v1 = *(const uint4*)(Vp + (int64_t)s1 * g.sn + c8 * 8);
-      const int pos = (k0 & ~15) + vslot(k0 & 15);
-      const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
-      const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = (a0[e] & 0xffffu) | (a1[e] << 16);
-        const uint32_t hi = (a0[e] >> 16) | (a1[e] & 0xffff0000u);
-        *(uint32_t*)(Vt + (c8 * 8 + 2 * e) * VLD + pos) = lo;
-        *(uint32_t*)(Vt + (c8 * 8 + 2 * e + 1) * VLD + pos) = hi;
-      }
-    }
-    __syncthreads();
+  // One step: compute tile t from (kt, vt) while tile t + 1 loads into (kn, vn).
+  auto step = [&](int t, const uint16_t* kt, const uint16_t* vt, uint16_t* kn, uint16_t* vn) {
+    // Plain s_barrier (no fence): a fence would also wait for the tile t+1
+    // loads just issued.  Ordering is explicit instead: each wave waits for
+    // its own loads of tile t and for its LDS writes before the barrier.
+    if (t + 1 < ntile) issue_loads(t + 1, kn, vn);
+    if (t + 2 < ntile) fill_pos(t + 2);
+    if (t + 1 < ntile)
+      __builtin_amdgcn_s_waitcnt(0x3f70 | (2 * LPT));  // vmcnt(2*LPT): tile t has landed
+    else
+      __builtin_amdgcn_s_waitcnt(0x3f70);              // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
     if (wave_active) {
-      // S^T for 64 keys x 32 queries: two 32-key blocks
-      f32x16 S[2];
+      f32x16 S;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) S[kb][i] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const bf16x8 av =
-              __builtin_bit_cast(bf16x8, *(const uint4*)(Ks + (kb * 32 + n) * KLD + ks * 16 + h * 8));
-          S[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], S[kb], 0, 0, 0);
-        }
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int c8 = (2 * ks + h) ^ kv_swz(n);
+        const bf16x8 av = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
+        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], S, 0, 0, 0);
       }
-      // online softmax (base 2); key of register i: kb*32 + (i/4)*8 + h*4 + i%4
-      const bool tail = (t + 1) * KT > w.nkeys;
+      // register i holds key (i/4)*8 + h*4 + i%4 of the tile
       float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      if ((t + 1) * KT > w.nkeys) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float s = S[kb][i] * sl2;
-          if (tail) {
-            const int key = t * KT + kb * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
-            if (key >= w.nkeys) s = -INFINITY;
-          }
-          S[kb][i] = s;
-          mt = fmaxf(mt, s);
+          const int key = t * KT + (i >> 2) * 8 + h * 4 + (i & 3);
+          if (key >= w.nkeys) S[i] = -INFINITY;
         }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mt = fmaxf(mt, S[i]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      const bool need = mt > m_run + 8.f;
+      if (__ballot(need)) {
+        const float m_new = need ? mt : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) O[db][i] *= alpha;
+      }
+      bf16x8 P[2];
       float ls = 0.f;
-      bf16x8 P[4];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(S[c * 8 + e], sl2, -m_run));
+          ls += p;
+          P[c][e] = (__bf16)p;
+        }
+      l_run += ls;
+      // O^T += V^T P^T: two 16-key chunks, V^T fragments by transposing reads
+      const int grp = lane >> 4, gl = lane & 15;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float p = __builtin_amdgcn_exp2f(S[kb][hh * 8 + e] - m_new);
-            ls += p;
-            P[kb * 2 + hh][e] = (__bf16)p;
-          }
-      l_run = l_run * alpha + ls;
+      for (int db = 0; db < NDB; ++db) {
+        const int dv = db * 32 + 16 * (grp & 1) + 4 * (gl & 3);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) O[db][i] *= alpha;
-      // O^T += V^T P^T over four 16-key chunks
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const bf16x8 av =
-              __builtin_bit_cast(bf16x8, *(const uint4*)(Vt + (db * 32 + n) * VLD + c * 16 + h * 8));
+        for (int c = 0; c < 2; ++c) {
+          const int key0 = 16 * c + 4 * h + (gl >> 2);
+          const int key1 = key0 + 8;
+          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz(key0))) * 8 + (dv & 7));
+          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz(key1))) * 8 + (dv & 7));
+          const bf16x8 av = __builtin_bit_cast(
+              bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
           O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, P[c], O[db], 0, 0, 0);
         }
+      }
     }
-    __syncthreads();
+    // every wave is done with this buffer before tile t + 2 is loaded into it
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+  };
+  fill_pos(0);
+  if (ntile > 1) fill_pos(1);
+  __syncthreads();
+  issue_loads(0, Kb0, Vb0);
+  for (int t = 0; t < ntile; t += 2) {
+    step(t, Kb0, Vb0, Kb1, Vb1);
+    if (t + 1 < ntile) step(t + 1, Kb1, Vb1, Kb0, Vb0);
   }
   if (!qvalid) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -299,7 +401,7 @@ __global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
                                              O[db][i4 * 4 + 2] * inv, O[db][i4 * 4 + 3] * inv);
         }
     } else {
-      uint16_t* dst = (uint16_t*)A.out + base + (int64_t)qrow * g.sn;
+      uint16_t* dst = (uint16_t*)A.out + qbase + (int64_t)qrow * g.sn;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -307,12 +409,30 @@ __global__ __launch_bounds__(128) void k_attn_bf16(Geom g, AttnArgs A) {
           const int dv = db * 32 + i4 * 8 + h * 4;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const __bf16 b = (__bf16)(O[db][i4 * 4 + e] * inv);
-            dst[dv + e] = __builtin_bit_cast(uint16_t, b);
+            const __bf16 bv = (__bf16)(O[db][i4 * 4 + e] * inv);
+            dst[dv + e] = __builtin_bit_cast(uint16_t, bv);
           }
         }
     }
   }
+}
+
+// Group-major copies of K and V (Sec. 4.3): position p of head bh holds row
+// perm_kv[p].  Each row is moved as 16-byte pieces.
+template <int D>
+__global__ __launch_bounds__(256) void k_permute_kv(Geom g, const void* k, const void* v,
+                                                    const int32_t* permk, uint16_t* kperm,
+                                                    uint16_t* vperm) {
+  constexpr int CH = D / 8, RPB = 256 / CH;
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int p = blockIdx.x * RPB + tid / CH, c = tid % CH;
+  if (p >= g.N) return;
+  const int64_t base = head_base(g, bh);
+  const int src = permk[(size_t)bh * g.N + p];
+  const uint4 kv = *(const uint4*)((const uint16_t*)k + base + (int64_t)src * g.sn + c * 8);
+  const uint4 vv = *(const uint4*)((const uint16_t*)v + base + (int64_t)src * g.sn + c * 8);
+  *(uint4*)(kperm + ((size_t)bh * g.N + p) * D + c * 8) = kv;
+  *(uint4*)(vperm + ((size_t)bh * g.N + p) * D + c * 8) = vv;
 }
 
 // fp32 variant (VALU): one thread per query row, 32-key tiles staged in LDS.
@@ -817,6 +937,8 @@ static AttnArgs make_args(const Work* w, const void* q, const void* k, const voi
     a.rng_cnt = w->rng_cnt;
     a.probes = w->probes;
     a.nprobes = w->nprobes;
+    a.kperm = w->kperm;
+    a.vperm = w->vperm;
   }
   return a;
 }
@@ -825,17 +947,21 @@ template <int D>
 static void attend_d(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
                      void* out, hipStream_t s, hipEvent_t* ev) {
   const AttnArgs a = make_args(&w, q, k, v, out);
-  const dim3 gs(g.nchunk_max, g.BH);
   const dim3 gp((g.M + 63) / 64, g.nsplit, g.BH);
+  if (g.bf16) {
+    constexpr int CH = D / 8;
+    k_permute_kv<D><<<dim3((g.N + 256 / CH - 1) / (256 / CH), g.BH), 256, 0, s>>>(
+        g, k, v, w.permk, w.kperm, w.vperm);
+  }
   if (ev) (void)hipEventRecord(ev[0], s);
   if (g.bf16)
-    k_attn_bf16<D, MODE_SPARSE><<<gs, 128, 0, s>>>(g, a);
+    k_attn_mfma<D, MODE_SPARSE><<<dim3(8 * g.nchunk_per_xcd, g.BH), 128, 0, s>>>(g, a);
   else
-    k_attn_f32<D, MODE_SPARSE><<<gs, 64, 0, s>>>(g, a);
+    k_attn_f32<D, MODE_SPARSE><<<dim3(g.nchunk_max, g.BH), 64, 0, s>>>(g, a);
   if (ev) (void)hipEventRecord(ev[1], s);
   if (g.M > 0) {
     if (g.bf16)
-      k_attn_bf16<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
+      k_attn_mfma<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
     else
       k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(g, a);
     k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
@@ -863,12 +989,12 @@ void launch_dense(const Geom& g, const void* q, const void* k, const void* v, vo
   const dim3 gd((g.N + 63) / 64, g.BH);
   if (g.d == 64) {
     if (g.bf16)
-      k_attn_bf16<64, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
+      k_attn_mfma<64, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
     else
       k_attn_f32<64, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
   } else {
     if (g.bf16)
-      k_attn_bf16<128, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
+      k_attn_mfma<128, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
     else
       k_attn_f32<128, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
   }

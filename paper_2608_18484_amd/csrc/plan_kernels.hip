@@ -29,6 +29,7 @@ __global__ void k_plan_init(Geom g, Work w) {
   for (int i = threadIdx.x; i < 16; i += blockDim.x) w.stats[bh * 16 + i] = 0;
   for (int i = threadIdx.x; i < 2 * (g.T + 1); i += blockDim.x)
     w.kmstate[bh * 2 * (g.T + 1) + i] = (i % (g.T + 1) == 0) ? 1 : 0;
+  for (int i = threadIdx.x; i < 2 * g.T; i += blockDim.x) w.km_fbcnt[bh * 2 * g.T + i] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -227,62 +228,65 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 // four threads per row.
 // ---------------------------------------------------------------------------
 
-template <int D>
+template <int D, int MAXR>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
                                                  int rms, float eps, float* phi, int64_t* stats) {
-  constexpr int ROWS = 64, MAXC = 32;
-  __shared__ float xs[ROWS][D + 1];
-  __shared__ float fs[D * 128];
+  // one row per thread; F (D x R) broadcast from LDS
+  __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
   const int bh = blockIdx.y, tid = threadIdx.x;
-  const int r0 = blockIdx.x * ROWS;
-  const int64_t base = head_base(g, bh);
   const float* Fh = F + (size_t)bh * D * R;
-  for (int i = tid; i < D * R; i += 256) fs[i] = Fh[i];
-  for (int i = tid; i < ROWS * D; i += 256) {
-    const int rr = i / D, c = i % D;
-    const int row = r0 + rr;
-    xs[rr][c] = (row < g.NV) ? load_x(x, g.bf16, base + (int64_t)(g.ntext + row) * g.sn + c) : 0.f;
-  }
+  for (int i = tid; i < D * R; i += 256) fs[(i / R) * MAXR + (i % R)] = Fh[i];
   __syncthreads();
-  const int rr = tid >> 2, part = tid & 3;
-  float acc[MAXC];
+  const int row = blockIdx.x * 256 + tid;
+  if (row >= g.NV) return;
+  const int64_t base = head_base(g, bh) + (int64_t)(g.ntext + row) * g.sn;
+  float acc[MAXR];
 #pragma unroll
-  for (int u = 0; u < MAXC; ++u) acc[u] = 0.f;
-  for (int k = 0; k < D; ++k) {
-    const float xk = xs[rr][k];
+  for (int c = 0; c < MAXR; ++c) acc[c] = 0.f;
+  for (int k0 = 0; k0 < D; k0 += 8) {
+    float xv[8];
+    if (g.bf16) {
+      const uint4 u = *(const uint4*)((const uint16_t*)x + base + k0);
+      const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = part + 4 * u;
-      if (c < R) acc[u] = fmaf(xk, fs[k * R + c], acc[u]);
+      for (int e = 0; e < 4; ++e) {
+        xv[2 * e] = __uint_as_float(wds[e] << 16);
+        xv[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+      }
+    } else {
+      const float4 u0 = *(const float4*)((const float*)x + base + k0);
+      const float4 u1 = *(const float4*)((const float*)x + base + k0 + 4);
+      xv[0] = u0.x; xv[1] = u0.y; xv[2] = u0.z; xv[3] = u0.w;
+      xv[4] = u1.x; xv[5] = u1.y; xv[6] = u1.z; xv[7] = u1.w;
+    }
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const float* fr = fs + (k0 + kk) * MAXR;
+#pragma unroll
+      for (int c = 0; c < MAXR; ++c)
+        if (c < R) acc[c] = fmaf(xv[kk], fr[c], acc[c]);
     }
   }
   float den = 1.f;
   if (rms) {
     float ss = 0.f;
 #pragma unroll
-    for (int u = 0; u < MAXC; ++u)
-      if (part + 4 * u < R) ss = fmaf(acc[u], acc[u], ss);
-    ss += __shfl_xor(ss, 1);
-    ss += __shfl_xor(ss, 2);
+    for (int c = 0; c < MAXR; ++c)
+      if (c < R) ss = fmaf(acc[c], acc[c], ss);
     den = fmaxf(sqrtf(ss / (float)R), eps);
   }
-  const int row = r0 + rr;
-  if (row < g.NV) {
-    float* out = phi + ((size_t)bh * g.NV + row) * R;
-    bool bad = false;
+  float* out = phi + ((size_t)bh * g.NV + row) * R;
+  bool bad = false;
 #pragma unroll
-    for (int u = 0; u < MAXC; ++u) {
-      const int c = part + 4 * u;
-      if (c < R) {
-        const float v = acc[u] / den;
-        bad |= !isfinite(v);
-        out[c] = v;
-      }
+  for (int c = 0; c < MAXR; ++c)
+    if (c < R) {
+      const float v = acc[c] / den;
+      bad |= !isfinite(v);
+      out[c] = v;
     }
-    if (bad)
-      atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
-               (unsigned long long)SPARSEPR_FLAG_NONFINITE_INPUT);
-  }
+  if (bad)
+    atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
+             (unsigned long long)SPARSEPR_FLAG_NONFINITE_INPUT);
 }
 
 // ---------------------------------------------------------------------------
@@ -302,6 +306,16 @@ struct KmArgs {
   int row0, N;
   int R, C;           // coordinate rank, groups
   int offstride, nblk, cmax, sel, T;
+  // MFMA screening of the assignment
+  uint16_t* xhi;      // [BH][n][RP]
+  uint16_t* xlo;
+  float* xn;          // [BH][n]
+  uint16_t* chi;      // [BH][CP][RP]
+  uint16_t* clo;
+  float* cu;          // [BH][CP]
+  int32_t* fb;        // [BH][n]
+  int32_t* fbcnt;     // [BH][2][T]
+  int RP, CP;         // rank padded to 16, groups padded to 32 (strides of the above)
 };
 
 __device__ __forceinline__ int32_t* km_changed(const KmArgs& a, int bh) {
@@ -310,6 +324,12 @@ __device__ __forceinline__ int32_t* km_changed(const KmArgs& a, int bh) {
 
 __device__ __forceinline__ bool km_skip(const KmArgs& a, int bh, int it) {
   return it >= 0 && km_changed(a, bh)[it] == 0;
+}
+
+// An assignment is skipped once the previous one changed no label: the
+// centroids, and hence every later assignment, are then final.
+__device__ __forceinline__ bool km_skip_assign(const KmArgs& a, int bh, int it) {
+  return it > 0 && km_changed(a, bh)[it - 1] == 0;
 }
 
 __global__ void k_km_init(KmArgs a) {
@@ -322,52 +342,210 @@ __global__ void k_km_init(KmArgs a) {
   a.cent[(size_t)bh * a.C * a.R + i] = a.pts[((size_t)bh * a.n + src) * a.R + c];
 }
 
-// Exact assignment: one point per thread, centroids staged through LDS.
+// ---- MFMA-screened exact assignment -------------------------------------
+// The assignment is defined by the exact float scores above.  To avoid
+// scanning every centroid on the VALU, the scores are first estimated with
+// bf16 MFMA on a three-term split (x = x_hi + x_lo, c = c_hi + c_lo;
+// t~ = x_hi c_hi + x_hi c_lo + x_lo c_hi) and bounded: the neglected terms
+// are below 3.1 * 2^-16 sum|x_k c_k|, the fp32 accumulation of the 3R exact
+// bf16 products and the exact float chain each below gamma_{3R} and
+// gamma_R times sum|x_k c_k|, so with |sum| <= |x||c| every estimated score
+// is within Delta = 1.6e-4 |x| c_max + 1.2e-7 u_max of the exact one (Delta
+// below carries another factor 2).  When the best estimate beats the
+// runner-up by more than 2 Delta, its centroid is the exact argmin; every
+// other point is rescored exactly by k_km_fallback.
+
+__device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
+  return __builtin_bit_cast(uint16_t, (__bf16)x);
+}
+
+// Points: bf16 hi/lo split (padded to RP with zeros) and norms; once per
+// k-means.
+__global__ __launch_bounds__(256) void k_km_prep_points(KmArgs a) {
+  const int bh = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= a.n) return;
+  const float* x = a.pts + ((size_t)bh * a.n + j) * a.R;
+  uint16_t* hi = a.xhi + ((size_t)bh * a.n + j) * a.RP;
+  uint16_t* lo = a.xlo + ((size_t)bh * a.n + j) * a.RP;
+  float ss = 0.f;
+  for (int k = 0; k < a.RP; ++k) {
+    const float v = k < a.R ? x[k] : 0.f;
+    const uint16_t h = bf16_rne_bits(v);
+    hi[k] = h;
+    lo[k] = bf16_rne_bits(v - bf16_bits_to_f32(h));
+    ss = fmaf(v, v, ss);
+  }
+  a.xn[(size_t)bh * a.n + j] = sqrtf(ss) * 1.000001f;
+}
+
+// Centroids: hi/lo split and exact squared norms (+inf for the padding rows).
+__global__ __launch_bounds__(64) void k_km_prep_cent(KmArgs a, int it) {
+  const int bh = blockIdx.y;
+  if (km_skip_assign(a, bh, it)) return;
+  const int b = blockIdx.x * 64 + threadIdx.x;
+  if (b >= a.CP) return;
+  uint16_t* hi = a.chi + ((size_t)bh * a.CP + b) * a.RP;
+  uint16_t* lo = a.clo + ((size_t)bh * a.CP + b) * a.RP;
+  float u = INFINITY;
+  if (b < a.C) {
+    const float* c = a.cent + ((size_t)bh * a.C + b) * a.R;
+    u = 0.f;
+    for (int k = 0; k < a.R; ++k) u = fmaf(c[k], c[k], u);
+    for (int k = 0; k < a.RP; ++k) {
+      const float v = k < a.R ? c[k] : 0.f;
+      const uint16_t h = bf16_rne_bits(v);
+      hi[k] = h;
+      lo[k] = bf16_rne_bits(v - bf16_bits_to_f32(h));
+    }
+  } else {
+    for (int k = 0; k < a.RP; ++k) hi[k] = lo[k] = 0;
+  }
+  a.cu[(size_t)bh * a.CP + b] = u;
+}
+
+// Screening: a block of 4 waves takes 128 points (32 per wave, the N side of
+// v_mfma_f32_32x32x16_bf16) against 32-centroid tiles staged in LDS (the M
+// side).  Lane (n, h) ends with the best and second-best estimate of point n
+// over half of the centroids; the halves are merged with one exchange.
+template <int RP>
+__global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
+  constexpr int KS = RP / 16;
+  constexpr int LD = RP + 8;  // padded LDS row (bf16)
+  __shared__ __attribute__((aligned(16))) uint16_t shi[32 * LD];
+  __shared__ __attribute__((aligned(16))) uint16_t slo[32 * LD];
+  __shared__ float su[32];
+  const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (km_skip_assign(a, bh, it)) return;
+  const int n = lane & 31, h = lane >> 5;
+  const int j = blockIdx.x * 128 + wv * 32 + n;
+  const int jc = min(j, a.n - 1);
+  bf16x8 bhi[KS], blo[KS];
+  const uint16_t* xh = a.xhi + ((size_t)bh * a.n + jc) * RP;
+  const uint16_t* xl = a.xlo + ((size_t)bh * a.n + jc) * RP;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    bhi[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xh + ks * 16 + h * 8));
+    blo[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
+  }
+  float best = INFINITY, second = INFINITY, umax = 0.f;
+  int bidx = -1;
+  const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
+  const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
+  const float* cu = a.cu + (size_t)bh * a.CP;
+  for (int c0 = 0; c0 < a.CP; c0 += 32) {
+    __syncthreads();
+    for (int i = tid; i < 32 * RP / 8; i += 256) {
+      const int r = i / (RP / 8), c8 = i % (RP / 8);
+      *(uint4*)(shi + r * LD + c8 * 8) = *(const uint4*)(chi + (size_t)(c0 + r) * RP + c8 * 8);
+      *(uint4*)(slo + r * LD + c8 * 8) = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
+    }
+    if (tid < 32) su[tid] = cu[c0 + tid];
+    __syncthreads();
+    f32x16 S;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const uint4*)(shi + n * LD + ks * 16 + h * 8));
+      const bf16x8 al = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bhi[ks], S, 0, 0, 0);
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, blo[ks], S, 0, 0, 0);
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bhi[ks], S, 0, 0, 0);
+    }
+    // register i holds centroid c0 + (i/4)*8 + h*4 + i%4 (ascending in i)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = (i >> 2) * 8 + h * 4 + (i & 3);
+      const float u = su[r];
+      const float sh = fmaf(-2.f, S[i], u);
+      if (c0 + r < a.C) umax = fmaxf(umax, u);
+      if (sh < best) {
+        second = best;
+        best = sh;
+        bidx = c0 + r;
+      } else {
+        second = fminf(second, sh);
+      }
+    }
+  }
+  const float ob = __shfl_xor(best, 32), os = __shfl_xor(second, 32);
+  const int oi = __shfl_xor(bidx, 32);
+  if (ob < best || (ob == best && oi < bidx)) {
+    second = fminf(best, os);
+    best = ob;
+    bidx = oi;
+  } else {
+    second = fminf(second, ob);
+  }
+  umax = fmaxf(umax, __shfl_xor(umax, 32));
+  if (h != 0 || j >= a.n) return;
+  const float xn = a.xn[(size_t)bh * a.n + j];
+  const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
+  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  if (second - best > 2.f * delta) {
+    const int old = lab[j];
+    lab[j] = bidx;
+    if (it > 0 && old != bidx) atomicAdd(&km_changed(a, bh)[it], 1);
+  } else {
+    int32_t* cnt = a.fbcnt + (size_t)bh * 2 * a.T + a.sel * a.T + it;
+    const int slot = atomicAdd(cnt, 1);
+    a.fb[(size_t)bh * a.n + slot] = j;
+  }
+}
+
+// Exact scan (the defining float score) for the points the screen could not
+// decide.  Blocks stride over the list; every thread takes one point.
 template <int MAXR>
-__global__ __launch_bounds__(256) void k_km_assign(KmArgs a, int it) {
+__global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
   constexpr int CB = 64;
   __shared__ float cs[CB][MAXR + 1];
   __shared__ float cu[CB];
   const int bh = blockIdx.y, tid = threadIdx.x;
-  int32_t* chg = km_changed(a, bh);
-  if (it > 0 && chg[it - 1] == 0) return;  // converged: labels and centroids are final
-  const int j = blockIdx.x * 256 + tid;
+  if (km_skip_assign(a, bh, it)) return;
+  const int cnt = a.fbcnt[(size_t)bh * 2 * a.T + a.sel * a.T + it];
   const int R = a.R;
-  float x[MAXR];
-  const float* pj = a.pts + ((size_t)bh * a.n + min(j, a.n - 1)) * R;
-#pragma unroll
-  for (int k = 0; k < MAXR; ++k) x[k] = (k < R) ? pj[k] : 0.f;
   const float* cent = a.cent + (size_t)bh * a.C * R;
-  float best = 0.f;
-  int bi = -1;
-  for (int c0 = 0; c0 < a.C; c0 += CB) {
-    const int cn = min(CB, a.C - c0);
-    __syncthreads();
-    for (int i = tid; i < cn * R; i += 256) cs[i / R][i % R] = cent[(size_t)c0 * R + i];
-    __syncthreads();
-    if (tid < cn) {
-      float u = 0.f;
-      for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
-      cu[tid] = u;
-    }
-    __syncthreads();
-    for (int b = 0; b < cn; ++b) {
-      float t = 0.f;
+  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  for (int base = blockIdx.x * 256; base < cnt; base += gridDim.x * 256) {
+    const int e = base + tid;
+    const int j = e < cnt ? a.fb[(size_t)bh * a.n + e] : 0;
+    float x[MAXR];
+    const float* pj = a.pts + ((size_t)bh * a.n + j) * R;
 #pragma unroll
-      for (int k = 0; k < MAXR; ++k)
-        if (k < R) t = fmaf(x[k], cs[b][k], t);
-      const float s = fmaf(-2.f, t, cu[b]);
-      if (bi < 0 || s < best) {
-        best = s;
-        bi = c0 + b;
+    for (int k = 0; k < MAXR; ++k) x[k] = (k < R) ? pj[k] : 0.f;
+    float best = 0.f;
+    int bi = -1;
+    for (int c0 = 0; c0 < a.C; c0 += CB) {
+      const int cn = min(CB, a.C - c0);
+      __syncthreads();
+      for (int i = tid; i < cn * R; i += 256) cs[i / R][i % R] = cent[(size_t)c0 * R + i];
+      __syncthreads();
+      if (tid < cn) {
+        float u = 0.f;
+        for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
+        cu[tid] = u;
+      }
+      __syncthreads();
+      if (e < cnt) {
+        for (int b = 0; b < cn; ++b) {
+          float t = 0.f;
+#pragma unroll
+          for (int k = 0; k < MAXR; ++k)
+            if (k < R) t = fmaf(x[k], cs[b][k], t);
+          const float sc = fmaf(-2.f, t, cu[b]);
+          if (bi < 0 || sc < best) {
+            best = sc;
+            bi = c0 + b;
+          }
+        }
       }
     }
-  }
-  if (j < a.n) {
-    int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-    const int old = lab[j];
-    lab[j] = bi;
-    if (it > 0 && old != bi) atomicAdd(&chg[it], 1);
+    if (e < cnt) {
+      const int old = lab[j];
+      lab[j] = bi;
+      if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
+    }
   }
 }
 
@@ -1054,21 +1232,60 @@ static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
   k_sort_scatter<<<dim3(a.nblk, BH), 64, a.C * sizeof(int), s>>>(a, it);
 }
 
-static void run_kmeans(const Geom& g, const KmArgs& a, hipStream_t s) {
+template <int MAXR>
+static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   const int BH = g.BH;
+  k_km_prep_cent<<<dim3(a.CP / 64 + 1, BH), 64, 0, s>>>(a, it);
+  const dim3 grid((a.n + 127) / 128, BH);
+  if (a.RP == 16)
+    k_km_assign_mfma<16><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 32)
+    k_km_assign_mfma<32><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 48)
+    k_km_assign_mfma<48><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 64)
+    k_km_assign_mfma<64><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 80)
+    k_km_assign_mfma<80><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 96)
+    k_km_assign_mfma<96><<<grid, 256, 0, s>>>(a, it);
+  else if (a.RP == 112)
+    k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
+  else
+    k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
+  k_km_fallback<MAXR><<<dim3(64, BH), 256, 0, s>>>(a, it);
+}
+
+static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
+  const int BH = g.BH;
+  KmArgs a = a0;
+  a.RP = (a.R + 15) / 16 * 16;
+  a.CP = (a.C + 31) / 32 * 32;
   k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
+  k_km_prep_points<<<dim3((a.n + 255) / 256, BH), 256, 0, s>>>(a);
   for (int it = 0; it < g.T; ++it) {
-    dim3 grid((a.n + 255) / 256, BH);
     if (a.R <= 32)
-      k_km_assign<32><<<grid, 256, 0, s>>>(a, it);
+      assign_step<32>(g, a, it, s);
     else if (a.R <= 64)
-      k_km_assign<64><<<grid, 256, 0, s>>>(a, it);
+      assign_step<64>(g, a, it, s);
     else
-      k_km_assign<128><<<grid, 256, 0, s>>>(a, it);
+      assign_step<128>(g, a, it, s);
     run_sort(a, BH, it, s);
     k_km_update<<<dim3((a.C + 3) / 4, BH), 256, 0, s>>>(a, it);
   }
   if (a.row0 > 0) k_prefix_group<<<dim3((a.row0 + 255) / 256, BH), 256, 0, s>>>(a);
+}
+
+template <int D>
+static void project(const Geom& g, const void* x, const float* F, int R, int rms, float eps,
+                    float* phi, int64_t* stats, hipStream_t s) {
+  const dim3 grid((g.NV + 255) / 256, g.BH);
+  if (R <= 32)
+    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
+  else if (R <= 64)
+    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
+  else
+    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
 }
 
 template <int D>
@@ -1078,20 +1295,20 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1)
   k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
-  k_project<D><<<dim3((g.NV + 63) / 64, BH), 256, 0, s>>>(k, g, w.fk, g.rk, 0, 0.f, w.phik,
-                                                         w.stats);
+  project<D>(g, k, w.fk, g.rk, 0, 0.f, w.phik, w.stats, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
-            g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T};
+            g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
   run_kmeans(g, ak, s);
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
                                                          w.kbar);
   k_query_metric<D><<<BH, 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
-  k_project<D><<<dim3((g.NV + 63) / 64, BH), 256, 0, s>>>(q, g, w.fq, g.rq, 1, g.eps_q, w.phiq,
-                                                         w.stats);
+  project<D>(g, q, w.fq, g.rq, 1, g.eps_q, w.phiq, w.stats, s);
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
-            g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T};
+            g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
   run_kmeans(g, aq, s);
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
                                                          w.qbar);
@@ -1129,10 +1346,12 @@ void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s) {
   (void)bh;  // every head is rebuilt; heads not imported reproduce their own data
   const int BH = g.BH;
   KmArgs ak{nullptr, nullptr, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.N, 0, g.N,
-            0, g.CKt, g.CKt + 1, g.nsort_blk_full, g.cmax, 0, g.T};
+            0, g.CKt, g.CKt + 1, g.nsort_blk_full, g.cmax, 0, g.T,
+            nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0};
   run_sort(ak, BH, -1, s);
   KmArgs aq{nullptr, nullptr, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.N, 0, g.N,
-            0, g.CQt, g.CQt + 1, g.nsort_blk_full, g.cmax, 1, g.T};
+            0, g.CQt, g.CQt + 1, g.nsort_blk_full, g.cmax, 1, g.T,
+            nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0};
   run_sort(aq, BH, -1, s);
   k_zero_routed<<<BH, 64, 0, s>>>(g, w);
   k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);

@@ -39,10 +39,13 @@ struct Geom {
   float rho, ridge, eps_q, eps_x;
   int64_t budget;         // video x video pair budget after the probe reservation
   int nchunk_max;         // attention work items per head (upper bound)
+  int nchunk_per_xcd;     // ceil(nchunk_max / 8): chunks of one head per XCD
   int nsplit;             // probe attention key splits
   int nsort_blk;          // counting-sort blocks over NV rows
   int nsort_blk_full;     // counting-sort blocks over N rows
   int cmax;               // max(CKt, CQt)
+  int rpad;               // max(rk, rq) rounded up to 16 (MFMA k-steps)
+  int cpad;               // max(CK, CQ) rounded up to 32 (MFMA tiles)
 };
 
 // Device workspace: every array is [BH][...] contiguous.
@@ -65,6 +68,14 @@ struct Work {
   int32_t* offq;    // [BH][CQt+1]
   int32_t* blkhist; // [BH][nsort_blk_full][cmax]
   int32_t* kmstate; // [BH][2][T+1]: labels changed per assignment (kv, q)
+  uint16_t* km_xhi; // [BH][NV][rpad] bf16 high part of the k-means points
+  uint16_t* km_xlo; // [BH][NV][rpad] bf16 low part (x - hi)
+  float* km_xn;     // [BH][NV] point norms
+  uint16_t* km_chi; // [BH][cpad][rpad] bf16 high part of the centroids
+  uint16_t* km_clo; // [BH][cpad][rpad]
+  float* km_cu;     // [BH][cpad] exact squared centroid norms (+inf for padding)
+  int32_t* km_fb;   // [BH][NV] points whose assignment needs the exact scan
+  int32_t* km_fbcnt;// [BH][2][T] number of such points per assignment
   float* kbar;      // [BH][CK][d]
   float* qbar;      // [BH][CQ][d]
   float* prio;      // [BH][CQ][CK]
@@ -82,6 +93,8 @@ struct Work {
   float* pw;          // [BH][M]
   int32_t* nprobes;   // [BH]
   int32_t* picks;     // [BH][M] probe-selection scratch
+  uint16_t* kperm;    // [BH][N][d]  bf16 K in group-major order
+  uint16_t* vperm;    // [BH][N][dv] bf16 V in group-major order
   float* osp;         // [BH][N][dv]
   float* odp;         // [BH][M][dv]
   float* part;        // [BH][M][nsplit][dv+2] split partials (o, m, l)
