@@ -231,59 +231,79 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 template <int D, int MAXR>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
                                                  int rms, float eps, float* phi, int64_t* stats) {
-  // one row per thread; F (D x R) broadcast from LDS
+  // 64 rows per block, 4 threads per row, MAXR/4 output columns per thread;
+  // the row tile and F are staged in LDS, outputs are written as float4
+  constexpr int ROWS = 64, CPT = MAXR / 4;
+  __shared__ float xs[ROWS][D + 4];
   __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
   const int bh = blockIdx.y, tid = threadIdx.x;
+  const int r0 = blockIdx.x * ROWS;
   const float* Fh = F + (size_t)bh * D * R;
-  for (int i = tid; i < D * R; i += 256) fs[(i / R) * MAXR + (i % R)] = Fh[i];
-  __syncthreads();
-  const int row = blockIdx.x * 256 + tid;
-  if (row >= g.NV) return;
-  const int64_t base = head_base(g, bh) + (int64_t)(g.ntext + row) * g.sn;
-  float acc[MAXR];
+  for (int i = tid; i < D * MAXR; i += 256) {
+    const int k = i / MAXR, c = i % MAXR;
+    fs[i] = c < R ? Fh[k * R + c] : 0.f;
+  }
+  const int64_t base = head_base(g, bh);
+  for (int i = tid; i < ROWS * D / 8; i += 256) {
+    const int rr = i / (D / 8), c8 = i % (D / 8);
+    const int row = r0 + rr;
+    float v[8];
+    if (row < g.NV) {
+      const int64_t off = base + (int64_t)(g.ntext + row) * g.sn + c8 * 8;
+      if (g.bf16) {
+        const uint4 u = *(const uint4*)((const uint16_t*)x + off);
+        const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-  for (int c = 0; c < MAXR; ++c) acc[c] = 0.f;
-  for (int k0 = 0; k0 < D; k0 += 8) {
-    float xv[8];
-    if (g.bf16) {
-      const uint4 u = *(const uint4*)((const uint16_t*)x + base + k0);
-      const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        xv[2 * e] = __uint_as_float(wds[e] << 16);
-        xv[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+        for (int e = 0; e < 4; ++e) {
+          v[2 * e] = __uint_as_float(wds[e] << 16);
+          v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+        }
+      } else {
+        const float4 u0 = *(const float4*)((const float*)x + off);
+        const float4 u1 = *(const float4*)((const float*)x + off + 4);
+        v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
+        v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
       }
     } else {
-      const float4 u0 = *(const float4*)((const float*)x + base + k0);
-      const float4 u1 = *(const float4*)((const float*)x + base + k0 + 4);
-      xv[0] = u0.x; xv[1] = u0.y; xv[2] = u0.z; xv[3] = u0.w;
-      xv[4] = u1.x; xv[5] = u1.y; xv[6] = u1.z; xv[7] = u1.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
     }
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const float* fr = fs + (k0 + kk) * MAXR;
+    for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
+  }
+  __syncthreads();
+  const int rr = tid >> 2, part = tid & 3;
+  float acc[CPT];
 #pragma unroll
-      for (int c = 0; c < MAXR; ++c)
-        if (c < R) acc[c] = fmaf(xv[kk], fr[c], acc[c]);
-    }
+  for (int u = 0; u < CPT; ++u) acc[u] = 0.f;
+  for (int k = 0; k < D; ++k) {
+    const float xk = xs[rr][k];
+    const float* fr = fs + k * MAXR + part * CPT;
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) acc[u] = fmaf(xk, fr[u], acc[u]);
   }
   float den = 1.f;
   if (rms) {
     float ss = 0.f;
 #pragma unroll
-    for (int c = 0; c < MAXR; ++c)
-      if (c < R) ss = fmaf(acc[c], acc[c], ss);
+    for (int u = 0; u < CPT; ++u) ss = fmaf(acc[u], acc[u], ss);
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
     den = fmaxf(sqrtf(ss / (float)R), eps);
   }
+  const int row = r0 + rr;
+  if (row >= g.NV) return;
   float* out = phi + ((size_t)bh * g.NV + row) * R;
   bool bad = false;
 #pragma unroll
-  for (int c = 0; c < MAXR; ++c)
+  for (int u = 0; u < CPT; ++u) {
+    const int c = part * CPT + u;
     if (c < R) {
-      const float v = acc[c] / den;
+      const float v = acc[u] / den;
       bad |= !isfinite(v);
       out[c] = v;
     }
+  }
   if (bad)
     atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
              (unsigned long long)SPARSEPR_FLAG_NONFINITE_INPUT);
@@ -360,23 +380,35 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
 }
 
 // Points: bf16 hi/lo split (padded to RP with zeros) and norms; once per
-// k-means.
+// k-means.  One thread per 8 coordinates of a point (16-byte stores).
 __global__ __launch_bounds__(256) void k_km_prep_points(KmArgs a) {
   const int bh = blockIdx.y;
-  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int nch = a.RP / 8;
+  const int gid = blockIdx.x * 256 + threadIdx.x;
+  const int j = gid / nch, c8 = gid % nch;
   if (j >= a.n) return;
   const float* x = a.pts + ((size_t)bh * a.n + j) * a.R;
-  uint16_t* hi = a.xhi + ((size_t)bh * a.n + j) * a.RP;
-  uint16_t* lo = a.xlo + ((size_t)bh * a.n + j) * a.RP;
+  uint32_t hw[4], lw[4];
   float ss = 0.f;
-  for (int k = 0; k < a.RP; ++k) {
-    const float v = k < a.R ? x[k] : 0.f;
-    const uint16_t h = bf16_rne_bits(v);
-    hi[k] = h;
-    lo[k] = bf16_rne_bits(v - bf16_bits_to_f32(h));
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int k0 = c8 * 8 + 2 * e;
+    const float v0 = k0 < a.R ? x[k0] : 0.f;
+    const float v1 = k0 + 1 < a.R ? x[k0 + 1] : 0.f;
+    const uint16_t h0 = bf16_rne_bits(v0), h1 = bf16_rne_bits(v1);
+    const uint16_t l0 = bf16_rne_bits(v0 - bf16_bits_to_f32(h0));
+    const uint16_t l1 = bf16_rne_bits(v1 - bf16_bits_to_f32(h1));
+    hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lw[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    ss = fmaf(v0, v0, ss);
+    ss = fmaf(v1, v1, ss);
   }
-  a.xn[(size_t)bh * a.n + j] = sqrtf(ss) * 1.000001f;
+  *(uint4*)(a.xhi + ((size_t)bh * a.n + j) * a.RP + c8 * 8) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+  *(uint4*)(a.xlo + ((size_t)bh * a.n + j) * a.RP + c8 * 8) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+  if (c8 == 0) {
+    for (int k = 8; k < a.R; ++k) ss = fmaf(x[k], x[k], ss);
+    a.xn[(size_t)bh * a.n + j] = sqrtf(ss) * 1.000001f;
+  }
 }
 
 // Centroids: hi/lo split and exact squared norms (+inf for the padding rows).
@@ -428,8 +460,9 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
     bhi[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xh + ks * 16 + h * 8));
     blo[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
   }
-  float best = INFINITY, second = INFINITY, umax = 0.f;
-  int bidx = -1;
+  // three smallest estimates (value, centroid) of this lane, ascending
+  float t1 = INFINITY, t2 = INFINITY, t3 = INFINITY, umax = 0.f;
+  int i1 = -1, i2 = -1, i3 = -1;
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
   const float* cu = a.cu + (size_t)bh * a.CP;
@@ -460,88 +493,125 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       const float u = su[r];
       const float sh = fmaf(-2.f, S[i], u);
       if (c0 + r < a.C) umax = fmaxf(umax, u);
-      if (sh < best) {
-        second = best;
-        best = sh;
-        bidx = c0 + r;
-      } else {
-        second = fminf(second, sh);
+      if (sh < t3) {
+        const int cb = c0 + r;
+        if (sh < t2) {
+          t3 = t2;
+          i3 = i2;
+          if (sh < t1) {
+            t2 = t1;
+            i2 = i1;
+            t1 = sh;
+            i1 = cb;
+          } else {
+            t2 = sh;
+            i2 = cb;
+          }
+        } else {
+          t3 = sh;
+          i3 = cb;
+        }
       }
     }
   }
-  const float ob = __shfl_xor(best, 32), os = __shfl_xor(second, 32);
-  const int oi = __shfl_xor(bidx, 32);
-  if (ob < best || (ob == best && oi < bidx)) {
-    second = fminf(best, os);
-    best = ob;
-    bidx = oi;
-  } else {
-    second = fminf(second, ob);
+  // merge with the other half of the centroids (lane l ^ 32, same point):
+  // insert its three entries (any order of equal values is fine: only the
+  // third smallest value decides whether the list holds every candidate)
+  {
+    const float o1 = __shfl_xor(t1, 32), o2 = __shfl_xor(t2, 32), o3 = __shfl_xor(t3, 32);
+    const int j1 = __shfl_xor(i1, 32), j2 = __shfl_xor(i2, 32), j3 = __shfl_xor(i3, 32);
+    auto ins = [&](float v, int idx) {
+      if (v < t3) {
+        if (v < t2) {
+          t3 = t2;
+          i3 = i2;
+          if (v < t1) {
+            t2 = t1;
+            i2 = i1;
+            t1 = v;
+            i1 = idx;
+          } else {
+            t2 = v;
+            i2 = idx;
+          }
+        } else {
+          t3 = v;
+          i3 = idx;
+        }
+      }
+    };
+    ins(o1, j1);
+    ins(o2, j2);
+    ins(o3, j3);
   }
   umax = fmaxf(umax, __shfl_xor(umax, 32));
   if (h != 0 || j >= a.n) return;
   const float xn = a.xn[(size_t)bh * a.n + j];
   const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-  if (second - best > 2.f * delta) {
-    const int old = lab[j];
-    lab[j] = bidx;
-    if (it > 0 && old != bidx) atomicAdd(&km_changed(a, bh)[it], 1);
+  int label;
+  if (t2 - t1 > 2.f * delta) {
+    label = i1;  // unique candidate: the exact argmin
+  } else if (t3 - t1 > 2.f * delta) {
+    // exactly two candidates: rescore both with the defining float score
+    const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
+    const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
+    const float* c2 = a.cent + ((size_t)bh * a.C + i2) * a.R;
+    float d1 = 0.f, d2 = 0.f;
+    for (int k = 0; k < a.R; ++k) {
+      const float xk = xp[k];
+      d1 = fmaf(xk, c1[k], d1);
+      d2 = fmaf(xk, c2[k], d2);
+    }
+    const float s1 = fmaf(-2.f, d1, cu[i1]), s2 = fmaf(-2.f, d2, cu[i2]);
+    label = (s2 < s1 || (s2 == s1 && i2 < i1)) ? i2 : i1;
   } else {
     int32_t* cnt = a.fbcnt + (size_t)bh * 2 * a.T + a.sel * a.T + it;
     const int slot = atomicAdd(cnt, 1);
     a.fb[(size_t)bh * a.n + slot] = j;
+    return;
   }
+  const int old = lab[j];
+  lab[j] = label;
+  if (it > 0 && old != label) atomicAdd(&km_changed(a, bh)[it], 1);
 }
 
 // Exact scan (the defining float score) for the points the screen could not
-// decide.  Blocks stride over the list; every thread takes one point.
-template <int MAXR>
+// decide.  One wave per point: each lane scores a strided subset of the
+// centroids with the float chain, then the wave keeps the smallest score and
+// the lowest index among equal scores.
 __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
-  constexpr int CB = 64;
-  __shared__ float cs[CB][MAXR + 1];
-  __shared__ float cu[CB];
-  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int bh = blockIdx.y, lane = threadIdx.x & 63;
   if (km_skip_assign(a, bh, it)) return;
   const int cnt = a.fbcnt[(size_t)bh * 2 * a.T + a.sel * a.T + it];
-  const int R = a.R;
-  const float* cent = a.cent + (size_t)bh * a.C * R;
+  const float* cu = a.cu + (size_t)bh * a.CP;
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-  for (int base = blockIdx.x * 256; base < cnt; base += gridDim.x * 256) {
-    const int e = base + tid;
-    const int j = e < cnt ? a.fb[(size_t)bh * a.n + e] : 0;
-    float x[MAXR];
-    const float* pj = a.pts + ((size_t)bh * a.n + j) * R;
-#pragma unroll
-    for (int k = 0; k < MAXR; ++k) x[k] = (k < R) ? pj[k] : 0.f;
-    float best = 0.f;
-    int bi = -1;
-    for (int c0 = 0; c0 < a.C; c0 += CB) {
-      const int cn = min(CB, a.C - c0);
-      __syncthreads();
-      for (int i = tid; i < cn * R; i += 256) cs[i / R][i % R] = cent[(size_t)c0 * R + i];
-      __syncthreads();
-      if (tid < cn) {
-        float u = 0.f;
-        for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
-        cu[tid] = u;
-      }
-      __syncthreads();
-      if (e < cnt) {
-        for (int b = 0; b < cn; ++b) {
-          float t = 0.f;
-#pragma unroll
-          for (int k = 0; k < MAXR; ++k)
-            if (k < R) t = fmaf(x[k], cs[b][k], t);
-          const float sc = fmaf(-2.f, t, cu[b]);
-          if (bi < 0 || sc < best) {
-            best = sc;
-            bi = c0 + b;
-          }
-        }
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwave = gridDim.x * 4;
+  for (int e = wave; e < cnt; e += nwave) {
+    const int j = a.fb[(size_t)bh * a.n + e];
+    const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
+    float best = INFINITY;
+    int bi = 0x7fffffff;
+    for (int b = lane; b < a.C; b += 64) {
+      const float* cb = a.cent + ((size_t)bh * a.C + b) * a.R;
+      float t = 0.f;
+      for (int k = 0; k < a.R; ++k) t = fmaf(xp[k], cb[k], t);
+      const float sc = fmaf(-2.f, t, cu[b]);
+      if (sc < best) {  // b ascending within the lane: ties keep the lower index
+        best = sc;
+        bi = b;
       }
     }
-    if (e < cnt) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o);
+      const int oi = __shfl_xor(bi, o);
+      if (ob < best || (ob == best && oi < bi)) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    if (lane == 0) {
       const int old = lab[j];
       lab[j] = bi;
       if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
@@ -1253,7 +1323,7 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  k_km_fallback<MAXR><<<dim3(64, BH), 256, 0, s>>>(a, it);
+  k_km_fallback<<<dim3(64, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
@@ -1262,7 +1332,7 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
   a.RP = (a.R + 15) / 16 * 16;
   a.CP = (a.C + 31) / 32 * 32;
   k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
-  k_km_prep_points<<<dim3((a.n + 255) / 256, BH), 256, 0, s>>>(a);
+  k_km_prep_points<<<dim3((a.n * (a.RP / 8) + 255) / 256, BH), 256, 0, s>>>(a);
   for (int it = 0; it < g.T; ++it) {
     if (a.R <= 32)
       assign_step<32>(g, a, it, s);
@@ -1279,7 +1349,7 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
 template <int D>
 static void project(const Geom& g, const void* x, const float* F, int R, int rms, float eps,
                     float* phi, int64_t* stats, hipStream_t s) {
-  const dim3 grid((g.NV + 255) / 256, g.BH);
+  const dim3 grid((g.NV + 63) / 64, g.BH);
   if (R <= 32)
     k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
   else if (R <= 64)
