@@ -111,7 +111,8 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->fitv, 3 * dv * 4);
   add(&w->fity, dv * r * 4);
   add(&w->fitpsi, dv * r * 4);
-  add(&w->fitscr, (2 * M * dv + M * r + dv * r) * 8);
+  add(&w->fitscr, (2 * M * dv + M * r + dv * r + M) * 8);
+  add(&w->fitgram, 2 * dv * dv * 8);
   add(&w->stats, 16 * 8);
   size_t off = 0;
   for (auto& it : L.items) off += align256((size_t)g.BH * it.per_head);

@@ -557,31 +557,41 @@ __global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
 template <int D, typename T>
 __device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag);
 
+// Per-head scratch of the fit: xbar [M][D], rbar [M][D], rbar*Psi [M][r],
+// rhs [D][r], w~ [M] (all double).
+struct FitScratch {
+  double *xb, *rb, *rp, *rhs, *wt;
+};
+
+__device__ __forceinline__ FitScratch fit_scratch(const Geom& g, const Work& w, int bh) {
+  const size_t D = g.dv, M = g.M, r = g.r;
+  double* base = w.fitscr + (size_t)bh * (2 * M * D + M * r + D * r + M);
+  FitScratch f;
+  f.xb = base;
+  f.rb = f.xb + M * D;
+  f.rp = f.rb + M * D;
+  f.rhs = f.rp + M * r;
+  f.wt = f.rhs + D * r;
+  return f;
+}
+
+// Weighted statistics of the probes (eqs. app_normalized_weights ...
+// app_regression_weights): mu_x, mu_R, s_x, xbar, Rbar and w~.
 template <int D>
-__global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
-  using T = typename std::conditional<D <= 64, double, float>::type;
-  constexpr int LD = D + 1;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * D * LD * sizeof(T)];
-  __shared__ T rc[D / 2], rs[D / 2];
-  __shared__ int order[D];
-  __shared__ double red[2];
-  __shared__ int flag, rank_s, fail;
+__global__ __launch_bounds__(256) void k_fit_prep(Geom g, Work w) {
+  __shared__ double swsh;
   const int bh = blockIdx.x, tid = threadIdx.x;
   const int np = w.nprobes[bh];
   const int r = g.r;
   float* fv = w.fitv + (size_t)bh * 3 * D;
   float* Y = w.fity + (size_t)bh * D * r;
   float* Psi = w.fitpsi + (size_t)bh * D * r;
-  double* xb = w.fitscr + (size_t)bh * ((size_t)2 * g.M * D + (size_t)g.M * r + (size_t)D * r);  // [M][D]
-  double* rb = xb + (size_t)g.M * D;                            // [M][D]
-  double* rp = rb + (size_t)g.M * D;                            // [M][r]   Rbar Psi
-  double* rhs = rp + (size_t)g.M * r;                           // [D][r]
-  for (int i = tid; i < D * r; i += 1024) {
+  for (int i = tid; i < D * r; i += 256) {
     Y[i] = 0.f;
     Psi[i] = 0.f;
   }
   if (np == 0) {
-    for (int c = tid; c < D; c += 1024) {
+    for (int c = tid; c < D; c += 256) {
       fv[c] = 0.f;
       fv[D + c] = 1.f;
       fv[2 * D + c] = 0.f;
@@ -589,6 +599,7 @@ __global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
     if (tid == 0) w.stats[(size_t)bh * 16 + ST_FIT_RANK] = 0;
     return;
   }
+  const FitScratch f = fit_scratch(g, w, bh);
   const int32_t* pr = w.probes + (size_t)bh * g.M;
   const float* pwt = w.pw + (size_t)bh * g.M;
   const float* osp = w.osp + (size_t)bh * g.N * D;
@@ -596,13 +607,12 @@ __global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
   if (tid == 0) {
     double s = 0.0;
     for (int p = 0; p < np; ++p) s += (double)pwt[p];
-    red[0] = s;
+    swsh = s;
   }
   __syncthreads();
-  const double sw = red[0];
-  // weighted statistics, one thread per output dimension
-  if (tid < D) {
-    const int c = tid;
+  const double sw = swsh;
+  for (int p = tid; p < np; p += 256) f.wt[p] = (double)np * (double)pwt[p] / sw;
+  for (int c = tid; c < D; c += 256) {
     double mx = 0.0, mr = 0.0;
     for (int p = 0; p < np; ++p) {
       const double al = (double)pwt[p] / sw;
@@ -619,24 +629,82 @@ __global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
     const double sx = sqrt(vx + (double)g.eps_x);
     for (int p = 0; p < np; ++p) {
       const double x = osp[(size_t)pr[p] * D + c];
-      xb[(size_t)p * D + c] = (x - mx) / sx;
-      rb[(size_t)p * D + c] = ((double)odp[(size_t)p * D + c] - x) - mr;
+      f.xb[(size_t)p * D + c] = (x - mx) / sx;
+      f.rb[(size_t)p * D + c] = ((double)odp[(size_t)p * D + c] - x) - mr;
     }
     fv[c] = (float)mx;
     fv[D + c] = (float)sx;
     fv[2 * D + c] = (float)mr;
   }
-  __syncthreads();
-  // H = Rbar^T W Rbar into the Jacobi matrix
+}
+
+// The two weighted Gram matrices of the fit, one 32 x 32 tile per block:
+// which = 0: H = Rbar^T W Rbar (its eigenvectors are the right singular
+// vectors of W^1/2 Rbar, eq. app_probe_residual_basis); which = 1:
+// S = xbar^T W xbar + lambda I (eq. app_ridge_closed_form).
+template <int D>
+__global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
+  constexpr int PB = 64;
+  __shared__ double sa[PB][33], sb[PB][33];
+  __shared__ double swt[PB];
+  const int bh = blockIdx.z, which = blockIdx.y, tid = threadIdx.x;
+  const int np = w.nprobes[bh];
+  if (np == 0) return;
+  const int ti = blockIdx.x / (D / 32), tj = blockIdx.x % (D / 32);
+  const FitScratch f = fit_scratch(g, w, bh);
+  const double* src = which == 0 ? f.rb : f.xb;
+  const int li = tid / 8, lj = (tid % 8) * 4;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int p0 = 0; p0 < np; p0 += PB) {
+    const int pn = min(PB, np - p0);
+    __syncthreads();
+    for (int i = tid; i < pn * 32; i += 256) {
+      const int p = i / 32, c = i % 32;
+      sa[p][c] = src[(size_t)(p0 + p) * D + ti * 32 + c];
+      sb[p][c] = src[(size_t)(p0 + p) * D + tj * 32 + c];
+    }
+    for (int p = tid; p < pn; p += 256) swt[p] = f.wt[p0 + p];
+    __syncthreads();
+    for (int p = 0; p < pn; ++p) {
+      const double a = swt[p] * sa[p][li];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] += a * sb[p][lj + e];
+    }
+  }
+  double* G = w.fitgram + ((size_t)bh * 2 + which) * D * D;
+  const int i = ti * 32 + li;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int j = tj * 32 + lj + e;
+    G[(size_t)i * D + j] = acc[e] + ((which == 1 && i == j) ? (double)g.ridge : 0.0);
+  }
+}
+
+// Residual subspace and ridge solve, one block of 1024 threads per head:
+// Psi = leading r eigenvectors of H with sigma > 1e-6 sigma_1 (Jacobi in
+// LDS); then (xbar^T W xbar + lambda I) Y = xbar^T W (Rbar Psi) by Cholesky,
+// so Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
+template <int D>
+__global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
+  using T = typename std::conditional<D <= 64, double, float>::type;
+  constexpr int LD = D + 1;
+  constexpr size_t JAC = 2 * D * LD * sizeof(T), CHOL = (size_t)D * D * sizeof(double);
+  __shared__ __attribute__((aligned(16))) unsigned char smem[JAC > CHOL ? JAC : CHOL];
+  __shared__ T rc[D / 2], rs[D / 2];
+  __shared__ int order[D];
+  __shared__ int flag, rank_s, fail;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int np = w.nprobes[bh];
+  if (np == 0) return;
+  const int r = g.r;
+  float* Y = w.fity + (size_t)bh * D * r;
+  float* Psi = w.fitpsi + (size_t)bh * D * r;
+  const FitScratch f = fit_scratch(g, w, bh);
+  const double* H = w.fitgram + ((size_t)bh * 2 + 0) * D * D;
+  const double* Sg = w.fitgram + ((size_t)bh * 2 + 1) * D * D;
   T* Am = (T*)smem;
   T* Vm = Am + D * LD;
-  const double wscale = (double)np / sw;
-  for (int e = tid; e < D * D; e += 1024) {
-    const int i = e / D, j = e % D;
-    double acc = 0.0;
-    for (int p = 0; p < np; ++p) acc += wscale * (double)pwt[p] * rb[(size_t)p * D + i] * rb[(size_t)p * D + j];
-    Am[i * LD + j] = (T)acc;
-  }
+  for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
   __syncthreads();
   jacobi_eig_lds_fit<D, T>(Am, Vm, rc, rs, &flag);
   if (tid < D) {
@@ -670,31 +738,23 @@ __global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
     const int row = i / rk, t = i % rk;
     Psi[row * r + t] = (float)Vm[row * LD + order[t]];
   }
-  __syncthreads();
-  // Rbar Psi (M x rk) and rhs = xbar^T W (Rbar Psi) (D x rk)
   for (int i = tid; i < np * rk; i += 1024) {
     const int p = i / rk, t = i % rk;
     double acc = 0.0;
-    for (int c = 0; c < D; ++c) acc += rb[(size_t)p * D + c] * (double)Vm[c * LD + order[t]];
-    rp[(size_t)p * r + t] = acc;
+    for (int c = 0; c < D; ++c) acc += f.rb[(size_t)p * D + c] * (double)Vm[c * LD + order[t]];
+    f.rp[(size_t)p * r + t] = acc;
   }
   __syncthreads();
   for (int i = tid; i < D * rk; i += 1024) {
     const int c = i / rk, t = i % rk;
     double acc = 0.0;
-    for (int p = 0; p < np; ++p)
-      acc += wscale * (double)pwt[p] * xb[(size_t)p * D + c] * rp[(size_t)p * r + t];
-    rhs[(size_t)c * r + t] = acc;
+    for (int p = 0; p < np; ++p) acc += f.wt[p] * f.xb[(size_t)p * D + c] * f.rp[(size_t)p * r + t];
+    f.rhs[(size_t)c * r + t] = acc;
   }
-  // S = xbar^T W xbar + lambda I in LDS (double), then Cholesky S = L L^T
+  // Cholesky S = L L^T in LDS (double)
   double* S = (double*)smem;
   __syncthreads();
-  for (int e = tid; e < D * D; e += 1024) {
-    const int i = e / D, j = e % D;
-    double acc = 0.0;
-    for (int p = 0; p < np; ++p) acc += wscale * (double)pwt[p] * xb[(size_t)p * D + i] * xb[(size_t)p * D + j];
-    S[i * D + j] = acc + (i == j ? (double)g.ridge : 0.0);
-  }
+  for (int e = tid; e < D * D; e += 1024) S[e] = Sg[e];
   __syncthreads();
   for (int j = 0; j < D; ++j) {
     if (tid == 0) {
@@ -717,16 +777,16 @@ __global__ __launch_bounds__(1024) void k_fit(Geom g, Work w) {
   if (tid < rk && !fail) {
     const int t = tid;
     for (int i = 0; i < D; ++i) {
-      double acc = rhs[(size_t)i * r + t];
-      for (int k = 0; k < i; ++k) acc -= S[i * D + k] * rhs[(size_t)k * r + t];
-      rhs[(size_t)i * r + t] = acc / S[i * D + i];
+      double acc = f.rhs[(size_t)i * r + t];
+      for (int k = 0; k < i; ++k) acc -= S[i * D + k] * f.rhs[(size_t)k * r + t];
+      f.rhs[(size_t)i * r + t] = acc / S[i * D + i];
     }
     for (int i = D - 1; i >= 0; --i) {
-      double acc = rhs[(size_t)i * r + t];
-      for (int k = i + 1; k < D; ++k) acc -= S[k * D + i] * rhs[(size_t)k * r + t];
-      rhs[(size_t)i * r + t] = acc / S[i * D + i];
+      double acc = f.rhs[(size_t)i * r + t];
+      for (int k = i + 1; k < D; ++k) acc -= S[k * D + i] * f.rhs[(size_t)k * r + t];
+      f.rhs[(size_t)i * r + t] = acc / S[i * D + i];
     }
-    for (int i = 0; i < D; ++i) Y[i * r + t] = (float)rhs[(size_t)i * r + t];
+    for (int i = 0; i < D; ++i) Y[i * r + t] = (float)f.rhs[(size_t)i * r + t];
   }
   if (tid == 0) {
     int64_t* st = w.stats + (size_t)bh * 16;
@@ -847,10 +907,11 @@ __device__ __forceinline__ void rr_pair2(int step, int i, int n, int& p, int& q)
 template <int D, typename T>
 __device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
   constexpr int LD = D + 1, P = D / 2;
+  __shared__ int pp[P], pq[P];  // this step's rotation pairs
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int i = tid; i < D * D; i += nt) {
-    const int rr = i / D, c = i % D;
-    V[rr * LD + c] = (rr == c) ? T(1) : T(0);
+    const int r = i / D, c = i % D;
+    V[r * LD + c] = (r == c) ? T(1) : T(0);
   }
   __syncthreads();
   for (int sweep = 0; sweep < 20; ++sweep) {
@@ -860,6 +921,8 @@ __device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
       if (tid < P) {
         int p, q;
         rr_pair2(step, tid, D, p, q);
+        pp[tid] = p;
+        pq[tid] = q;
         const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
         T c = 1, s = 0;
         const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
@@ -881,9 +944,7 @@ __device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
         const T si = rs[i], sj = rs[j];
         if (si == T(0) && sj == T(0)) continue;
         const T ci = rc[i], cj = rc[j];
-        int p, q, p2, q2;
-        rr_pair2(step, i, D, p, q);
-        rr_pair2(step, j, D, p2, q2);
+        const int p = pp[i], q = pq[i], p2 = pp[j], q2 = pq[j];
         const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
         const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
         const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
@@ -901,8 +962,7 @@ __device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
         const T sj = rs[j];
         if (sj == T(0)) continue;
         const T cj = rc[j];
-        int p, q;
-        rr_pair2(step, j, D, p, q);
+        const int p = pp[j], q = pq[j];
         const T vp = V[row * LD + p], vq = V[row * LD + q];
         V[row * LD + p] = cj * vp - sj * vq;
         V[row * LD + q] = sj * vp + cj * vq;
@@ -967,7 +1027,9 @@ static void attend_d(const Geom& g, const Work& w, const void* q, const void* k,
     k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
   }
   if (ev) (void)hipEventRecord(ev[2], s);
-  k_fit<D><<<g.BH, 1024, 0, s>>>(g, w);
+  k_fit_prep<D><<<g.BH, 256, 0, s>>>(g, w);
+  k_fit_gram<D><<<dim3((D / 32) * (D / 32), 2, g.BH), 256, 0, s>>>(g, w);
+  k_fit_solve<D><<<g.BH, 1024, 0, s>>>(g, w);
   if (ev) (void)hipEventRecord(ev[3], s);
   k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(g, w, out);
   if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w, out);

@@ -94,6 +94,7 @@ __device__ __forceinline__ void rr_pair(int step, int i, int n, int& p, int& q) 
 template <int D, typename T>
 __device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
   constexpr int LD = D + 1, P = D / 2;
+  __shared__ int pp[P], pq[P];  // this step's rotation pairs
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int i = tid; i < D * D; i += nt) {
     const int r = i / D, c = i % D;
@@ -107,6 +108,8 @@ __device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
       if (tid < P) {
         int p, q;
         rr_pair(step, tid, D, p, q);
+        pp[tid] = p;
+        pq[tid] = q;
         const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
         T c = 1, s = 0;
         const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
@@ -128,9 +131,7 @@ __device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
         const T si = rs[i], sj = rs[j];
         if (si == T(0) && sj == T(0)) continue;
         const T ci = rc[i], cj = rc[j];
-        int p, q, p2, q2;
-        rr_pair(step, i, D, p, q);
-        rr_pair(step, j, D, p2, q2);
+        const int p = pp[i], q = pq[i], p2 = pp[j], q2 = pq[j];
         const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
         const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
         const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
@@ -148,8 +149,7 @@ __device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
         const T sj = rs[j];
         if (sj == T(0)) continue;
         const T cj = rc[j];
-        int p, q;
-        rr_pair(step, j, D, p, q);
+        const int p = pp[j], q = pq[j];
         const T vp = V[row * LD + p], vq = V[row * LD + q];
         V[row * LD + p] = cj * vp - sj * vq;
         V[row * LD + q] = sj * vp + cj * vq;

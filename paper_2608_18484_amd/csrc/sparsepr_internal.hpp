@@ -101,7 +101,8 @@ struct Work {
   float* fitv;        // [BH][3*dv] mu_x, s_x, mu_r
   float* fity;        // [BH][dv][r] B Psi
   float* fitpsi;      // [BH][dv][r]
-  double* fitscr;     // [BH][2*M*dv + M*r + dv*r] fit scratch
+  double* fitscr;     // [BH][2*M*dv + M*r + dv*r + M] fit scratch
+  double* fitgram;    // [BH][2][dv][dv] Rbar^T W Rbar and xbar^T W xbar + lambda I
   int64_t* stats;     // [BH][16]
 };
 
