@@ -159,13 +159,13 @@ __device__ __forceinline__ void g2lds16(const void* src, const void* lds_base) {
 //  * Online softmax in base 2 with lazy rescaling: the running maximum only
 //    moves (and O, l are rescaled) when a tile's maximum exceeds it by 2^8.
 template <int D, int MODE>
-__global__ __launch_bounds__(128) void k_attn_mfma(Geom g, AttnArgs A) {
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_mfma(Geom g, AttnArgs A) {
   constexpr int KT = 32;
   constexpr int CH = D / 8;                    // 16-byte chunks per row
   constexpr int NKS = D / 16;                  // k-steps of Q K^T
   constexpr int NDB = D / 32;                  // 32-wide blocks of O^T
   constexpr int LPT = KT * CH / 128;           // 16-byte loads per thread per tensor per tile
-  constexpr int MAXR = 1024;                   // routed ranges staged in LDS
+  constexpr int MAXR = 512;                    // routed ranges staged in LDS
   __shared__ __attribute__((aligned(1024))) uint16_t Kb0[KT * D];
   __shared__ __attribute__((aligned(1024))) uint16_t Kb1[KT * D];
   __shared__ __attribute__((aligned(1024))) uint16_t Vb0[KT * D];
