@@ -184,7 +184,7 @@ def main():
         "exec_pairs": st["exec_pairs"],
         "kmeans_assignments": [st["kmeans_iters_kv"], st["kmeans_iters_q"]],
         "phase_ms": phases,
-        "roofline": {"bound": "mfma", "kernel": "k_attn_bf16<128, MODE_SPARSE>",
+        "roofline": {"bound": "mfma", "kernel": "k_attn_mfma<128, MODE_SPARSE>",
                      "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
                      "kernel_ms": round(attn_ms, 4), "traffic": None},
