@@ -25,6 +25,7 @@
 
 #include "device_utils.hpp"
 #include "sparsepr_internal.hpp"
+#include "jacobi_lds.hpp"
 
 namespace sparsepr {
 
@@ -554,9 +555,6 @@ __global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
 // so Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
 // ---------------------------------------------------------------------------
 
-template <int D, typename T>
-__device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag);
-
 // Per-head scratch of the fit: xbar [M][D], rbar [M][D], rbar*Psi [M][r],
 // rhs [D][r], w~ [M] (all double).
 struct FitScratch {
@@ -690,7 +688,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   constexpr int LD = D + 1;
   constexpr size_t JAC = 2 * D * LD * sizeof(T), CHOL = (size_t)D * D * sizeof(double);
   __shared__ __attribute__((aligned(16))) unsigned char smem[JAC > CHOL ? JAC : CHOL];
-  __shared__ T rc[D / 2], rs[D / 2];
+  __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
   __shared__ int flag, rank_s, fail;
   const int bh = blockIdx.x, tid = threadIdx.x;
@@ -706,7 +704,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   T* Vm = Am + D * LD;
   for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
   __syncthreads();
-  jacobi_eig_lds_fit<D, T>(Am, Vm, rc, rs, &flag);
+  jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag);
   if (tid < D) {
     const T li = Am[tid * LD + tid];
     int rank = 0;
@@ -801,76 +799,106 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
 // Probe rows are overwritten afterwards by k_probe_scatter.
 template <int D>
 __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
-  constexpr int ROWS = 64;
-  __shared__ float xs[ROWS][D + 1];
-  __shared__ float ts[ROWS][33];
-  __shared__ float fy[D][33], fp[D][33];
-  __shared__ float mux[D], sx[D], mur[D];
+  // 64 rows per block.  Thread (row = tid / 4, quarter = tid % 4) owns the
+  // columns [quarter * D/4, quarter * D/4 + D/4) of its row: it standardises
+  // them once into LDS, computes a quarter of the rank directions of
+  // t = xbar Y (Y = B_lambda Psi), and after the exchange forms its columns of
+  // x + mu_R + t Psi^T.  The rank is processed in slices of 16 directions.
+  constexpr int ROWS = 64, CW = D / 4, RS = 16;
+  __shared__ float xb[ROWS][D + 1];
+  __shared__ float ts[ROWS][RS + 1];
+  __shared__ __attribute__((aligned(16))) float fy[D][RS];
+  __shared__ __attribute__((aligned(16))) float fp[D][RS];
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int r0 = blockIdx.x * ROWS;
   const int r = g.r;
-  const int rr = min(r, 32);
+  const int rw = tid >> 2, qtr = tid & 3;
+  const int row = r0 + rw;
+  const bool valid = row < g.N;
+  const bool text = row < g.ntext;
   const float* fv = w.fitv + (size_t)bh * 3 * D;
-  for (int c = tid; c < D; c += 256) {
-    mux[c] = fv[c];
-    sx[c] = fv[D + c];
-    mur[c] = fv[2 * D + c];
-  }
   const float* Y = w.fity + (size_t)bh * D * r;
   const float* Psi = w.fitpsi + (size_t)bh * D * r;
-  const float* osp = w.osp + (size_t)bh * g.N * D;
-  for (int i = tid; i < ROWS * D; i += 256) {
-    const int rr2 = i / D, c = i % D;
-    const int row = r0 + rr2;
-    xs[rr2][c] = row < g.N ? osp[(size_t)row * D + c] : 0.f;
+  const float* src = w.osp + ((size_t)bh * g.N + (valid ? row : 0)) * D + qtr * CW;
+  float x[CW], acc[CW];
+#pragma unroll
+  for (int c4 = 0; c4 < CW / 4; ++c4) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (valid) v = *(const float4*)(src + 4 * c4);
+    x[4 * c4] = v.x;
+    x[4 * c4 + 1] = v.y;
+    x[4 * c4 + 2] = v.z;
+    x[4 * c4 + 3] = v.w;
   }
-  __syncthreads();
-  const int64_t base = head_base(g, bh);
-  // the residual rank is processed in slices of up to 32 directions
-  float accs[ROWS * D / 256];
 #pragma unroll
-  for (int u = 0; u < ROWS * D / 256; ++u) accs[u] = 0.f;
-  for (int t0 = 0; t0 < r; t0 += 32) {
-    const int tn = min(32, r - t0);
+  for (int c = 0; c < CW; ++c) {
+    const int col = qtr * CW + c;
+    xb[rw][col] = (x[c] - fv[col]) / fv[D + col];
+    acc[c] = 0.f;
+  }
+  for (int t0 = 0; t0 < r; t0 += RS) {
+    const int tn = min(RS, r - t0);
     __syncthreads();
-    for (int i = tid; i < D * tn; i += 256) {
-      const int c = i / tn, t = i % tn;
-      fy[c][t] = Y[c * r + t0 + t];
-      fp[c][t] = Psi[c * r + t0 + t];
+    for (int i = tid; i < D * RS; i += 256) {
+      const int c = i / RS, t = i % RS;
+      fy[c][t] = t < tn ? Y[c * r + t0 + t] : 0.f;
+      fp[c][t] = t < tn ? Psi[c * r + t0 + t] : 0.f;
     }
     __syncthreads();
-    for (int i = tid; i < ROWS * tn; i += 256) {
-      const int rw = i / tn, t = i % tn;
-      float acc = 0.f;
-      for (int c = 0; c < D; ++c) acc = fmaf((xs[rw][c] - mux[c]) / sx[c], fy[c][t], acc);
-      ts[rw][t] = acc;
+    // t[rw][qtr*4 .. qtr*4+4): dims in index order
+    float tq[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < D; ++c) {
+      const float xv = xb[rw][c];
+      const float4 y4 = *(const float4*)&fy[c][qtr * 4];
+      tq[0] = fmaf(xv, y4.x, tq[0]);
+      tq[1] = fmaf(xv, y4.y, tq[1]);
+      tq[2] = fmaf(xv, y4.z, tq[2]);
+      tq[3] = fmaf(xv, y4.w, tq[3]);
     }
-    __syncthreads();
 #pragma unroll
-    for (int u = 0; u < ROWS * D / 256; ++u) {
-      const int i = tid + 256 * u;
-      const int rw = i / D, c = i % D;
-      float acc = accs[u];
-      for (int t = 0; t < tn; ++t) acc = fmaf(ts[rw][t], fp[c][t], acc);
-      accs[u] = acc;
+    for (int e = 0; e < 4; ++e) ts[rw][qtr * 4 + e] = tq[e];
+    __syncthreads();
+    float tr[RS];
+#pragma unroll
+    for (int t = 0; t < RS; ++t) tr[t] = ts[rw][t];
+#pragma unroll
+    for (int c = 0; c < CW; ++c) {
+      const int col = qtr * CW + c;
+      float a = acc[c];
+#pragma unroll
+      for (int t4 = 0; t4 < RS / 4; ++t4) {
+        const float4 p4 = *(const float4*)&fp[col][t4 * 4];
+        a = fmaf(tr[4 * t4], p4.x, a);
+        a = fmaf(tr[4 * t4 + 1], p4.y, a);
+        a = fmaf(tr[4 * t4 + 2], p4.z, a);
+        a = fmaf(tr[4 * t4 + 3], p4.w, a);
+      }
+      acc[c] = a;
     }
   }
-  (void)rr;
+  if (!valid) return;
+  const int64_t dst = head_base(g, bh) + (int64_t)row * g.sn + qtr * CW;
+  float o[CW];
 #pragma unroll
-  for (int u = 0; u < ROWS * D / 256; ++u) {
-    const int i = tid + 256 * u;
-    const int rw = i / D, c = i % D;
-    const int row = r0 + rw;
-    if (row >= g.N) continue;
-    const float x = xs[rw][c];
-    const float v = (row < g.ntext) ? x : x + mur[c] + accs[u];
-    const int64_t idx = base + (int64_t)row * g.sn + c;
-    if (g.bf16) {
-      const __bf16 b = (__bf16)v;
-      ((uint16_t*)out)[idx] = __builtin_bit_cast(uint16_t, b);
-    } else {
-      ((float*)out)[idx] = v;
+  for (int c = 0; c < CW; ++c) o[c] = text ? x[c] : x[c] + fv[2 * D + qtr * CW + c] + acc[c];
+  if (g.bf16) {
+    uint16_t* op = (uint16_t*)out + dst;
+#pragma unroll
+    for (int c8 = 0; c8 < CW / 8; ++c8) {
+      uint32_t wd[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e]);
+        const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e + 1]);
+        wd[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+      }
+      *(uint4*)(op + c8 * 8) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
     }
+  } else {
+    float* op = (float*)out + dst;
+#pragma unroll
+    for (int c4 = 0; c4 < CW / 4; ++c4)
+      *(float4*)(op + 4 * c4) = make_float4(o[4 * c4], o[4 * c4 + 1], o[4 * c4 + 2], o[4 * c4 + 3]);
   }
 }
 
@@ -888,96 +916,6 @@ __global__ __launch_bounds__(128) void k_probe_scatter(Geom g, Work w, void* out
     ((float*)out)[idx] = v;
   }
 }
-
-// ---------------------------------------------------------------------------
-// Jacobi eigensolver for the fit (same method as the planner's, duplicated
-// here so each translation unit stands alone).
-// ---------------------------------------------------------------------------
-
-__device__ __forceinline__ void rr_pair2(int step, int i, int n, int& p, int& q) {
-  if (i == 0) {
-    p = step;
-    q = n - 1;
-  } else {
-    p = (step + i) % (n - 1);
-    q = (step - i + n - 1) % (n - 1);
-  }
-}
-
-template <int D, typename T>
-__device__ void jacobi_eig_lds_fit(T* A, T* V, T* rc, T* rs, int* flag) {
-  constexpr int LD = D + 1, P = D / 2;
-  __shared__ int pp[P], pq[P];  // this step's rotation pairs
-  const int tid = threadIdx.x, nt = blockDim.x;
-  for (int i = tid; i < D * D; i += nt) {
-    const int r = i / D, c = i % D;
-    V[r * LD + c] = (r == c) ? T(1) : T(0);
-  }
-  __syncthreads();
-  for (int sweep = 0; sweep < 20; ++sweep) {
-    if (tid == 0) *flag = 0;
-    __syncthreads();
-    for (int step = 0; step < D - 1; ++step) {
-      if (tid < P) {
-        int p, q;
-        rr_pair2(step, tid, D, p, q);
-        pp[tid] = p;
-        pq[tid] = q;
-        const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
-        T c = 1, s = 0;
-        const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
-        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
-          const T theta = (aqq - app) / (T(2) * apq);
-          const T at = fabs(theta);
-          const T t = (at > T(1e10)) ? T(0.5) / theta
-                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
-          c = T(1) / sqrt(t * t + T(1));
-          s = t * c;
-          *flag = 1;
-        }
-        rc[tid] = c;
-        rs[tid] = s;
-      }
-      __syncthreads();
-      for (int idx = tid; idx < P * P; idx += nt) {
-        const int i = idx / P, j = idx % P;
-        const T si = rs[i], sj = rs[j];
-        if (si == T(0) && sj == T(0)) continue;
-        const T ci = rc[i], cj = rc[j];
-        const int p = pp[i], q = pq[i], p2 = pp[j], q2 = pq[j];
-        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
-        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
-        const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
-        const T y10 = x10 * cj - x11 * sj, y11 = x10 * sj + x11 * cj;
-        T z00 = ci * y00 - si * y10, z01 = ci * y01 - si * y11;
-        T z10 = si * y00 + ci * y10, z11 = si * y01 + ci * y11;
-        if (i == j) z01 = z10 = T(0);
-        A[p * LD + p2] = z00;
-        A[p * LD + q2] = z01;
-        A[q * LD + p2] = z10;
-        A[q * LD + q2] = z11;
-      }
-      for (int idx = tid; idx < D * P; idx += nt) {
-        const int row = idx / P, j = idx % P;
-        const T sj = rs[j];
-        if (sj == T(0)) continue;
-        const T cj = rc[j];
-        const int p = pp[j], q = pq[j];
-        const T vp = V[row * LD + p], vq = V[row * LD + q];
-        V[row * LD + p] = cj * vp - sj * vq;
-        V[row * LD + q] = sj * vp + cj * vq;
-      }
-      __syncthreads();
-    }
-    const int more = *flag;
-    __syncthreads();
-    if (!more) break;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Host launchers
-// ---------------------------------------------------------------------------
 
 static AttnArgs make_args(const Work* w, const void* q, const void* k, const void* v, void* out) {
   AttnArgs a{};

@@ -1,0 +1,99 @@
+// Symmetric eigensolver used by the response bases (App. B.1, B.2) and the
+// probe-residual basis (App. A.3 eq. app_probe_residual_basis): parallel
+// cyclic Jacobi in LDS, one block of NT threads per matrix.
+//
+// Each step applies the D/2 disjoint rotations of the round-robin (circle)
+// ordering.  One thread per pair computes the rotation; then A <- J^T A J is
+// applied as independent 2x2 blocks (pair i rows x pair j columns) and
+// V <- V J as independent row pairs, in one pass with one barrier.  With
+// NT a multiple of D/2 every thread keeps the same column pair j for the
+// whole step, so its rotation is read from LDS once.  On return A's diagonal
+// holds the eigenvalues and V's columns the eigenvectors (row stride D + 1).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+namespace sparsepr {
+
+template <typename T>
+struct alignas(16) JacobiRot {
+  T c, s;
+  int p, q;
+};
+
+template <int D, typename T, int NT>
+__device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
+  constexpr int LD = D + 1, P = D / 2;
+  static_assert(NT % P == 0 && (P * P) % NT == 0 && (D * P) % NT == 0, "thread mapping");
+  const int tid = threadIdx.x;
+  for (int i = tid; i < D * D; i += NT) {
+    const int r = i / D, c = i % D;
+    V[r * LD + c] = (r == c) ? T(1) : T(0);
+  }
+  __syncthreads();
+  for (int sweep = 0; sweep < 20; ++sweep) {
+    if (tid == 0) *flag = 0;
+    __syncthreads();
+    for (int step = 0; step < D - 1; ++step) {
+      if (tid < P) {
+        int p, q;
+        if (tid == 0) {
+          p = step;
+          q = D - 1;
+        } else {
+          p = (step + tid) % (D - 1);
+          q = (step - tid + D - 1) % (D - 1);
+        }
+        const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
+        T c = 1, s = 0;
+        const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
+        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
+          const T theta = (aqq - app) / (T(2) * apq);
+          const T at = fabs(theta);
+          const T t = (at > T(1e10)) ? T(0.5) / theta
+                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
+          c = T(1) / sqrt(t * t + T(1));
+          s = t * c;
+          *flag = 1;
+        }
+        rot[tid] = JacobiRot<T>{c, s, p, q};
+      }
+      __syncthreads();
+      const int j = tid % P;
+      const JacobiRot<T> rj = rot[j];
+#pragma unroll
+      for (int k = 0; k < P * P / NT; ++k) {
+        const int i = tid / P + k * (NT / P);
+        const JacobiRot<T> ri = rot[i];
+        if (ri.s == T(0) && rj.s == T(0)) continue;
+        const int p = ri.p, q = ri.q, p2 = rj.p, q2 = rj.q;
+        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
+        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
+        const T y00 = x00 * rj.c - x01 * rj.s, y01 = x00 * rj.s + x01 * rj.c;
+        const T y10 = x10 * rj.c - x11 * rj.s, y11 = x10 * rj.s + x11 * rj.c;
+        T z00 = ri.c * y00 - ri.s * y10, z01 = ri.c * y01 - ri.s * y11;
+        T z10 = ri.s * y00 + ri.c * y10, z11 = ri.s * y01 + ri.c * y11;
+        if (i == j) z01 = z10 = T(0);
+        A[p * LD + p2] = z00;
+        A[p * LD + q2] = z01;
+        A[q * LD + p2] = z10;
+        A[q * LD + q2] = z11;
+      }
+      if (rj.s != T(0)) {
+#pragma unroll
+        for (int k = 0; k < D * P / NT; ++k) {
+          const int row = tid / P + k * (NT / P);
+          const T vp = V[row * LD + rj.p], vq = V[row * LD + rj.q];
+          V[row * LD + rj.p] = rj.c * vp - rj.s * vq;
+          V[row * LD + rj.q] = rj.s * vp + rj.c * vq;
+        }
+      }
+      __syncthreads();
+    }
+    const int more = *flag;
+    __syncthreads();
+    if (!more) break;
+  }
+}
+
+}  // namespace sparsepr

@@ -17,6 +17,7 @@
 
 #include "device_utils.hpp"
 #include "sparsepr_internal.hpp"
+#include "jacobi_lds.hpp"
 
 namespace sparsepr {
 
@@ -72,96 +73,6 @@ __global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, doubl
   for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / (double)g.Ms;
 }
 
-// ---------------------------------------------------------------------------
-// Symmetric eigensolver: parallel cyclic Jacobi in LDS, one block of 1024
-// threads per matrix (double for d = 64, float for d = 128, whose two d x d
-// matrices would not fit in LDS in double).  Each step applies D/2 disjoint rotations chosen by
-// the round-robin (circle) ordering; A <- J^T A J on 2x2 blocks, V <- V J.
-// On return the eigenvalues are on A's diagonal and V's columns hold the
-// eigenvectors.
-// ---------------------------------------------------------------------------
-
-__device__ __forceinline__ void rr_pair(int step, int i, int n, int& p, int& q) {
-  if (i == 0) {
-    p = step;
-    q = n - 1;
-  } else {
-    p = (step + i) % (n - 1);
-    q = (step - i + n - 1) % (n - 1);
-  }
-}
-
-template <int D, typename T>
-__device__ void jacobi_eig_lds(T* A, T* V, T* rc, T* rs, int* flag) {
-  constexpr int LD = D + 1, P = D / 2;
-  __shared__ int pp[P], pq[P];  // this step's rotation pairs
-  const int tid = threadIdx.x, nt = blockDim.x;
-  for (int i = tid; i < D * D; i += nt) {
-    const int r = i / D, c = i % D;
-    V[r * LD + c] = (r == c) ? T(1) : T(0);
-  }
-  __syncthreads();
-  for (int sweep = 0; sweep < 20; ++sweep) {
-    if (tid == 0) *flag = 0;
-    __syncthreads();
-    for (int step = 0; step < D - 1; ++step) {
-      if (tid < P) {
-        int p, q;
-        rr_pair(step, tid, D, p, q);
-        pp[tid] = p;
-        pq[tid] = q;
-        const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
-        T c = 1, s = 0;
-        const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
-        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
-          const T theta = (aqq - app) / (T(2) * apq);
-          const T at = fabs(theta);
-          const T t = (at > T(1e10)) ? T(0.5) / theta
-                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
-          c = T(1) / sqrt(t * t + T(1));
-          s = t * c;
-          *flag = 1;
-        }
-        rc[tid] = c;
-        rs[tid] = s;
-      }
-      __syncthreads();
-      for (int idx = tid; idx < P * P; idx += nt) {
-        const int i = idx / P, j = idx % P;
-        const T si = rs[i], sj = rs[j];
-        if (si == T(0) && sj == T(0)) continue;
-        const T ci = rc[i], cj = rc[j];
-        const int p = pp[i], q = pq[i], p2 = pp[j], q2 = pq[j];
-        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
-        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
-        const T y00 = x00 * cj - x01 * sj, y01 = x00 * sj + x01 * cj;
-        const T y10 = x10 * cj - x11 * sj, y11 = x10 * sj + x11 * cj;
-        T z00 = ci * y00 - si * y10, z01 = ci * y01 - si * y11;
-        T z10 = si * y00 + ci * y10, z11 = si * y01 + ci * y11;
-        if (i == j) z01 = z10 = T(0);
-        A[p * LD + p2] = z00;
-        A[p * LD + q2] = z01;
-        A[q * LD + p2] = z10;
-        A[q * LD + q2] = z11;
-      }
-      for (int idx = tid; idx < D * P; idx += nt) {
-        const int row = idx / P, j = idx % P;
-        const T sj = rs[j];
-        if (sj == T(0)) continue;
-        const T cj = rc[j];
-        const int p = pp[j], q = pq[j];
-        const T vp = V[row * LD + p], vq = V[row * LD + q];
-        V[row * LD + p] = cj * vp - sj * vq;
-        V[row * LD + q] = sj * vp + cj * vq;
-      }
-      __syncthreads();
-    }
-    const int more = *flag;
-    __syncthreads();
-    if (!more) break;
-  }
-}
-
 // Sort the eigenvalues on A's diagonal in descending order (ties by index):
 // order[t] = index of the t-th largest.  Needs D threads.
 template <int D, typename T>
@@ -190,7 +101,7 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   constexpr int LD = D + 1;
   __shared__ T A[D * LD];
   __shared__ T V[D * LD];
-  __shared__ T rc[D / 2], rs[D / 2];
+  __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
   __shared__ double lam[D];
   __shared__ int flag;
@@ -199,7 +110,7 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   const double* G = gram + (size_t)bh * D * D;
   for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
   __syncthreads();
-  jacobi_eig_lds<D, T>(A, V, rc, rs, &flag);
+  jacobi_eig_lds<D, T, 1024>(A, V, rot, &flag);
   eig_order<D, T>(A, order);
   const double l1 = A[order[0] * LD + order[0]];
   if (tid < D) {
@@ -224,24 +135,27 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 
 // ---------------------------------------------------------------------------
 // Response coordinates phi = F^T x (eq. key_response_feature), optionally
-// divided by max(RMS, eps) (eq. query_response_feature).  64 rows per block,
-// four threads per row.
+// divided by max(RMS, eps) (eq. query_response_feature).  64 rows per block;
+// thread (ty, tx) computes rows ty + 16u (u < 4) x columns [tx*CPT, tx*CPT +
+// CPT), so each LDS read of F feeds four rows.
 // ---------------------------------------------------------------------------
 
 template <int D, int MAXR>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
                                                  int rms, float eps, float* phi, int64_t* stats) {
-  // 64 rows per block, 4 threads per row, MAXR/4 output columns per thread;
-  // the row tile and F are staged in LDS, outputs are written as float4
-  constexpr int ROWS = 64, CPT = MAXR / 4;
-  __shared__ float xs[ROWS][D + 4];
+  constexpr int ROWS = 64, CPT = MAXR / 16;
+  __shared__ float xs[ROWS][D + 1];
   __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int r0 = blockIdx.x * ROWS;
   const float* Fh = F + (size_t)bh * D * R;
-  for (int i = tid; i < D * MAXR; i += 256) {
-    const int k = i / MAXR, c = i % MAXR;
-    fs[i] = c < R ? Fh[k * R + c] : 0.f;
+  if (R == MAXR) {
+    for (int i = tid; i < D * MAXR / 4; i += 256) ((float4*)fs)[i] = ((const float4*)Fh)[i];
+  } else {
+    for (int i = tid; i < D * MAXR; i += 256) {
+      const int k = i / MAXR, c = i % MAXR;
+      fs[i] = c < R ? Fh[k * R + c] : 0.f;
+    }
   }
   const int64_t base = head_base(g, bh);
   for (int i = tid; i < ROWS * D / 8; i += 256) {
@@ -272,36 +186,46 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
     for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
   }
   __syncthreads();
-  const int rr = tid >> 2, part = tid & 3;
-  float acc[CPT];
+  const int ty = tid >> 4, tx = tid & 15;
+  float acc[4][CPT];
 #pragma unroll
-  for (int u = 0; u < CPT; ++u) acc[u] = 0.f;
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) acc[u][c] = 0.f;
   for (int k = 0; k < D; ++k) {
-    const float xk = xs[rr][k];
-    const float* fr = fs + k * MAXR + part * CPT;
+    float xv[4], fv[CPT];
 #pragma unroll
-    for (int u = 0; u < CPT; ++u) acc[u] = fmaf(xk, fr[u], acc[u]);
-  }
-  float den = 1.f;
-  if (rms) {
-    float ss = 0.f;
+    for (int u = 0; u < 4; ++u) xv[u] = xs[ty + 16 * u][k];
 #pragma unroll
-    for (int u = 0; u < CPT; ++u) ss = fmaf(acc[u], acc[u], ss);
-    ss += __shfl_xor(ss, 1);
-    ss += __shfl_xor(ss, 2);
-    den = fmaxf(sqrtf(ss / (float)R), eps);
+    for (int c = 0; c < CPT; ++c) fv[c] = fs[k * MAXR + tx * CPT + c];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) acc[u][c] = fmaf(xv[u], fv[c], acc[u][c]);
   }
-  const int row = r0 + rr;
-  if (row >= g.NV) return;
-  float* out = phi + ((size_t)bh * g.NV + row) * R;
   bool bad = false;
 #pragma unroll
-  for (int u = 0; u < CPT; ++u) {
-    const int c = part * CPT + u;
-    if (c < R) {
-      const float v = acc[u] / den;
-      bad |= !isfinite(v);
-      out[c] = v;
+  for (int u = 0; u < 4; ++u) {
+    float den = 1.f;
+    if (rms) {
+      float ss = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) ss = fmaf(acc[u][c], acc[u][c], ss);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
+      den = fmaxf(sqrtf(ss / (float)R), eps);
+    }
+    const int row = r0 + ty + 16 * u;
+    if (row >= g.NV) continue;
+    float* out = phi + ((size_t)bh * g.NV + row) * R;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int col = tx * CPT + c;
+      if (col < R) {
+        const float v = acc[u][c] / den;
+        bad |= !isfinite(v);
+        out[col] = v;
+      }
     }
   }
   if (bad)
@@ -577,33 +501,54 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
 }
 
 // Exact scan (the defining float score) for the points the screen could not
-// decide.  One wave per point: each lane scores a strided subset of the
-// centroids with the float chain, then the wave keeps the smallest score and
-// the lowest index among equal scores.
+// decide.  A block takes 64 such points at a time (one per four threads, the
+// point in registers) and streams the centroids through LDS in 64-row
+// chunks; each thread scores every fourth centroid of a chunk with the float
+// chain, and the four partial minima of a point (lowest index among equal
+// scores) are merged with two exchanges.
+template <int RP>
 __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
-  const int bh = blockIdx.y, lane = threadIdx.x & 63;
+  constexpr int PB = 64, CB = 64;
+  __shared__ float cs[CB][RP + 1];
+  __shared__ float us[CB];
+  const int bh = blockIdx.y, tid = threadIdx.x;
   if (km_skip_assign(a, bh, it)) return;
   const int cnt = a.fbcnt[(size_t)bh * 2 * a.T + a.sel * a.T + it];
   const float* cu = a.cu + (size_t)bh * a.CP;
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwave = gridDim.x * 4;
-  for (int e = wave; e < cnt; e += nwave) {
-    const int j = a.fb[(size_t)bh * a.n + e];
-    const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
+  const int R = a.R;
+  const int pi = tid >> 2, part = tid & 3;
+  for (int e0 = blockIdx.x * PB; e0 < cnt; e0 += gridDim.x * PB) {
+    const int e = e0 + pi;
+    const bool valid = e < cnt;
+    const int j = valid ? a.fb[(size_t)bh * a.n + e] : 0;
+    float x[RP];
+    const float* xp = a.pts + ((size_t)bh * a.n + j) * R;
+#pragma unroll
+    for (int k = 0; k < RP; ++k) x[k] = (valid && k < R) ? xp[k] : 0.f;
     float best = INFINITY;
     int bi = 0x7fffffff;
-    for (int b = lane; b < a.C; b += 64) {
-      const float* cb = a.cent + ((size_t)bh * a.C + b) * a.R;
-      float t = 0.f;
-      for (int k = 0; k < a.R; ++k) t = fmaf(xp[k], cb[k], t);
-      const float sc = fmaf(-2.f, t, cu[b]);
-      if (sc < best) {  // b ascending within the lane: ties keep the lower index
-        best = sc;
-        bi = b;
+    for (int b0 = 0; b0 < a.C; b0 += CB) {
+      __syncthreads();
+      for (int i = tid; i < CB * RP; i += 256) {
+        const int b = b0 + i / RP, k = i % RP;
+        cs[i / RP][k] = (b < a.C && k < R) ? a.cent[((size_t)bh * a.C + b) * R + k] : 0.f;
+      }
+      if (tid < CB) us[tid] = (b0 + tid < a.C) ? cu[b0 + tid] : INFINITY;
+      __syncthreads();
+      for (int bb = part; bb < CB && b0 + bb < a.C; bb += 4) {
+        float t = 0.f;
+#pragma unroll
+        for (int k = 0; k < RP; ++k) t = fmaf(x[k], cs[bb][k], t);
+        const float sc = fmaf(-2.f, t, us[bb]);
+        if (sc < best) {  // centroids ascending within the thread: ties keep the lower index
+          best = sc;
+          bi = b0 + bb;
+        }
       }
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
+    for (int o = 1; o < 4; o <<= 1) {
       const float ob = __shfl_xor(best, o);
       const int oi = __shfl_xor(bi, o);
       if (ob < best || (ob == best && oi < bi)) {
@@ -611,7 +556,7 @@ __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
         bi = oi;
       }
     }
-    if (lane == 0) {
+    if (valid && part == 0) {
       const int old = lab[j];
       lab[j] = bi;
       if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
@@ -705,10 +650,23 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   const int s0 = off[b], s1 = off[b + 1];
   if (s1 == s0) return;
   const float* pts = a.pts + (size_t)bh * a.n * a.R;
-  for (int k = lane; k < a.R; k += 64) {
+  const int R = a.R;
+  for (int k = lane; k < R; k += 64) {
+    // members loaded four at a time, added in ascending order
     double sum = 0.0;
-    for (int m = s0; m < s1; ++m) sum += (double)pts[(size_t)(perm[m] - a.row0) * a.R + k];
-    a.cent[((size_t)bh * a.C + b) * a.R + k] = (float)(sum / (double)(s1 - s0));
+    int m = s0;
+    for (; m + 4 <= s1; m += 4) {
+      const float v0 = pts[(size_t)(perm[m] - a.row0) * R + k];
+      const float v1 = pts[(size_t)(perm[m + 1] - a.row0) * R + k];
+      const float v2 = pts[(size_t)(perm[m + 2] - a.row0) * R + k];
+      const float v3 = pts[(size_t)(perm[m + 3] - a.row0) * R + k];
+      sum += (double)v0;
+      sum += (double)v1;
+      sum += (double)v2;
+      sum += (double)v3;
+    }
+    for (; m < s1; ++m) sum += (double)pts[(size_t)(perm[m] - a.row0) * R + k];
+    a.cent[((size_t)bh * a.C + b) * R + k] = (float)(sum / (double)(s1 - s0));
   }
 }
 
@@ -732,6 +690,8 @@ __global__ void k_prefix_group(KmArgs a) {
 __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const int32_t* perm,
                                                     const int32_t* off, int C, int offstride,
                                                     float* mean) {
+  // lane l owns channels 2l and 2l + 1; rows are loaded four at a time and
+  // added in ascending order
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + wv;
   if (b >= C) return;
@@ -739,10 +699,33 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
   const int32_t* o = off + (size_t)bh * offstride;
   const int32_t* p = perm + (size_t)bh * g.N;
   const int s0 = o[b], s1 = o[b + 1];
-  for (int c = lane; c < g.d; c += 64) {
-    double sum = 0.0;
-    for (int m = s0; m < s1; ++m) sum += (double)load_x(x, g.bf16, base + (int64_t)p[m] * g.sn + c);
-    mean[((size_t)bh * C + b) * g.d + c] = (s1 > s0) ? (float)(sum / (double)(s1 - s0)) : 0.f;
+  for (int c = 2 * lane; c < g.d; c += 128) {
+    double s0d = 0.0, s1d = 0.0;
+    auto ld2 = [&](int m) -> float2 {
+      const int64_t idx = base + (int64_t)p[m] * g.sn + c;
+      if (g.bf16) {
+        const uint32_t u = *(const uint32_t*)((const uint16_t*)x + idx);
+        return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+      }
+      return *(const float2*)((const float*)x + idx);
+    };
+    int m = s0;
+    for (; m + 4 <= s1; m += 4) {
+      const float2 v0 = ld2(m), v1 = ld2(m + 1), v2 = ld2(m + 2), v3 = ld2(m + 3);
+      s0d += (double)v0.x; s1d += (double)v0.y;
+      s0d += (double)v1.x; s1d += (double)v1.y;
+      s0d += (double)v2.x; s1d += (double)v2.y;
+      s0d += (double)v3.x; s1d += (double)v3.y;
+    }
+    for (; m < s1; ++m) {
+      const float2 v = ld2(m);
+      s0d += (double)v.x;
+      s1d += (double)v.y;
+    }
+    const double n = (double)(s1 - s0);
+    float* dst = mean + ((size_t)bh * C + b) * g.d + c;
+    dst[0] = (s1 > s0) ? (float)(s0d / n) : 0.f;
+    dst[1] = (s1 > s0) ? (float)(s1d / n) : 0.f;
   }
 }
 
@@ -752,18 +735,22 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
 template <int D>
 __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const int32_t* offk,
                                                       Geom g, double* gram) {
-  constexpr int ENT = D * D / 256;
-  constexpr int GB = 16;
+  // block (x, bh) computes output rows [8x, 8x + 8); every entry is summed
+  // over the groups in ascending order
+  constexpr int RB = 8, GB = 32;
+  constexpr int TPR = 256 / RB;       // threads per output row
+  constexpr int ENT = D / TPR;        // entries per thread
   __shared__ double mu[D];
-  __shared__ double ks[GB][D];
+  __shared__ double ks[GB][D + 1];
   __shared__ int cplus;
-  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int bh = blockIdx.y, tid = threadIdx.x;
   const int C = g.CK;
   const int32_t* o = offk + (size_t)bh * (g.CKt + 1);
   const float* kb = kbar + (size_t)bh * C * D;
   if (tid < D) {
     double s = 0.0;
     int cp = 0;
+#pragma unroll 8
     for (int b = 0; b < C; ++b)
       if (o[b + 1] > o[b]) {
         s += (double)kb[(size_t)b * D + tid];
@@ -773,7 +760,7 @@ __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const i
     if (tid == 0) cplus = cp;
   }
   __syncthreads();
-  const int e0 = tid * ENT, ra = e0 / D, cb = e0 % D;
+  const int ra = blockIdx.x * RB + tid / TPR, cb = (tid % TPR) * ENT;
   double acc[ENT];
 #pragma unroll
   for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
@@ -785,7 +772,8 @@ __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const i
       ks[t / D][c] = v;
     }
     __syncthreads();
-    for (int i = 0; i < GB; ++i) {
+    const int cnt = min(GB, C - b0);
+    for (int i = 0; i < cnt; ++i) {
       const double a = ks[i][ra];
 #pragma unroll
       for (int e = 0; e < ENT; ++e) acc[e] += a * ks[i][cb + e];
@@ -793,9 +781,9 @@ __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const i
     __syncthreads();
   }
   const double den = (double)max(cplus, 1) * (double)D;
-  double* out = gram + (size_t)bh * D * D;
+  double* out = gram + (size_t)bh * D * D + (size_t)ra * D + cb;
 #pragma unroll
-  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / den;
+  for (int e = 0; e < ENT; ++e) out[e] = acc[e] / den;
 }
 
 // ---------------------------------------------------------------------------
@@ -808,93 +796,108 @@ __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const i
 // |G_a||G_b| fits in the budget, which already excludes the probes' cost.
 // ---------------------------------------------------------------------------
 
+template <int D>
 __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const float* kbar, Geom g,
                                                     const int32_t* offq, const int32_t* offk,
                                                     float* prio, int32_t* forced) {
-  extern __shared__ float sm[];  // qrow[d] | s[CK]
-  __shared__ double red[4];
-  __shared__ float redf[4];
-  __shared__ int redi[4];
-  const int a = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
-  const int lane = tid & 63, wv = tid >> 6;
-  const int CK = g.CK, D = g.d;
+  // Block (x, bh) owns query groups [64x, 64x + 64).  Phase 1: s_ab for every
+  // K/V group in 64 x 64 tiles staged in LDS, 4 x 4 cells per thread, each
+  // the fmaf chain over the dims in index order.  Phase 2: one wave per query
+  // group computes lse_a in double, pi_ab and the forced (best) cell.
+  constexpr int TR = 64;
+  __shared__ float qs[TR][D + 1];
+  __shared__ float ks[TR][D + 1];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int a0 = blockIdx.x * TR;
+  const int CK = g.CK, CQ = g.CQ;
   const int32_t* oq = offq + (size_t)bh * (g.CQt + 1);
   const int32_t* ok = offk + (size_t)bh * (g.CKt + 1);
-  float* pr = prio + ((size_t)bh * g.CQ + a) * CK;
-  const int na = oq[a + 1] - oq[a];
-  if (na == 0) {
-    for (int b = tid; b < CK; b += 256) pr[b] = 0.f;
-    if (tid == 0) forced[(size_t)bh * g.CQ + a] = -1;
-    return;
-  }
-  float* qrow = sm;
-  float* s = sm + D;
-  for (int c = tid; c < D; c += 256) qrow[c] = qbar[((size_t)bh * g.CQ + a) * D + c];
-  __syncthreads();
   const float scale = (float)(1.0 / sqrt((double)D));
+  const float* qb = qbar + (size_t)bh * CQ * D;
   const float* kb = kbar + (size_t)bh * CK * D;
-  float mx = -INFINITY;
-  for (int b = tid; b < CK; b += 256) {
-    float v = -INFINITY;
-    if (ok[b + 1] > ok[b]) {
-      float t = 0.f;
-      for (int c = 0; c < D; ++c) t = fmaf(qrow[c], kb[(size_t)b * D + c], t);
-      v = t * scale;
+  float* prh = prio + (size_t)bh * CQ * CK;
+  for (int i = tid; i < TR * D; i += 256) {
+    const int r = i / D, c = i % D;
+    qs[r][c] = (a0 + r < CQ) ? qb[(size_t)(a0 + r) * D + c] : 0.f;
+  }
+  const int ty = tid >> 4, tx = tid & 15;
+  for (int b0 = 0; b0 < CK; b0 += TR) {
+    __syncthreads();
+    for (int i = tid; i < TR * D; i += 256) {
+      const int r = i / D, c = i % D;
+      ks[r][c] = (b0 + r < CK) ? kb[(size_t)(b0 + r) * D + c] : 0.f;
     }
-    s[b] = v;
-    mx = fmaxf(mx, v);
-  }
-  mx = wave_max(mx);
-  if (lane == 0) redf[wv] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
-  double z = 0.0;
-  for (int b = tid; b < CK; b += 256) {
-    const int nb = ok[b + 1] - ok[b];
-    if (nb > 0) z += (double)nb * exp((double)s[b] - (double)mx);
-  }
-  z = wave_sum_d(z);
-  if (lane == 0) red[wv] = z;
-  __syncthreads();
-  const float lse = (float)((double)mx + log(red[0] + red[1] + red[2] + red[3]));
-  float bestv = -INFINITY;
-  int besti = 0x7fffffff;
-  for (int b = tid; b < CK; b += 256) {
-    float p = 0.f;
-    if (ok[b + 1] > ok[b]) {
-      p = s[b] - lse;
-      if (besti == 0x7fffffff || p > bestv || (p == bestv && b < besti)) {
-        bestv = p;
-        besti = b;
-      }
-    }
-    pr[b] = p;
-  }
+    __syncthreads();
+    float acc[4][4];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(bestv, o);
-    const int oi = __shfl_xor(besti, o);
-    if (oi != 0x7fffffff && (besti == 0x7fffffff || ov > bestv || (ov == bestv && oi < besti))) {
-      bestv = ov;
-      besti = oi;
-    }
-  }
-  __syncthreads();
-  if (lane == 0) {
-    redf[wv] = bestv;
-    redi[wv] = besti;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    float bv = redf[0];
-    int bi = redi[0];
-    for (int k = 1; k < 4; ++k)
-      if (redi[k] != 0x7fffffff &&
-          (bi == 0x7fffffff || redf[k] > bv || (redf[k] == bv && redi[k] < bi))) {
-        bv = redf[k];
-        bi = redi[k];
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[u][v] = 0.f;
+    for (int c = 0; c < D; ++c) {
+      float qv[4], kv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        qv[u] = qs[ty + 16 * u][c];
+        kv[u] = ks[tx + 16 * u][c];
       }
-    forced[(size_t)bh * g.CQ + a] = (bi == 0x7fffffff) ? -1 : bi;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(qv[u], kv[v], acc[u][v]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int a = a0 + ty + 16 * u, b = b0 + tx + 16 * v;
+        if (a < CQ && b < CK) prh[(size_t)a * CK + b] = acc[u][v] * scale;
+      }
+  }
+  __syncthreads();
+  const int wv = tid >> 6, lane = tid & 63;
+  for (int rr = wv; rr < TR; rr += 4) {
+    const int a = a0 + rr;
+    if (a >= CQ) break;
+    float* pr = prh + (size_t)a * CK;
+    if (oq[a + 1] == oq[a]) {
+      for (int b = lane; b < CK; b += 64) pr[b] = 0.f;
+      if (lane == 0) forced[(size_t)bh * CQ + a] = -1;
+      continue;
+    }
+    float mx = -INFINITY;
+    for (int b = lane; b < CK; b += 64)
+      if (ok[b + 1] > ok[b]) mx = fmaxf(mx, pr[b]);
+    mx = wave_max(mx);
+    double z = 0.0;
+    for (int b = lane; b < CK; b += 64) {
+      const int nb = ok[b + 1] - ok[b];
+      if (nb > 0) z += (double)nb * exp((double)pr[b] - (double)mx);
+    }
+    z = wave_sum_d(z);
+    const float lse = (float)((double)mx + log(z));
+    float bestv = -INFINITY;
+    int besti = 0x7fffffff;
+    for (int b = lane; b < CK; b += 64) {
+      float pv = 0.f;
+      if (ok[b + 1] > ok[b]) {
+        pv = pr[b] - lse;
+        if (besti == 0x7fffffff || pv > bestv) {  // b ascending within the lane
+          bestv = pv;
+          besti = b;
+        }
+      }
+      pr[b] = pv;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bestv, o);
+      const int oi = __shfl_xor(besti, o);
+      if (oi != 0x7fffffff && (besti == 0x7fffffff || ov > bestv || (ov == bestv && oi < besti))) {
+        bestv = ov;
+        besti = oi;
+      }
+    }
+    if (lane == 0) forced[(size_t)bh * CQ + a] = (besti == 0x7fffffff) ? -1 : besti;
   }
 }
 
@@ -1125,7 +1128,21 @@ __global__ void k_probe_d2(Geom g, Work w) {
   const float* ph = w.phiq + ((size_t)bh * g.NV + i) * g.rq;
   const float* c = w.centq + ((size_t)bh * g.CQ + a) * g.rq;
   float acc = 0.f;
-  for (int k = 0; k < g.rq; ++k) {
+  int k = 0;
+  if ((g.rq & 3) == 0) {
+    for (; k < g.rq; k += 4) {
+      const float4 p4 = *(const float4*)(ph + k), c4 = *(const float4*)(c + k);
+      float diff = p4.x - c4.x;
+      acc = fmaf(diff, diff, acc);
+      diff = p4.y - c4.y;
+      acc = fmaf(diff, diff, acc);
+      diff = p4.z - c4.z;
+      acc = fmaf(diff, diff, acc);
+      diff = p4.w - c4.w;
+      acc = fmaf(diff, diff, acc);
+    }
+  }
+  for (; k < g.rq; ++k) {
     const float diff = ph[k] - c[k];
     acc = fmaf(diff, diff, acc);
   }
@@ -1323,7 +1340,7 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  k_km_fallback<<<dim3(64, BH), 256, 0, s>>>(a, it);
+  k_km_fallback<MAXR><<<dim3(16, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
@@ -1373,7 +1390,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
                                                          w.kbar);
-  k_query_metric<D><<<BH, 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
+  k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
   project<D>(g, q, w.fq, g.rq, 1, g.eps_q, w.phiq, w.stats, s);
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
@@ -1383,8 +1400,8 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
                                                          w.qbar);
   // Routing (Sec. 4.3)
-  k_route_prio<<<dim3(g.CQ, BH), 256, (g.d + g.CK) * sizeof(float), s>>>(
-      w.qbar, w.kbar, g, w.offq, w.offk, w.prio, w.forced);
+  k_route_prio<D><<<dim3((g.CQ + 63) / 64, BH), 256, 0, s>>>(w.qbar, w.kbar, g, w.offq, w.offk,
+                                                             w.prio, w.forced);
   k_sel_init<<<BH, 256, 0, s>>>(g, w);
   const int64_t ncell = (int64_t)g.CQ * g.CK;
   const int gsel = (int)std::min<int64_t>(std::max<int64_t>((ncell + 4095) / 4096, 1), 512);
