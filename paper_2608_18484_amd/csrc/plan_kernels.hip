@@ -384,12 +384,23 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
     bhi[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xh + ks * 16 + h * 8));
     blo[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
   }
-  // three smallest estimates (value, centroid) of this lane, ascending
-  float t1 = INFINITY, t2 = INFINITY, t3 = INFINITY, umax = 0.f;
-  int i1 = -1, i2 = -1, i3 = -1;
+  // Largest centroid squared norm of the head (for the error bound).
+  __shared__ float sred[4];
+  float umax = 0.f;
+  const float* cu = a.cu + (size_t)bh * a.CP;
+  for (int b = tid; b < a.C; b += 256) umax = fmaxf(umax, cu[b]);
+  umax = wave_max(umax);
+  if (lane == 0) sred[wv] = umax;
+  // Three smallest estimates of this lane, ascending, each with its centroid
+  // index in the low IB mantissa bits (C <= 2^IB).  Replacing those bits
+  // moves a value by at most 2^(IB-23) of its magnitude, which the decision
+  // below adds to the error bound.  Keeping (value, index) in one float lets
+  // min / med3 maintain the sorted triple in three instructions per score.
+  const int ib = 32 - __clz(a.CP - 1);
+  const uint32_t imask = (1u << ib) - 1u;
+  float t1 = INFINITY, t2 = INFINITY, t3 = INFINITY;
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
-  const float* cu = a.cu + (size_t)bh * a.CP;
   for (int c0 = 0; c0 < a.CP; c0 += 32) {
     __syncthreads();
     for (int i = tid; i < 32 * RP / 8; i += 256) {
@@ -397,7 +408,9 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       *(uint4*)(shi + r * LD + c8 * 8) = *(const uint4*)(chi + (size_t)(c0 + r) * RP + c8 * 8);
       *(uint4*)(slo + r * LD + c8 * 8) = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
     }
-    if (tid < 32) su[tid] = cu[c0 + tid];
+    // padding centroids get a huge finite norm: their scores stay finite
+    // (an index packed into +inf would make a NaN) and never win
+    if (tid < 32) su[tid] = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
     __syncthreads();
     f32x16 S;
 #pragma unroll
@@ -410,73 +423,49 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, blo[ks], S, 0, 0, 0);
       S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bhi[ks], S, 0, 0, 0);
     }
-    // register i holds centroid c0 + (i/4)*8 + h*4 + i%4 (ascending in i)
+    // register i holds centroid c0 + (i/4)*8 + h*4 + i%4
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int r = (i >> 2) * 8 + h * 4 + (i & 3);
-      const float u = su[r];
-      const float sh = fmaf(-2.f, S[i], u);
-      if (c0 + r < a.C) umax = fmaxf(umax, u);
-      if (sh < t3) {
-        const int cb = c0 + r;
-        if (sh < t2) {
-          t3 = t2;
-          i3 = i2;
-          if (sh < t1) {
-            t2 = t1;
-            i2 = i1;
-            t1 = sh;
-            i1 = cb;
-          } else {
-            t2 = sh;
-            i2 = cb;
-          }
-        } else {
-          t3 = sh;
-          i3 = cb;
-        }
+    for (int i4 = 0; i4 < 4; ++i4) {
+      const float4 u4 = *(const float4*)&su[i4 * 8 + h * 4];
+      const float uu[4] = {u4.x, u4.y, u4.z, u4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float sh = fmaf(-2.f, S[i4 * 4 + e], uu[e]);
+        const uint32_t idx = (uint32_t)(c0 + i4 * 8 + h * 4 + e);
+        const float pk = __uint_as_float((__float_as_uint(sh) & ~imask) | idx);
+        const float n3 = __builtin_amdgcn_fmed3f(t2, t3, pk);
+        const float n2 = __builtin_amdgcn_fmed3f(t1, t2, pk);
+        t1 = fminf(t1, pk);
+        t2 = n2;
+        t3 = n3;
       }
     }
   }
-  // merge with the other half of the centroids (lane l ^ 32, same point):
-  // insert its three entries (any order of equal values is fine: only the
-  // third smallest value decides whether the list holds every candidate)
+  // merge with the other half of the centroids (lane l ^ 32, same point)
   {
     const float o1 = __shfl_xor(t1, 32), o2 = __shfl_xor(t2, 32), o3 = __shfl_xor(t3, 32);
-    const int j1 = __shfl_xor(i1, 32), j2 = __shfl_xor(i2, 32), j3 = __shfl_xor(i3, 32);
-    auto ins = [&](float v, int idx) {
-      if (v < t3) {
-        if (v < t2) {
-          t3 = t2;
-          i3 = i2;
-          if (v < t1) {
-            t2 = t1;
-            i2 = i1;
-            t1 = v;
-            i1 = idx;
-          } else {
-            t2 = v;
-            i2 = idx;
-          }
-        } else {
-          t3 = v;
-          i3 = idx;
-        }
-      }
-    };
-    ins(o1, j1);
-    ins(o2, j2);
-    ins(o3, j3);
+    const float ov[3] = {o1, o2, o3};
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+      const float n3 = __builtin_amdgcn_fmed3f(t2, t3, ov[e]);
+      const float n2 = __builtin_amdgcn_fmed3f(t1, t2, ov[e]);
+      t1 = fminf(t1, ov[e]);
+      t2 = n2;
+      t3 = n3;
+    }
   }
-  umax = fmaxf(umax, __shfl_xor(umax, 32));
+  __syncthreads();
+  umax = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
   if (h != 0 || j >= a.n) return;
+  const int i1 = (int)(__float_as_uint(t1) & imask), i2 = (int)(__float_as_uint(t2) & imask);
   const float xn = a.xn[(size_t)bh * a.n + j];
   const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
+  const float ek = ldexpf(1.f, ib - 22);
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   int label;
-  if (t2 - t1 > 2.f * delta) {
+  if (t2 - t1 > 2.f * delta + ek * (fabsf(t1) + fabsf(t2))) {
     label = i1;  // unique candidate: the exact argmin
-  } else if (t3 - t1 > 2.f * delta) {
+  } else if (t3 - t1 > 2.f * delta + ek * (fabsf(t1) + fabsf(t3))) {
     // exactly two candidates: rescore both with the defining float score
     const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
     const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
@@ -509,7 +498,7 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
 template <int RP>
 __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
   constexpr int PB = 64, CB = 64;
-  __shared__ float cs[CB][RP + 1];
+  __shared__ __attribute__((aligned(16))) float cs[CB][RP + 4];
   __shared__ float us[CB];
   const int bh = blockIdx.y, tid = threadIdx.x;
   if (km_skip_assign(a, bh, it)) return;
@@ -539,7 +528,13 @@ __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
       for (int bb = part; bb < CB && b0 + bb < a.C; bb += 4) {
         float t = 0.f;
 #pragma unroll
-        for (int k = 0; k < RP; ++k) t = fmaf(x[k], cs[bb][k], t);
+        for (int k4 = 0; k4 < RP / 4; ++k4) {
+          const float4 c4 = *(const float4*)&cs[bb][4 * k4];
+          t = fmaf(x[4 * k4], c4.x, t);
+          t = fmaf(x[4 * k4 + 1], c4.y, t);
+          t = fmaf(x[4 * k4 + 2], c4.z, t);
+          t = fmaf(x[4 * k4 + 3], c4.w, t);
+        }
         const float sc = fmaf(-2.f, t, us[bb]);
         if (sc < best) {  // centroids ascending within the thread: ties keep the lower index
           best = sc;
@@ -1340,7 +1335,7 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  k_km_fallback<MAXR><<<dim3(16, BH), 256, 0, s>>>(a, it);
+  k_km_fallback<MAXR><<<dim3(32, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
