@@ -96,6 +96,10 @@ def main():
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention error check")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run one plain fp32 copy (x * 1 over 256 MiB in, 256 MiB out) before the "
+                         "timed region, so hardware counters of a known traffic can calibrate "
+                         "those of the attention kernel")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: every SparsePR head is an independent call, and "
@@ -125,6 +129,13 @@ def main():
         call()
     torch.cuda.synchronize()
     log("warmup done")
+    if args.copy_probe:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=q.device)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy probe: 268435456 bytes read, 268435456 bytes written")
 
     # timed region: K whole calls bracketed by synchronisation
     ev0 = torch.cuda.Event(enable_timing=True)

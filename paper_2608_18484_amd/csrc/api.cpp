@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -108,6 +109,7 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->osp, N * dv * 4);
   add(&w->odp, M * dv * 4);
   add(&w->part, M * g.nsplit * (dv + 2) * 4);
+  add(&w->mlst, N * 4 * 4);
   add(&w->fitv, 3 * dv * 4);
   add(&w->fity, dv * r * 4);
   add(&w->fitpsi, dv * r * 4);
@@ -197,6 +199,16 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.nchunk_max = (N + kQTile - 1) / kQTile + g.CQt;
   g.nchunk_per_xcd = (g.nchunk_max + 7) / 8;
   g.nsplit = (N + kProbeSplit - 1) / kProbeSplit;
+  {
+    // Key segments of the sparse attention: each launch reads one slice of
+    // the group-major K/V, sized to stay resident in one XCD's 4 MB L2 while
+    // every XCD works through that slice for all query groups (6 MiB measured
+    // best on the long-video workload among 2-12 MiB and a single pass).
+    const double head_kv = (double)N * (double)(g.d + g.dv) * (g.bf16 ? 2.0 : 4.0);
+    double seg_bytes = 6.0 * 1024 * 1024;
+    if (const char* e = getenv("SPARSEPR_SEG_KB")) seg_bytes = std::max(64.0, atof(e)) * 1024.0;
+    g.nseg = (int)std::min(64.0, std::max(1.0, std::ceil(head_kv / seg_bytes)));
+  }
   g.nsort_blk = (NV + kSortBlock - 1) / kSortBlock;
   g.nsort_blk_full = (N + kSortBlock - 1) / kSortBlock;
   g.cmax = std::max(g.CKt, g.CQt);

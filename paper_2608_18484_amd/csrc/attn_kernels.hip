@@ -49,6 +49,10 @@ struct AttnArgs {
   const int32_t* nprobes;
   const uint16_t* kperm;
   const uint16_t* vperm;
+  // MODE_SPARSE key segment: only keys at group-major positions in
+  // [seg_lo, seg_hi) are processed; (O, m, l) carry over between segments
+  float* mlst;
+  int seg_lo, seg_hi, seg_first, seg_last;
 };
 
 // Where the rows and keys of one block come from.
@@ -197,7 +201,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     w.nrows = c.z;
     w.nkeys = c.w;
     w.k0 = 0;
-    if (w.nrows <= 0 || w.nkeys <= 0) return;
+    if (w.nrows <= 0 || w.nkeys <= 0) return;  // every routed query group has keys
     Kp = A.kperm + (size_t)bh * g.N * D;
     Vp = A.vperm + (size_t)bh * g.N * D;
   } else {
@@ -226,22 +230,46 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   // routed ranges of the query group (positions in the group-major K/V),
   // staged in LDS when they fit; never read through generic pointers (flat
-  // accesses would make the compiler wait for the in-flight tile loads)
+  // accesses would make the compiler wait for the in-flight tile loads).
+  // Only the ranges meeting the key segment [seg_lo, seg_hi) are walked, each
+  // clipped to it: ranges are sorted and disjoint, so they are the run
+  // [j0, j0 + nseg) and their clipped lengths sum to this launch's keys.
   typedef const __attribute__((address_space(1))) int* gptr_int;
   gptr_int grng = nullptr;
-  int nr = 0;
+  int nr = 0, j0 = 0, nseg = 0;
+  __shared__ int sred[2][3];
   if (MODE == MODE_SPARSE) {
     grng = (gptr_int)(A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt);
     nr = A.rng_cnt[(size_t)bh * g.CQt + w.a];
     for (int i = tid; i < min(nr, MAXR); i += 128) srng[i] = make_int2(grng[2 * i], grng[2 * i + 1]);
     __syncthreads();
+    int below = 0, before_end = 0, keys = 0;
+    for (int i = tid; i < nr; i += 128) {
+      const int2 r = (i < MAXR) ? srng[i] : make_int2(grng[2 * i], grng[2 * i + 1]);
+      below += (r.x + r.y <= A.seg_lo);
+      before_end += (r.x < A.seg_hi);
+      keys += max(min(r.x + r.y, A.seg_hi) - max(r.x, A.seg_lo), 0);
+    }
+    below = wave_sum_i(below);
+    before_end = wave_sum_i(before_end);
+    keys = wave_sum_i(keys);
+    if (lane == 0) {
+      sred[wv][0] = below;
+      sred[wv][1] = before_end;
+      sred[wv][2] = keys;
+    }
+    __syncthreads();
+    j0 = sred[0][0] + sred[1][0];
+    nseg = sred[0][1] + sred[1][1] - j0;
+    w.nkeys = sred[0][2] + sred[1][2];
   }
-  const bool rng_in_lds = nr <= MAXR;
-  auto range_at = [&](int j) -> int2 {
-    if (rng_in_lds) return srng[j];
-    return make_int2(grng[2 * j], grng[2 * j + 1]);
+  auto range_at = [&](int j) -> int2 {  // clipped range j of the segment's run
+    const int jj = j0 + j;
+    const int2 r = (jj < MAXR) ? srng[jj] : make_int2(grng[2 * jj], grng[2 * jj + 1]);
+    const int lo = max(r.x, A.seg_lo), hi = min(r.x + r.y, A.seg_hi);
+    return make_int2(lo, hi - lo);
   };
-  const int safe_pos = (MODE == MODE_SPARSE) ? range_at(0).x : w.k0;
+  const int safe_pos = (MODE == MODE_SPARSE) ? (nseg > 0 ? range_at(0).x : 0) : w.k0;
   KeyCursor cur{0, 0};
   auto fill_pos = [&](int tt) {  // key positions of tile tt -> ring slot tt % 3
     if (tid < KT) {
@@ -250,7 +278,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if (f < w.nkeys) {
         if (MODE == MODE_SPARSE) {
           int2 r = range_at(cur.j);
-          while (f >= cur.cum + r.y && cur.j + 1 < nr) {
+          while (f >= cur.cum + r.y && cur.j + 1 < nseg) {
             cur.cum += r.y;
             ++cur.j;
             r = range_at(cur.j);
@@ -283,8 +311,30 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) O[db][i] = 0.f;
+  if (MODE == MODE_SPARSE && !A.seg_first && qvalid) {
+    // resume the running state left by the previous key segment
+    const float* src = A.osp + ((size_t)bh * g.N + qrow) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const float4 v4 = *(const float4*)(src + db * 32 + i4 * 8 + h * 4);
+        O[db][i4 * 4] = v4.x;
+        O[db][i4 * 4 + 1] = v4.y;
+        O[db][i4 * 4 + 2] = v4.z;
+        O[db][i4 * 4 + 3] = v4.w;
+      }
+    const float* ml = A.mlst + ((size_t)bh * g.N + qrow) * 4;
+    m_run = ml[0];
+    l_run = ml[1 + h];
+  }
   // s_waitcnt immediate (gfx9 encoding) waiting for lgkmcnt(0) only
   constexpr int kWaitLgkm0 = 0xC07F;
+  // The Q operands and any resumed state were loaded into registers with
+  // ordinary global loads.  Wait for them here, once: otherwise the
+  // compiler's wait before their first use inside the loop would be a
+  // vmcnt(0) on every iteration, which also waits for the next tile's loads.
+  __builtin_amdgcn_s_waitcnt(0x3f70);
 
   const int ntile = (w.nkeys + KT - 1) / KT;
   // One step: compute tile t from (kt, vt) while tile t + 1 loads into (kn, vn).
@@ -292,8 +342,11 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // Plain s_barrier (no fence): a fence would also wait for the tile t+1
     // loads just issued.  Ordering is explicit instead: each wave waits for
     // its own loads of tile t and for its LDS writes before the barrier.
-    if (t + 1 < ntile) issue_loads(t + 1, kn, vn);
+    // Positions first: the range walk may read global memory, and the wait
+    // the compiler puts before its use also covers every load issued
+    // earlier; here those are only tile t's, which are awaited next anyway.
     if (t + 2 < ntile) fill_pos(t + 2);
+    if (t + 1 < ntile) issue_loads(t + 1, kn, vn);
     if (t + 1 < ntile)
       __builtin_amdgcn_s_waitcnt(0x3f70 | (2 * LPT));  // vmcnt(2*LPT): tile t has landed
     else
@@ -365,10 +418,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_barrier();
   };
-  fill_pos(0);
+  if (ntile > 0) fill_pos(0);
   if (ntile > 1) fill_pos(1);
   __syncthreads();
-  issue_loads(0, Kb0, Vb0);
+  if (ntile > 0) issue_loads(0, Kb0, Vb0);
   for (int t = 0; t < ntile; t += 2) {
     step(t, Kb0, Vb0, Kb1, Vb1);
     if (t + 1 < ntile) step(t + 1, Kb1, Vb1, Kb0, Vb0);
@@ -391,7 +444,21 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   } else {
     const float inv = 1.f / l_tot;
-    if (MODE == MODE_SPARSE) {
+    if (MODE == MODE_SPARSE && !A.seg_last) {
+      // hand the running state to the next key segment
+      float* dst = A.osp + ((size_t)bh * g.N + qrow) * D;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int dv = db * 32 + i4 * 8 + h * 4;
+          *(float4*)(dst + dv) =
+              make_float4(O[db][i4 * 4], O[db][i4 * 4 + 1], O[db][i4 * 4 + 2], O[db][i4 * 4 + 3]);
+        }
+      float* ml = A.mlst + ((size_t)bh * g.N + qrow) * 4;
+      if (h == 0) ml[0] = m_run;
+      ml[1 + h] = l_run;
+    } else if (MODE == MODE_SPARSE) {
       float* dst = A.osp + ((size_t)bh * g.N + qrow) * D;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
@@ -937,7 +1004,12 @@ static AttnArgs make_args(const Work* w, const void* q, const void* k, const voi
     a.nprobes = w->nprobes;
     a.kperm = w->kperm;
     a.vperm = w->vperm;
+    a.mlst = w->mlst;
   }
+  a.seg_lo = 0;
+  a.seg_hi = 0x7fffffff;
+  a.seg_first = 1;
+  a.seg_last = 1;
   return a;
 }
 
@@ -952,9 +1024,18 @@ static void attend_d(const Geom& g, const Work& w, const void* q, const void* k,
         g, k, v, w.permk, w.kperm, w.vperm);
   }
   if (ev) (void)hipEventRecord(ev[0], s);
-  if (g.bf16)
-    k_attn_mfma<D, MODE_SPARSE><<<dim3(8 * g.nchunk_per_xcd, g.BH), 128, 0, s>>>(g, a);
-  else
+  if (g.bf16) {
+    // one launch per key segment, so that all blocks in flight read the same
+    // slice of K/V and it stays in L2
+    for (int sg = 0; sg < g.nseg; ++sg) {
+      AttnArgs as = a;
+      as.seg_lo = (int)((int64_t)g.N * sg / g.nseg);
+      as.seg_hi = (int)((int64_t)g.N * (sg + 1) / g.nseg);
+      as.seg_first = sg == 0;
+      as.seg_last = sg == g.nseg - 1;
+      k_attn_mfma<D, MODE_SPARSE><<<dim3(8 * g.nchunk_per_xcd, g.BH), 128, 0, s>>>(g, as);
+    }
+  } else
     k_attn_f32<D, MODE_SPARSE><<<dim3(g.nchunk_max, g.BH), 64, 0, s>>>(g, a);
   if (ev) (void)hipEventRecord(ev[1], s);
   if (g.M > 0) {

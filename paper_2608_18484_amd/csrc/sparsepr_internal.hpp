@@ -41,6 +41,7 @@ struct Geom {
   int nchunk_max;         // attention work items per head (upper bound)
   int nchunk_per_xcd;     // ceil(nchunk_max / 8): chunks of one head per XCD
   int nsplit;             // probe attention key splits
+  int nseg;               // key segments of the sparse attention (one launch each)
   int nsort_blk;          // counting-sort blocks over NV rows
   int nsort_blk_full;     // counting-sort blocks over N rows
   int cmax;               // max(CKt, CQt)
@@ -98,6 +99,7 @@ struct Work {
   float* osp;         // [BH][N][dv]
   float* odp;         // [BH][M][dv]
   float* part;        // [BH][M][nsplit][dv+2] split partials (o, m, l)
+  float* mlst;        // [BH][N][4] running (m, l_lo, l_hi) of the sparse attention between key segments
   float* fitv;        // [BH][3*dv] mu_x, s_x, mu_r
   float* fity;        // [BH][dv][r] B Psi
   float* fitpsi;      // [BH][dv][r]

@@ -230,3 +230,21 @@ def test_independent_plan_agreement(orc):
     agree_k = np.mean(ex["labels_kv"] == pl["labels_kv"])
     print(f"label agreement kv={agree_k:.4f}")
     assert agree_k > 0.5
+
+
+@pytest.mark.parametrize("ntext", [0, 96])
+def test_key_segments_match_single_pass(orc, monkeypatch, ntext):
+    # The sparse attention runs once per slice of the group-major keys and
+    # carries (O, m, l) between launches in fp32.  Splitting into many slices
+    # only regroups the keys into tiles (fp32 rounding order), so the output
+    # must agree with the single pass to bf16 rounding, and with the oracle.
+    wl = medium(heads=2).with_(n_text=ntext)
+    monkeypatch.delenv("SPARSEPR_SEG_KB", raising=False)
+    r1 = _run(wl)
+    monkeypatch.setenv("SPARSEPR_SEG_KB", "64")
+    r2 = _run(wl)
+    assert rel_l2(r2["out"], r1["out"]) < 2e-3
+    ex = r2["op"].export(0, fields=["labels_q", "labels_kv", "routes", "probes", "probe_weights"])
+    ref, _ = _replay(orc, r2, ex, 0, 0)
+    err = rel_l2(r2["out"][0, 0], ref)
+    assert err < 2e-2, err
