@@ -167,7 +167,9 @@ sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const spars
  * 0 <= n_dense_prefix < n_q; 1 <= C_k, C_q <= n_v; 1 <= r_k, r_q;
  * 1 <= M_s; 0 <= M; 1 <= r <= d_v; 0 < rho <= 1; ridge >= 0; eps >= 0;
  * stride_n >= d.  UNSUPPORTED: d != d_v, d not in {64, 128}, C_k or C_q
- * above 8191, n_q above 2^24. */
+ * above 8191, n_q above 2^24, strides not multiples of 8 elements,
+ * n_kv * stride_n * element size of 4 GiB or more (one head's K/V rows are
+ * addressed with 32-bit byte offsets). */
 sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr_params* params,
                                      void* workspace, size_t bytes, sparsepr_plan_t* out);
 

@@ -146,6 +146,9 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "strides must be non-negative and stride_n >= d");
   if (s->stride_n % 8 != 0 || s->stride_h % 8 != 0 || s->stride_b % 8 != 0)
     return fail(SPARSEPR_ERR_UNSUPPORTED, "strides must be multiples of 8 elements");
+  // the attention kernels address one head's K/V rows with 32-bit byte offsets
+  if ((int64_t)s->n_kv * s->stride_n * (s->dtype == SPARSEPR_BF16 ? 2 : 4) >= (int64_t(1) << 32))
+    return fail(SPARSEPR_ERR_UNSUPPORTED, "n_kv * stride_n must stay below 4 GiB per head");
   const int N = s->n_q;
   if (p->n_dense_prefix < 0 || p->n_dense_prefix >= N)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "n_dense_prefix must be in [0, n_q)");

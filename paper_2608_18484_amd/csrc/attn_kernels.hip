@@ -151,6 +151,22 @@ __device__ __forceinline__ void g2lds16(const void* src, const void* lds_base) {
                : "memory");
 }
 
+// The same copy addressed as a uniform 64-bit base (SGPRs) plus a 32-bit
+// per-lane byte offset; `m0v` is the wave-uniform LDS destination.
+__device__ __forceinline__ void g2lds16s(const void* sbase, uint32_t voff, uint32_t m0v) {
+  // readfirstlane returns a signed int: widen through uint32_t so the low
+  // half of the address is zero-extended, never sign-extended
+  const uint64_t b = (uint64_t)(size_t)sbase;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
+  const uint32_t m0u = (uint32_t)__builtin_amdgcn_readfirstlane(m0v);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:0"
+               :
+               : "v"(voff), "s"(sb), "s"(m0u)
+               : "memory");
+}
+
 // Block-sparse flash attention, bf16 MFMA, fp32 accumulation.
 //  * 128 threads = 2 waves; a block owns up to 64 query rows (32 per wave)
 //    that share one key list: the routed ranges of their query group in the
@@ -171,10 +187,8 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   constexpr int NDB = D / 32;                  // 32-wide blocks of O^T
   constexpr int LPT = KT * CH / 128;           // 16-byte loads per thread per tensor per tile
   constexpr int MAXR = 512;                    // routed ranges staged in LDS
-  __shared__ __attribute__((aligned(1024))) uint16_t Kb0[KT * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t Kb1[KT * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t Vb0[KT * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t Vb1[KT * D];
+  // K and V tiles, double-buffered: tiles[0..1] = K, tiles[2..3] = V
+  __shared__ __attribute__((aligned(1024))) uint16_t tiles[4][KT * D];
   __shared__ int spos[3][KT];
   __shared__ int2 srng[MODE == MODE_SPARSE ? MAXR : 1];
 
@@ -291,16 +305,27 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       spos[tt % 3][tid] = pos;
     }
   };
-  auto issue_loads = [&](int tt, uint16_t* kb, uint16_t* vb) {  // tile tt -> (kb, vb)
+  // LDS byte address of tiles[0] (uniform); K buffer b is at +b*KT*D*2,
+  // V buffer b at +(2+b)*KT*D*2
+  const uint32_t lds_tiles = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)&tiles[0][0]);
+  const uint32_t row_bytes = (uint32_t)(ksn * 2);
+  auto issue_loads = [&](int tt, int buf) {  // tile tt -> K/V buffer `buf`
+    // all positions first (one LDS wait), then the copies
+    uint32_t voff[LPT];
 #pragma unroll
     for (int u = 0; u < LPT; ++u) {
       const int inst = wv * LPT + u;
       const int s = inst * 64 + lane;
       const int key = s / CH, p = s % CH;
       const int c8 = p ^ kv_swz(key);
-      const int64_t off = (int64_t)spos[tt % 3][key] * ksn + c8 * 8;
-      g2lds16(Kp + off, kb + inst * 512);
-      g2lds16(Vp + off, vb + inst * 512);
+      voff[u] = (uint32_t)spos[tt % 3][key] * row_bytes + (uint32_t)(c8 * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < LPT; ++u) {
+      const uint32_t dst = lds_tiles + (uint32_t)((wv * LPT + u) * 1024);
+      g2lds16s(Kp, voff[u], dst + (uint32_t)(buf * KT * D * 2));
+      g2lds16s(Vp, voff[u], dst + (uint32_t)((2 + buf) * KT * D * 2));
     }
   };
 
@@ -338,7 +363,9 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   const int ntile = (w.nkeys + KT - 1) / KT;
   // One step: compute tile t from (kt, vt) while tile t + 1 loads into (kn, vn).
-  auto step = [&](int t, const uint16_t* kt, const uint16_t* vt, uint16_t* kn, uint16_t* vn) {
+  auto step = [&](int t, int cb) {  // compute tile t from buffer cb; tile t+1 loads into 1-cb
+    const uint16_t* kt = tiles[cb];
+    const uint16_t* vt = tiles[2 + cb];
     // Plain s_barrier (no fence): a fence would also wait for the tile t+1
     // loads just issued.  Ordering is explicit instead: each wave waits for
     // its own loads of tile t and for its LDS writes before the barrier.
@@ -346,7 +373,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // the compiler puts before its use also covers every load issued
     // earlier; here those are only tile t's, which are awaited next anyway.
     if (t + 2 < ntile) fill_pos(t + 2);
-    if (t + 1 < ntile) issue_loads(t + 1, kn, vn);
+    if (t + 1 < ntile) issue_loads(t + 1, 1 - cb);
     if (t + 1 < ntile)
       __builtin_amdgcn_s_waitcnt(0x3f70 | (2 * LPT));  // vmcnt(2*LPT): tile t has landed
     else
@@ -421,10 +448,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   if (ntile > 0) fill_pos(0);
   if (ntile > 1) fill_pos(1);
   __syncthreads();
-  if (ntile > 0) issue_loads(0, Kb0, Vb0);
+  if (ntile > 0) issue_loads(0, 0);
   for (int t = 0; t < ntile; t += 2) {
-    step(t, Kb0, Vb0, Kb1, Vb1);
-    if (t + 1 < ntile) step(t + 1, Kb1, Vb1, Kb0, Vb0);
+    step(t, 0);
+    if (t + 1 < ntile) step(t + 1, 1);
   }
   if (!qvalid) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
