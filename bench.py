@@ -12,6 +12,7 @@ of the same workload on this host's cores.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +27,25 @@ sys.path.insert(0, ROOT)
 from paper_2608_18484_amd import workloads as W  # noqa: E402
 
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+ATTN_SRC = os.path.join(ROOT, "paper_2608_18484_amd", "csrc", "attn_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_attn_mfma_long_video_traffic.json")
+
+
+def attn_traffic(workload):
+    """HBM bytes of one call's sparse-attention launches, from the committed
+    FETCH_SIZE / WRITE_SIZE counter runs (scaled by the copy calibration), or
+    None when they were taken on another workload or on a different kernel
+    source than the one built now."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(ATTN_SRC, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != sha or rec.get("workload") != workload:
+        return None
+    return rec.get("hbm_bytes_per_call")
 
 
 def log(msg):
@@ -158,6 +178,7 @@ def main():
     tm = op.timings(reset=True, stream=stream)
     op.set_profiling(False)
     n_calls = max(tm["attend_calls"], 1)
+    nseg = tm["attn_launches"]
     attn_ms = tm["sparse_attn_ms"] / n_calls
     phases = {kk: round(tm[kk] / max(tm["plan_calls" if kk == "plan_ms" else "attend_calls"], 1), 4)
               for kk in ("plan_ms", "sparse_attn_ms", "probe_ms", "fit_ms", "correct_ms")}
@@ -198,7 +219,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "k_attn_mfma<128, MODE_SPARSE>",
                      "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-                     "kernel_ms": round(attn_ms, 4), "traffic": None},
+                     "kernel_ms": round(attn_ms, 4), "traffic": attn_traffic(wl.name),
+                     "unit_of_work": f"one call's sparse-attention launches ({nseg} key segments)"},
     }
 
     if not args.no_dense:

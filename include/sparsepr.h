@@ -214,12 +214,15 @@ sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const spa
  * Accumulated over the calls made while profiling was enabled. */
 typedef struct {
   double plan_ms;         /* partitioning, routing and probe choice */
-  double sparse_attn_ms;  /* the block-sparse attention kernel alone */
+  double sparse_attn_ms;  /* the block-sparse attention launches alone (one per key
+                             segment: a slice of the group-major keys sized to
+                             stay resident in L2) */
   double probe_ms;        /* exact probe rows and their merge */
   double fit_ms;          /* residual fit */
   double correct_ms;      /* correction, restore and probe rows */
   int32_t plan_calls;
   int32_t attend_calls;
+  int32_t attn_launches;  /* sparse-attention launches per attend call */
 } sparsepr_timings;
 
 /* Enable (1) or disable (0) event timing on this handle.  Creating the events

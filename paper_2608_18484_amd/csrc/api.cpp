@@ -618,6 +618,7 @@ sparsepr_status sparsepr_get_timings(sparsepr_plan_t plan, sparsepr_timings* out
   if (st != SPARSEPR_OK) return st;
   harvest(plan);
   *out = plan->acc;
+  out->attn_launches = plan->g.bf16 ? plan->g.nseg : 1;
   if (reset) plan->acc = sparsepr_timings{};
   return ok();
 }

@@ -167,6 +167,19 @@ __device__ __forceinline__ void g2lds16s(const void* sbase, uint32_t voff, uint3
                : "memory");
 }
 
+// Combine a value with the one held by lane l ^ 32 (the other half of the
+// same query's keys) through v_permlane32_swap: swapping a register with
+// itself leaves, in each lane, its own value in one result and its partner's
+// in the other, so max3 / the sum of both results combine the pair.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Block-sparse flash attention, bf16 MFMA, fp32 accumulation.
 //  * 128 threads = 2 waves; a block owns up to 64 query rows (32 per wave)
 //    that share one key list: the routed ranges of their query group in the
@@ -401,7 +414,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) mt = fmaxf(mt, S[i]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32)) * sl2;
+      mt = pair_max(mt) * sl2;
       const bool need = mt > m_run + 8.f;
       if (__ballot(need)) {
         const float m_new = need ? mt : m_run;
@@ -413,17 +426,24 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
           for (int i = 0; i < 16; ++i) O[db][i] *= alpha;
       }
+      // probabilities rounded to bf16 for the PV product; the row sum is
+      // taken over the same rounded values (two per dot2), so O and l share
+      // one set of weights
       bf16x8 P[2];
-      float ls = 0.f;
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(S[c * 8 + e], sl2, -m_run));
-          ls += p;
-          P[c][e] = (__bf16)p;
+        for (int e = 0; e < 8; ++e)
+          P[c][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(S[c * 8 + e], sl2, -m_run));
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pp = {P[c][e], P[c][e + 1]};
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run, false);
         }
-      l_run += ls;
       // O^T += V^T P^T: two 16-key chunks, V^T fragments by transposing reads
       const int grp = lane >> 4, gl = lane & 15;
 #pragma unroll
@@ -454,7 +474,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (t + 1 < ntile) step(t + 1, 1);
   }
   if (!qvalid) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = pair_sum(l_run);
   if (MODE == MODE_PROBE) {
     float* dst = A.part + (((size_t)bh * g.M + w.tile * 64 + qr) * g.nsplit + w.split) * (D + 2);
 #pragma unroll

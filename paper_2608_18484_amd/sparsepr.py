@@ -52,7 +52,7 @@ class Timings(ctypes.Structure):
     _fields_ = [("plan_ms", ctypes.c_double), ("sparse_attn_ms", ctypes.c_double),
                 ("probe_ms", ctypes.c_double), ("fit_ms", ctypes.c_double),
                 ("correct_ms", ctypes.c_double), ("plan_calls", ctypes.c_int32),
-                ("attend_calls", ctypes.c_int32)]
+                ("attend_calls", ctypes.c_int32), ("attn_launches", ctypes.c_int32)]
 
 
 _P = ctypes.c_void_p
