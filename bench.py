@@ -215,6 +215,7 @@ def main():
         "rho_route": round(st["rho_route"], 6),
         "exec_pairs": st["exec_pairs"],
         "kmeans_assignments": [st["kmeans_iters_kv"], st["kmeans_iters_q"]],
+        "kmeans_exact_rescans": st["kmeans_rescans"],
         "phase_ms": phases,
         "roofline": {"bound": "mfma", "kernel": "k_attn_mfma<128, MODE_SPARSE>",
                      "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,

@@ -101,6 +101,9 @@ typedef struct {
   int32_t kmeans_iters_kv;   /* max over heads of assignments performed */
   int32_t kmeans_iters_q;
   int32_t status_flags;      /* OR over heads of SPARSEPR_FLAG_* */
+  int64_t kmeans_rescans;    /* points whose assignment needed the exact scan over
+                                every centroid, summed over heads, both k-means and
+                                all assignments (a cost diagnostic) */
 } sparsepr_stats;
 
 #define SPARSEPR_FLAG_NONFINITE_INPUT 1 /* a NaN/Inf reached the partition features */

@@ -429,6 +429,7 @@ sparsepr_status sparsepr_get_stats(sparsepr_plan_t plan, sparsepr_stats* out, vo
     out->kmeans_iters_kv = std::max(out->kmeans_iters_kv, (int32_t)h[ST_ITK]);
     out->kmeans_iters_q = std::max(out->kmeans_iters_q, (int32_t)h[ST_ITQ]);
     out->status_flags |= (int32_t)h[ST_FLAGS];
+    out->kmeans_rescans += h[ST_RESCAN];
     rr += (double)h[ST_ROUTED_PAIRS] / nn;
     re += (double)h[ST_ROUTED_PAIRS] / nn + (double)h[ST_NPROBES] / (double)g.N;
   }

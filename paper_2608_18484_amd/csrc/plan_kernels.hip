@@ -360,45 +360,53 @@ __global__ __launch_bounds__(64) void k_km_prep_cent(KmArgs a, int it) {
   a.cu[(size_t)bh * a.CP + b] = u;
 }
 
-// Screening: a block of 4 waves takes 128 points (32 per wave, the N side of
-// v_mfma_f32_32x32x16_bf16) against 32-centroid tiles staged in LDS (the M
-// side).  Lane (n, h) ends with the best and second-best estimate of point n
-// over half of the centroids; the halves are merged with one exchange.
+// Screening: a block of 4 waves takes 256 points, 64 per wave as two sets
+// of 32 (the N side of v_mfma_f32_32x32x16_bf16), against 32-centroid tiles
+// staged in LDS (the M side); every centroid fragment read from LDS feeds
+// both sets.  Lane (n, h) ends with the three best estimates of point n of
+// each set over half of the centroids; the halves are merged with one
+// exchange, and lane h then decides set h's point.
 template <int RP>
 __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int KS = RP / 16;
   constexpr int LD = RP + 8;  // padded LDS row (bf16)
+  constexpr int NPS = 2;      // sets of 32 points per wave
   __shared__ __attribute__((aligned(16))) uint16_t shi[32 * LD];
   __shared__ __attribute__((aligned(16))) uint16_t slo[32 * LD];
-  __shared__ float su[32];
+  __shared__ __attribute__((aligned(16))) float su[32];
+  __shared__ float sred[4];
   const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip_assign(a, bh, it)) return;
   const int n = lane & 31, h = lane >> 5;
-  const int j = blockIdx.x * 128 + wv * 32 + n;
-  const int jc = min(j, a.n - 1);
-  bf16x8 bhi[KS], blo[KS];
-  const uint16_t* xh = a.xhi + ((size_t)bh * a.n + jc) * RP;
-  const uint16_t* xl = a.xlo + ((size_t)bh * a.n + jc) * RP;
+  const int jbase = blockIdx.x * (128 * NPS) + wv * (32 * NPS);
+  bf16x8 bhi[NPS][KS], blo[NPS][KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    bhi[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xh + ks * 16 + h * 8));
-    blo[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
+  for (int ps = 0; ps < NPS; ++ps) {
+    const int jc = min(jbase + ps * 32 + n, a.n - 1);
+    const uint16_t* xh = a.xhi + ((size_t)bh * a.n + jc) * RP;
+    const uint16_t* xl = a.xlo + ((size_t)bh * a.n + jc) * RP;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      bhi[ps][ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xh + ks * 16 + h * 8));
+      blo[ps][ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
+    }
   }
   // Largest centroid squared norm of the head (for the error bound).
-  __shared__ float sred[4];
   float umax = 0.f;
   const float* cu = a.cu + (size_t)bh * a.CP;
   for (int b = tid; b < a.C; b += 256) umax = fmaxf(umax, cu[b]);
   umax = wave_max(umax);
   if (lane == 0) sred[wv] = umax;
-  // Three smallest estimates of this lane, ascending, each with its centroid
+  // Three smallest estimates per point, ascending, each with its centroid
   // index in the low IB mantissa bits (C <= 2^IB).  Replacing those bits
   // moves a value by at most 2^(IB-23) of its magnitude, which the decision
   // below adds to the error bound.  Keeping (value, index) in one float lets
   // min / med3 maintain the sorted triple in three instructions per score.
   const int ib = 32 - __clz(a.CP - 1);
   const uint32_t imask = (1u << ib) - 1u;
-  float t1 = INFINITY, t2 = INFINITY, t3 = INFINITY;
+  float t1[NPS], t2[NPS], t3[NPS];
+#pragma unroll
+  for (int ps = 0; ps < NPS; ++ps) t1[ps] = t2[ps] = t3[ps] = INFINITY;
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
   for (int c0 = 0; c0 < a.CP; c0 += 32) {
@@ -412,16 +420,21 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
     // (an index packed into +inf would make a NaN) and never win
     if (tid < 32) su[tid] = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
     __syncthreads();
-    f32x16 S;
+    f32x16 S[NPS];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) S[i] = 0.f;
+    for (int ps = 0; ps < NPS; ++ps)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) S[ps][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const uint4*)(shi + n * LD + ks * 16 + h * 8));
       const bf16x8 al = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
-      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bhi[ks], S, 0, 0, 0);
-      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, blo[ks], S, 0, 0, 0);
-      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bhi[ks], S, 0, 0, 0);
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps) {
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bhi[ps][ks], S[ps], 0, 0, 0);
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, blo[ps][ks], S[ps], 0, 0, 0);
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bhi[ps][ks], S[ps], 0, 0, 0);
+      }
     }
     // register i holds centroid c0 + (i/4)*8 + h*4 + i%4
 #pragma unroll
@@ -430,42 +443,48 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       const float uu[4] = {u4.x, u4.y, u4.z, u4.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float sh = fmaf(-2.f, S[i4 * 4 + e], uu[e]);
         const uint32_t idx = (uint32_t)(c0 + i4 * 8 + h * 4 + e);
-        const float pk = __uint_as_float((__float_as_uint(sh) & ~imask) | idx);
-        const float n3 = __builtin_amdgcn_fmed3f(t2, t3, pk);
-        const float n2 = __builtin_amdgcn_fmed3f(t1, t2, pk);
-        t1 = fminf(t1, pk);
-        t2 = n2;
-        t3 = n3;
+#pragma unroll
+        for (int ps = 0; ps < NPS; ++ps) {
+          const float sh = fmaf(-2.f, S[ps][i4 * 4 + e], uu[e]);
+          const float pk = __uint_as_float((__float_as_uint(sh) & ~imask) | idx);
+          const float n3 = __builtin_amdgcn_fmed3f(t2[ps], t3[ps], pk);
+          const float n2 = __builtin_amdgcn_fmed3f(t1[ps], t2[ps], pk);
+          t1[ps] = fminf(t1[ps], pk);
+          t2[ps] = n2;
+          t3[ps] = n3;
+        }
       }
     }
   }
-  // merge with the other half of the centroids (lane l ^ 32, same point)
-  {
-    const float o1 = __shfl_xor(t1, 32), o2 = __shfl_xor(t2, 32), o3 = __shfl_xor(t3, 32);
-    const float ov[3] = {o1, o2, o3};
+  // merge with the other half of the centroids (lane l ^ 32, same points)
+#pragma unroll
+  for (int ps = 0; ps < NPS; ++ps) {
+    const float ov[3] = {__shfl_xor(t1[ps], 32), __shfl_xor(t2[ps], 32), __shfl_xor(t3[ps], 32)};
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
-      const float n3 = __builtin_amdgcn_fmed3f(t2, t3, ov[e]);
-      const float n2 = __builtin_amdgcn_fmed3f(t1, t2, ov[e]);
-      t1 = fminf(t1, ov[e]);
-      t2 = n2;
-      t3 = n3;
+      const float n3 = __builtin_amdgcn_fmed3f(t2[ps], t3[ps], ov[e]);
+      const float n2 = __builtin_amdgcn_fmed3f(t1[ps], t2[ps], ov[e]);
+      t1[ps] = fminf(t1[ps], ov[e]);
+      t2[ps] = n2;
+      t3[ps] = n3;
     }
   }
   __syncthreads();
   umax = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
-  if (h != 0 || j >= a.n) return;
-  const int i1 = (int)(__float_as_uint(t1) & imask), i2 = (int)(__float_as_uint(t2) & imask);
+  // lane (n, h) decides point n of set h
+  const int j = jbase + h * 32 + n;
+  if (j >= a.n) return;
+  const float T1 = h ? t1[1] : t1[0], T2 = h ? t2[1] : t2[0], T3 = h ? t3[1] : t3[0];
+  const int i1 = (int)(__float_as_uint(T1) & imask), i2 = (int)(__float_as_uint(T2) & imask);
   const float xn = a.xn[(size_t)bh * a.n + j];
   const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
   const float ek = ldexpf(1.f, ib - 22);
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   int label;
-  if (t2 - t1 > 2.f * delta + ek * (fabsf(t1) + fabsf(t2))) {
+  if (T2 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T2))) {
     label = i1;  // unique candidate: the exact argmin
-  } else if (t3 - t1 > 2.f * delta + ek * (fabsf(t1) + fabsf(t3))) {
+  } else if (T3 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T3))) {
     // exactly two candidates: rescore both with the defining float score
     const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
     const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
@@ -490,60 +509,50 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
 }
 
 // Exact scan (the defining float score) for the points the screen could not
-// decide.  A block takes 64 such points at a time (one per four threads, the
-// point in registers) and streams the centroids through LDS in 64-row
-// chunks; each thread scores every fourth centroid of a chunk with the float
-// chain, and the four partial minima of a point (lowest index among equal
-// scores) are merged with two exchanges.
+// decide; there are few of them, so each gets a block: the point sits in
+// LDS, every thread scores a strided subset of the centroids with the float
+// chain, and the block keeps the smallest score, lowest index among equal
+// scores.
 template <int RP>
 __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
-  constexpr int PB = 64, CB = 64;
-  __shared__ __attribute__((aligned(16))) float cs[CB][RP + 4];
-  __shared__ float us[CB];
-  const int bh = blockIdx.y, tid = threadIdx.x;
+  __shared__ __attribute__((aligned(16))) float xs[RP];
+  __shared__ float rs[4];
+  __shared__ int ri[4];
+  const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip_assign(a, bh, it)) return;
   const int cnt = a.fbcnt[(size_t)bh * 2 * a.T + a.sel * a.T + it];
   const float* cu = a.cu + (size_t)bh * a.CP;
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   const int R = a.R;
-  const int pi = tid >> 2, part = tid & 3;
-  for (int e0 = blockIdx.x * PB; e0 < cnt; e0 += gridDim.x * PB) {
-    const int e = e0 + pi;
-    const bool valid = e < cnt;
-    const int j = valid ? a.fb[(size_t)bh * a.n + e] : 0;
-    float x[RP];
-    const float* xp = a.pts + ((size_t)bh * a.n + j) * R;
-#pragma unroll
-    for (int k = 0; k < RP; ++k) x[k] = (valid && k < R) ? xp[k] : 0.f;
+  for (int e = blockIdx.x; e < cnt; e += gridDim.x) {
+    const int j = a.fb[(size_t)bh * a.n + e];
+    __syncthreads();
+    if (tid < RP) xs[tid] = tid < R ? a.pts[((size_t)bh * a.n + j) * R + tid] : 0.f;
+    __syncthreads();
     float best = INFINITY;
     int bi = 0x7fffffff;
-    for (int b0 = 0; b0 < a.C; b0 += CB) {
-      __syncthreads();
-      for (int i = tid; i < CB * RP; i += 256) {
-        const int b = b0 + i / RP, k = i % RP;
-        cs[i / RP][k] = (b < a.C && k < R) ? a.cent[((size_t)bh * a.C + b) * R + k] : 0.f;
+    for (int b = tid; b < a.C; b += 256) {  // ascending within the thread
+      const float* cb = a.cent + ((size_t)bh * a.C + b) * R;
+      float t = 0.f;
+      if ((R & 3) == 0) {
+        for (int k = 0; k < R; k += 4) {
+          const float4 c4 = *(const float4*)(cb + k);
+          t = fmaf(xs[k], c4.x, t);
+          t = fmaf(xs[k + 1], c4.y, t);
+          t = fmaf(xs[k + 2], c4.z, t);
+          t = fmaf(xs[k + 3], c4.w, t);
+        }
+      } else {
+        for (int k = 0; k < R; ++k) t = fmaf(xs[k], cb[k], t);
       }
-      if (tid < CB) us[tid] = (b0 + tid < a.C) ? cu[b0 + tid] : INFINITY;
-      __syncthreads();
-      for (int bb = part; bb < CB && b0 + bb < a.C; bb += 4) {
-        float t = 0.f;
-#pragma unroll
-        for (int k4 = 0; k4 < RP / 4; ++k4) {
-          const float4 c4 = *(const float4*)&cs[bb][4 * k4];
-          t = fmaf(x[4 * k4], c4.x, t);
-          t = fmaf(x[4 * k4 + 1], c4.y, t);
-          t = fmaf(x[4 * k4 + 2], c4.z, t);
-          t = fmaf(x[4 * k4 + 3], c4.w, t);
-        }
-        const float sc = fmaf(-2.f, t, us[bb]);
-        if (sc < best) {  // centroids ascending within the thread: ties keep the lower index
-          best = sc;
-          bi = b0 + bb;
-        }
+      const float sc = fmaf(-2.f, t, cu[b]);
+      if (sc < best) {
+        best = sc;
+        bi = b;
       }
     }
 #pragma unroll
-    for (int o = 1; o < 4; o <<= 1) {
+    for (int o = 32; o > 0; o >>= 1) {
       const float ob = __shfl_xor(best, o);
       const int oi = __shfl_xor(bi, o);
       if (ob < best || (ob == best && oi < bi)) {
@@ -551,7 +560,17 @@ __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
         bi = oi;
       }
     }
-    if (valid && part == 0) {
+    if (lane == 0) {
+      rs[wv] = best;
+      ri[wv] = bi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      for (int w2 = 1; w2 < 4; ++w2)
+        if (rs[w2] < best || (rs[w2] == best && ri[w2] < bi)) {
+          best = rs[w2];
+          bi = ri[w2];
+        }
       const int old = lab[j];
       lab[j] = bi;
       if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
@@ -1292,6 +1311,9 @@ __global__ __launch_bounds__(256) void k_plan_stats(Geom g, Work w, int with_kme
         for (int it = 1; it < g.T && chg[it - 1] != 0; ++it) ++n;
         st[sel == 0 ? ST_ITK : ST_ITQ] = n;
       }
+      int64_t rescans = 0;
+      for (int e = 0; e < 2 * g.T; ++e) rescans += w.km_fbcnt[(size_t)bh * 2 * g.T + e];
+      st[ST_RESCAN] = rescans;
     }
   }
 }
@@ -1318,7 +1340,7 @@ template <int MAXR>
 static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   const int BH = g.BH;
   k_km_prep_cent<<<dim3(a.CP / 64 + 1, BH), 64, 0, s>>>(a, it);
-  const dim3 grid((a.n + 127) / 128, BH);
+  const dim3 grid((a.n + 255) / 256, BH);
   if (a.RP == 16)
     k_km_assign_mfma<16><<<grid, 256, 0, s>>>(a, it);
   else if (a.RP == 32)
@@ -1335,7 +1357,7 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  k_km_fallback<MAXR><<<dim3(32, BH), 256, 0, s>>>(a, it);
+  k_km_fallback<MAXR><<<dim3(64, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {

@@ -120,6 +120,7 @@ enum {
   ST_FLAGS = 7,
   ST_NE_Q = 8,
   ST_NE_K = 9,
+  ST_RESCAN = 10,
   ST_FIT_RANK = 10,
 };
 

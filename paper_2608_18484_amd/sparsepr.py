@@ -45,7 +45,7 @@ class Stats(ctypes.Structure):
                 ("forced_cells", ctypes.c_int32), ("nonempty_q_groups", ctypes.c_int32),
                 ("nonempty_kv_groups", ctypes.c_int32), ("n_probes", ctypes.c_int32),
                 ("kmeans_iters_kv", ctypes.c_int32), ("kmeans_iters_q", ctypes.c_int32),
-                ("status_flags", ctypes.c_int32)]
+                ("status_flags", ctypes.c_int32), ("kmeans_rescans", ctypes.c_int64)]
 
 
 class Timings(ctypes.Structure):
