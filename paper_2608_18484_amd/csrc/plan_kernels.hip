@@ -409,17 +409,40 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   for (int ps = 0; ps < NPS; ++ps) t1[ps] = t2[ps] = t3[ps] = INFINITY;
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
-  for (int c0 = 0; c0 < a.CP; c0 += 32) {
-    __syncthreads();
-    for (int i = tid; i < 32 * RP / 8; i += 256) {
-      const int r = i / (RP / 8), c8 = i % (RP / 8);
-      *(uint4*)(shi + r * LD + c8 * 8) = *(const uint4*)(chi + (size_t)(c0 + r) * RP + c8 * 8);
-      *(uint4*)(slo + r * LD + c8 * 8) = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
+  // Centroid tiles go through registers: the next tile's loads are issued
+  // before the current tile is scored, so their latency overlaps the MFMAs.
+  constexpr int TPT = (32 * RP / 8 + 255) / 256;  // 16-byte pieces per thread and array
+  uint4 nh[TPT], nl[TPT];
+  float nu = 0.f;
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int u = 0; u < TPT; ++u) {
+      const int i = tid + 256 * u;
+      if (i < 32 * RP / 8) {
+        const int r = i / (RP / 8), c8 = i % (RP / 8);
+        nh[u] = *(const uint4*)(chi + (size_t)(c0 + r) * RP + c8 * 8);
+        nl[u] = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
+      }
     }
     // padding centroids get a huge finite norm: their scores stay finite
     // (an index packed into +inf would make a NaN) and never win
-    if (tid < 32) su[tid] = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
+    if (tid < 32) nu = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
+  };
+  fetch(0);
+  for (int c0 = 0; c0 < a.CP; c0 += 32) {
     __syncthreads();
+#pragma unroll
+    for (int u = 0; u < TPT; ++u) {
+      const int i = tid + 256 * u;
+      if (i < 32 * RP / 8) {
+        const int r = i / (RP / 8), c8 = i % (RP / 8);
+        *(uint4*)(shi + r * LD + c8 * 8) = nh[u];
+        *(uint4*)(slo + r * LD + c8 * 8) = nl[u];
+      }
+    }
+    if (tid < 32) su[tid] = nu;
+    __syncthreads();
+    if (c0 + 32 < a.CP) fetch(c0 + 32);
     f32x16 S[NPS];
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
@@ -704,8 +727,9 @@ __global__ void k_prefix_group(KmArgs a) {
 __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const int32_t* perm,
                                                     const int32_t* off, int C, int offstride,
                                                     float* mean) {
-  // lane l owns channels 2l and 2l + 1; rows are loaded four at a time and
-  // added in ascending order
+  // One wave per group; lane l owns channels 2l and 2l + 1.  The members'
+  // rows are fetched 64 at a time (lane i holds member m0 + i), their values
+  // loaded eight at a time and added in ascending member order.
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + wv;
   if (b >= C) return;
@@ -713,34 +737,45 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
   const int32_t* o = off + (size_t)bh * offstride;
   const int32_t* p = perm + (size_t)bh * g.N;
   const int s0 = o[b], s1 = o[b + 1];
-  for (int c = 2 * lane; c < g.d; c += 128) {
-    double s0d = 0.0, s1d = 0.0;
-    auto ld2 = [&](int m) -> float2 {
-      const int64_t idx = base + (int64_t)p[m] * g.sn + c;
-      if (g.bf16) {
-        const uint32_t u = *(const uint32_t*)((const uint16_t*)x + idx);
-        return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
-      }
-      return *(const float2*)((const float*)x + idx);
-    };
-    int m = s0;
-    for (; m + 4 <= s1; m += 4) {
-      const float2 v0 = ld2(m), v1 = ld2(m + 1), v2 = ld2(m + 2), v3 = ld2(m + 3);
-      s0d += (double)v0.x; s1d += (double)v0.y;
-      s0d += (double)v1.x; s1d += (double)v1.y;
-      s0d += (double)v2.x; s1d += (double)v2.y;
-      s0d += (double)v3.x; s1d += (double)v3.y;
+  // d <= 128: every channel pair has a lane; all lanes run the member loop
+  // (the row indices are exchanged with readlane), idle lanes only skip the adds
+  const int c = 2 * lane;
+  const bool cin = c < g.d;
+  double s0d = 0.0, s1d = 0.0;
+  auto ld2 = [&](int row) -> float2 {
+    if (!cin) return make_float2(0.f, 0.f);
+    const int64_t idx = base + (int64_t)row * g.sn + c;
+    if (g.bf16) {
+      const uint32_t u = *(const uint32_t*)((const uint16_t*)x + idx);
+      return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
     }
-    for (; m < s1; ++m) {
-      const float2 v = ld2(m);
+    return *(const float2*)((const float*)x + idx);
+  };
+  for (int m0 = s0; m0 < s1; m0 += 64) {
+    const int cm = min(64, s1 - m0);
+    const int pv = lane < cm ? p[m0 + lane] : 0;
+    int i = 0;
+    for (; i + 8 <= cm; i += 8) {
+      float2 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = ld2(__builtin_amdgcn_readlane(pv, i + u));
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        s0d += (double)v[u].x;
+        s1d += (double)v[u].y;
+      }
+    }
+    for (; i < cm; ++i) {
+      const float2 v = ld2(__builtin_amdgcn_readlane(pv, i));
       s0d += (double)v.x;
       s1d += (double)v.y;
     }
-    const double n = (double)(s1 - s0);
-    float* dst = mean + ((size_t)bh * C + b) * g.d + c;
-    dst[0] = (s1 > s0) ? (float)(s0d / n) : 0.f;
-    dst[1] = (s1 > s0) ? (float)(s1d / n) : 0.f;
   }
+  if (!cin) return;
+  const double n = (double)(s1 - s0);
+  float* dst = mean + ((size_t)bh * C + b) * g.d + c;
+  dst[0] = (s1 > s0) ? (float)(s0d / n) : 0.f;
+  dst[1] = (s1 > s0) ? (float)(s1d / n) : 0.f;
 }
 
 // Query-response metric M_Q = Kt^T Kt / (C_k^+ d) from the nonempty key-space
