@@ -394,15 +394,35 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_barrier();
     if (wave_active) {
+      // All LDS operand reads of the tile are issued first, so that their
+      // latency overlaps: the K fragments feed the score MFMAs, the V^T
+      // fragments (transposing reads) arrive while the softmax runs.
+      bf16x8 kf[NKS];
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int c8 = (2 * ks + h) ^ kv_swz(n);
+        kf[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
+      }
+      const int grp = lane >> 4, gl = lane & 15;
+      bf16x8 vf[NDB][2];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int dv = db * 32 + 16 * (grp & 1) + 4 * (gl & 3);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int key0 = 16 * c + 4 * h + (gl >> 2);
+          const int key1 = key0 + 8;
+          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz(key0))) * 8 + (dv & 7));
+          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz(key1))) * 8 + (dv & 7));
+          vf[db][c] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 S;
 #pragma unroll
       for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const int c8 = (2 * ks + h) ^ kv_swz(n);
-        const bf16x8 av = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
-        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], S, 0, 0, 0);
-      }
+      for (int ks = 0; ks < NKS; ++ks) S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qreg[ks], S, 0, 0, 0);
       // register i holds key (i/4)*8 + h*4 + i%4 of the tile
       float mt = -INFINITY;
       if ((t + 1) * KT > w.nkeys) {
@@ -444,22 +464,12 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const bf16x2 pp = {P[c][e], P[c][e + 1]};
           l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run, false);
         }
-      // O^T += V^T P^T: two 16-key chunks, V^T fragments by transposing reads
-      const int grp = lane >> 4, gl = lane & 15;
+      // O^T += V^T P^T over the two 16-key chunks
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const int dv = db * 32 + 16 * (grp & 1) + 4 * (gl & 3);
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int key0 = 16 * c + 4 * h + (gl >> 2);
-          const int key1 = key0 + 8;
-          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz(key0))) * 8 + (dv & 7));
-          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz(key1))) * 8 + (dv & 7));
-          const bf16x8 av = __builtin_bit_cast(
-              bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-          O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, P[c], O[db], 0, 0, 0);
-        }
-      }
+        for (int c = 0; c < 2; ++c)
+          O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db][c], P[c], O[db], 0, 0, 0);
     }
     // every wave is done with this buffer before tile t + 2 is loaded into it
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
