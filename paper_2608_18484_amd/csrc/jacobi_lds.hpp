@@ -90,6 +90,40 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
       }
       __syncthreads();
     }
+    // Stop once the off-diagonal part is small relative to the whole matrix:
+    // convergence is quadratic, and in float the eigenvectors reach their
+    // rounding floor about when the relative off-diagonal norm drops below
+    // 1e-4 (the remaining sweeps would rotate noise).
+    {
+      __shared__ T red[2][NT / 64];
+      T off = 0, tot = 0;
+      for (int i = tid; i < D * D; i += NT) {
+        const int r = i / D, c = i % D;
+        const T x = A[r * LD + c];
+        tot += x * x;
+        if (r != c) off += x * x;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        off += __shfl_xor(off, o);
+        tot += __shfl_xor(tot, o);
+      }
+      if ((tid & 63) == 0) {
+        red[0][tid >> 6] = off;
+        red[1][tid >> 6] = tot;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        T o2 = 0, t2 = 0;
+        for (int w = 0; w < NT / 64; ++w) {
+          o2 += red[0][w];
+          t2 += red[1][w];
+        }
+        const T stop = sizeof(T) == 8 ? T(1e-12) : T(1e-4);
+        if (o2 <= stop * stop * t2) *flag = 0;
+      }
+    }
+    __syncthreads();
     const int more = *flag;
     __syncthreads();
     if (!more) break;

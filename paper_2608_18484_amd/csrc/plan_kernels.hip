@@ -142,7 +142,8 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 
 template <int D, int MAXR>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
-                                                 int rms, float eps, float* phi, int64_t* stats) {
+                                                 int rms, float eps, float* phi, int64_t* stats,
+                                                 uint16_t* xhi, uint16_t* xlo, float* xn, int RP) {
   constexpr int ROWS = 64, CPT = MAXR / 16;
   __shared__ float xs[ROWS][D + 1];
   __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
@@ -216,17 +217,36 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
       den = fmaxf(sqrtf(ss / (float)R), eps);
     }
     const int row = r0 + ty + 16 * u;
+    // the k-means operands of the same coordinates: bf16 hi + lo halves
+    // (zero-padded to RP) and the row norm (its error-bound input)
+    float ssq = 0.f;
+    float vv[CPT];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int col = tx * CPT + c;
+      vv[c] = col < R ? acc[u][c] / den : 0.f;
+      ssq = fmaf(vv[c], vv[c], ssq);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) ssq += __shfl_xor(ssq, o);
     if (row >= g.NV) continue;
     float* out = phi + ((size_t)bh * g.NV + row) * R;
+    uint16_t* oh = xhi + ((size_t)bh * g.NV + row) * RP;
+    uint16_t* ol = xlo + ((size_t)bh * g.NV + row) * RP;
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int col = tx * CPT + c;
       if (col < R) {
-        const float v = acc[u][c] / den;
-        bad |= !isfinite(v);
-        out[col] = v;
+        bad |= !isfinite(vv[c]);
+        out[col] = vv[c];
+      }
+      if (col < RP) {
+        const uint16_t hb = __builtin_bit_cast(uint16_t, (__bf16)vv[c]);
+        oh[col] = hb;
+        ol[col] = __builtin_bit_cast(uint16_t, (__bf16)(vv[c] - bf16_bits_to_f32(hb)));
       }
     }
+    if (tx == 0) xn[(size_t)bh * g.NV + row] = sqrtf(ssq) * 1.000001f;
   }
   if (bad)
     atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
@@ -303,37 +323,8 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
-// Points: bf16 hi/lo split (padded to RP with zeros) and norms; once per
-// k-means.  One thread per 8 coordinates of a point (16-byte stores).
-__global__ __launch_bounds__(256) void k_km_prep_points(KmArgs a) {
-  const int bh = blockIdx.y;
-  const int nch = a.RP / 8;
-  const int gid = blockIdx.x * 256 + threadIdx.x;
-  const int j = gid / nch, c8 = gid % nch;
-  if (j >= a.n) return;
-  const float* x = a.pts + ((size_t)bh * a.n + j) * a.R;
-  uint32_t hw[4], lw[4];
-  float ss = 0.f;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int k0 = c8 * 8 + 2 * e;
-    const float v0 = k0 < a.R ? x[k0] : 0.f;
-    const float v1 = k0 + 1 < a.R ? x[k0 + 1] : 0.f;
-    const uint16_t h0 = bf16_rne_bits(v0), h1 = bf16_rne_bits(v1);
-    const uint16_t l0 = bf16_rne_bits(v0 - bf16_bits_to_f32(h0));
-    const uint16_t l1 = bf16_rne_bits(v1 - bf16_bits_to_f32(h1));
-    hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    lw[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-    ss = fmaf(v0, v0, ss);
-    ss = fmaf(v1, v1, ss);
-  }
-  *(uint4*)(a.xhi + ((size_t)bh * a.n + j) * a.RP + c8 * 8) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-  *(uint4*)(a.xlo + ((size_t)bh * a.n + j) * a.RP + c8 * 8) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
-  if (c8 == 0) {
-    for (int k = 8; k < a.R; ++k) ss = fmaf(x[k], x[k], ss);
-    a.xn[(size_t)bh * a.n + j] = sqrtf(ss) * 1.000001f;
-  }
-}
+// Points: the bf16 hi/lo split (padded to RP with zeros) and the norms are
+// written by k_project together with the coordinates.
 
 // Centroids: hi/lo split and exact squared norms (+inf for the padding rows).
 __global__ __launch_bounds__(64) void k_km_prep_cent(KmArgs a, int it) {
@@ -1401,7 +1392,6 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
   a.RP = (a.R + 15) / 16 * 16;
   a.CP = (a.C + 31) / 32 * 32;
   k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
-  k_km_prep_points<<<dim3((a.n * (a.RP / 8) + 255) / 256, BH), 256, 0, s>>>(a);
   for (int it = 0; it < g.T; ++it) {
     if (a.R <= 32)
       assign_step<32>(g, a, it, s);
@@ -1416,15 +1406,19 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
 }
 
 template <int D>
-static void project(const Geom& g, const void* x, const float* F, int R, int rms, float eps,
-                    float* phi, int64_t* stats, hipStream_t s) {
+static void project(const Geom& g, const Work& w, const void* x, const float* F, int R, int rms,
+                    float eps, float* phi, hipStream_t s) {
   const dim3 grid((g.NV + 63) / 64, g.BH);
+  const int RP = (R + 15) / 16 * 16;
   if (R <= 32)
-    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
+    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
+                                          w.km_xn, RP);
   else if (R <= 64)
-    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
+    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
+                                          w.km_xn, RP);
   else
-    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, stats);
+    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
+                                           w.km_xn, RP);
 }
 
 template <int D>
@@ -1434,7 +1428,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1)
   k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
-  project<D>(g, k, w.fk, g.rk, 0, 0.f, w.phik, w.stats, s);
+  project<D>(g, w, k, w.fk, g.rk, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
@@ -1444,7 +1438,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
                                                          w.kbar);
   k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
-  project<D>(g, q, w.fq, g.rq, 1, g.eps_q, w.phiq, w.stats, s);
+  project<D>(g, w, q, w.fq, g.rq, 1, g.eps_q, w.phiq, s);
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
