@@ -197,22 +197,35 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     return (bf16_round(x).view(np.uint32) >> 16).astype(np.uint16)
 
 
-def make_inputs(wl: Workload, heads: Optional[list] = None):
+def make_inputs(wl: Workload, heads: Optional[list] = None, workers: int = 1):
     """Q, K, V as float32 [B, H, N, d] (already rounded to bf16 values when
     wl.dtype == 'bf16'), plus per-head generator metadata.  `heads` limits
-    generation to a list of (b, h) pairs; other heads are left at zero."""
+    generation to a list of (b, h) pairs; other heads are left at zero.
+    `workers` > 1 draws heads on a thread pool (each head has its own
+    generator, so the result does not depend on it)."""
     shape = (wl.batch, wl.heads, wl.n, wl.d)
     q = np.zeros(shape, np.float32)
     k = np.zeros(shape, np.float32)
     v = np.zeros(shape, np.float32)
     meta = {}
     todo = heads if heads is not None else [(b, h) for b in range(wl.batch) for h in range(wl.heads)]
-    for b, h in todo:
+
+    def one(bh):
+        b, h = bh
         qh, kh, vh, beta, length = make_head(wl, b, h)
         if wl.dtype == "bf16":
             qh, kh, vh = bf16_round(qh), bf16_round(kh), bf16_round(vh)
         q[b, h], k[b, h], v[b, h] = qh, kh, vh
-        meta[(b, h)] = {"beta": beta, "length": length}
+        return bh, {"beta": beta, "length": length}
+
+    if workers > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(workers) as ex:
+            for bh, m in ex.map(one, todo):
+                meta[bh] = m
+    else:
+        for bh in todo:
+            meta[bh] = one(bh)[1]
     return q, k, v, meta
 
 
