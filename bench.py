@@ -116,6 +116,10 @@ def main():
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention error check")
+    ap.add_argument("--warm-start", action="store_true",
+                    help="steady state of consecutive calls: both k-means start from the previous "
+                         "call's centroids and run 2 assignments; calls alternate between the "
+                         "inputs and a copy perturbed by 5%% noise (as between denoising steps)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one plain fp32 copy (x * 1 over 256 MiB in, 256 MiB out) before the "
                          "timed region, so hardware counters of a known traffic can calibrate "
@@ -137,13 +141,28 @@ def main():
     log(f"inputs {tuple(q.shape)} {q.dtype} generated in {time.perf_counter() - t0:.1f}s")
 
     p = params_for(S, wl, args.density)
+    inputs = [(q, k, v)]
+    if args.warm_start:
+        p.warm_start, p.warm_iters = 1, 2
+        gen = torch.Generator(device=q.device)
+        gen.manual_seed(1234)
+
+        def nudge(x):
+            xf = x.float()
+            noise = torch.randn(xf.shape, generator=gen, device=x.device, dtype=torch.float32)
+            return (xf + 0.05 * xf.std() * noise).to(x.dtype)
+
+        inputs.append(tuple(nudge(x) for x in (q, k, v)))
     op = S.SparsePR(S.shape_of(q), p)
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream()
+    ncall = [0]
 
     def call():
-        op.plan(q, k, stream)
-        op.attend(q, k, v, out, stream)
+        qi, ki, vi = inputs[ncall[0] % len(inputs)]
+        ncall[0] += 1
+        op.plan(qi, ki, stream)
+        op.attend(qi, ki, vi, out, stream)
 
     for _ in range(args.warmup):
         call()
@@ -210,7 +229,10 @@ def main():
                    "n": wl.n, "heads": wl.batch * wl.heads, "d": d,
                    "target_exec_density": args.density, "kv_groups": wl.groups()[0],
                    "q_groups": wl.groups()[1], "probes": wl.n_probes, "resid_rank": wl.resid_rank,
-                   "ridge": wl.ridge, "kmeans_iters": wl.kmeans_iters},
+                   "ridge": wl.ridge, "kmeans_iters": wl.kmeans_iters,
+                   "kmeans_start": ("warm: 2 assignments from the previous call's centroids, "
+                                    "inputs alternating with a 5%-noise copy")
+                   if args.warm_start else "cold (strided rows)"},
         "rho_exec": round(st["rho_exec"], 6),
         "rho_route": round(st["rho_route"], 6),
         "exec_pairs": st["exec_pairs"],
@@ -225,7 +247,8 @@ def main():
     }
 
     if not args.no_dense:
-        dense = S.dense_attention(q, k, v)
+        ql, kl, vl = inputs[(ncall[0] - 1) % len(inputs)]  # the inputs of the last call
+        dense = S.dense_attention(ql, kl, vl)
         torch.cuda.synchronize()
         o = out.float()
         dn = dense.float()

@@ -84,6 +84,13 @@ typedef struct {
   float eps_x;                 /* variance floor of eq. app_feature_scale; 1e-6 */
   int32_t n_dense_prefix;      /* leading rows (e.g. text tokens) routed densely,
                                   outside clustering, probes and the budget; 0 */
+  int32_t warm_start;          /* 1: both k-means start from the final centroids of
+                                  this plan's previous sparsepr_plan call instead of
+                                  the strided rows (the warm-started k-means of
+                                  App. C.1, for consecutive calls such as denoising
+                                  steps); the first call on a plan starts cold; 0 */
+  int32_t warm_iters;          /* assignments of a warm-started k-means, in
+                                  [1, kmeans_iters]; 0 = kmeans_iters; 0 */
 } sparsepr_params;
 
 /* Realised accounting of one call (Sec. 4.3: rho_exec = rho_route + M/N_q). */

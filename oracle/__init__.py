@@ -124,13 +124,21 @@ def project(x, f, rms=False, eps=1e-6):
     return phi
 
 
-def kmeans(pts, c, iters):
+def kmeans(pts, c, iters, init=None):
+    """Lloyd k-means; cold start from the strided points, or warm start from
+    the centroids `init` (c x r) when given."""
     pts = _f32(pts)
     n, r = pts.shape
     labels = np.zeros(n, np.int32)
     cent = np.zeros((c, r), np.float32)
     counts = np.zeros(c, np.int32)
-    it = lib().or_kmeans(_p(pts), n, r, c, iters, _p(labels), _p(cent), _p(counts))
+    if init is None:
+        it = lib().or_kmeans(_p(pts), n, r, c, iters, _p(labels), _p(cent), _p(counts))
+    else:
+        init = _f32(init)
+        assert init.shape == (c, r)
+        it = lib().or_kmeans_from(_p(pts), n, r, c, iters, _p(init), _p(labels), _p(cent),
+                                  _p(counts))
     return labels, cent, counts, it
 
 

@@ -253,12 +253,9 @@ void or_kmeans_assign(const float* pts, int n, int r, const float* cent, int c, 
   free(u);
 }
 
-int or_kmeans(const float* pts, int n, int r, int c, int iters, int32_t* labels, float* cent,
-              int32_t* counts) {
-  /* Reading: cold start from the strided points floor(b*n/c); a fixed number
-   * of Lloyd iterations; empty groups keep their centroid. */
-  for (int b = 0; b < c; ++b)
-    memcpy(cent + (size_t)b * r, pts + (size_t)(((int64_t)b * n) / c) * r, sizeof(float) * r);
+/* Lloyd iterations from the centroids already in `cent`. */
+static int kmeans_iterate(const float* pts, int n, int r, int c, int iters, int32_t* labels,
+                          float* cent, int32_t* counts) {
   int32_t* prev = (int32_t*)malloc(sizeof(int32_t) * n);
   double* sum = (double*)malloc(sizeof(double) * (size_t)c * r);
   int done = 0;
@@ -286,6 +283,22 @@ int or_kmeans(const float* pts, int n, int r, int c, int iters, int32_t* labels,
   free(sum);
   free(prev);
   return done;
+}
+
+int or_kmeans(const float* pts, int n, int r, int c, int iters, int32_t* labels, float* cent,
+              int32_t* counts) {
+  /* Reading: cold start from the strided points floor(b*n/c); a fixed number
+   * of Lloyd iterations; empty groups keep their centroid. */
+  for (int b = 0; b < c; ++b)
+    memcpy(cent + (size_t)b * r, pts + (size_t)(((int64_t)b * n) / c) * r, sizeof(float) * r);
+  return kmeans_iterate(pts, n, r, c, iters, labels, cent, counts);
+}
+
+int or_kmeans_from(const float* pts, int n, int r, int c, int iters, const float* init,
+                   int32_t* labels, float* cent, int32_t* counts) {
+  /* Warm start (App. C.1): the same iterations from given centroids. */
+  memcpy(cent, init, sizeof(float) * (size_t)c * r);
+  return kmeans_iterate(pts, n, r, c, iters, labels, cent, counts);
 }
 
 void or_group_mean(const float* x, int n, int d, const int32_t* labels, int c, float* mean,

@@ -68,6 +68,12 @@ void or_project(const float* x, int n, int d, const double* f, int r, int rms, d
 int or_kmeans(const float* pts, int n, int r, int c, int iters, int32_t* labels, float* cent,
               int32_t* counts);
 
+/* The same Lloyd iterations started from the centroids `init` (c x r) instead
+ * of the strided points: the warm-started k-means of App. C.1, which reuses the
+ * previous call's centroids.  Returns the number of assignments performed. */
+int or_kmeans_from(const float* pts, int n, int r, int c, int iters, const float* init,
+                   int32_t* labels, float* cent, int32_t* counts);
+
 /* One assignment step with the score above (exposed for stage tests).
  * scores (optional): n x c. */
 void or_kmeans_assign(const float* pts, int n, int r, const float* cent, int c, int32_t* labels,

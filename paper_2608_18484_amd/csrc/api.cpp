@@ -163,6 +163,10 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   if (p->kmeans_iters < 1 || p->kmeans_iters > 1000)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "kmeans_iters must be in [1, 1000]");
   if (p->n_probes < 0) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "n_probes must be >= 0");
+  if (p->warm_start != 0 && p->warm_start != 1)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "warm_start must be 0 or 1");
+  if (p->warm_iters < 0 || p->warm_iters > p->kmeans_iters)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "warm_iters must be in [0, kmeans_iters]");
   if (p->resid_rank < 1 || p->resid_rank > s->d_v)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "resid_rank must be in [1, d_v]");
   if (!(p->target_exec_density > 0.f) || !(p->target_exec_density <= 1.f))
@@ -186,6 +190,8 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.CQt = CQ + (g.ntext > 0);
   g.Ms = std::min(p->n_sampled_queries, NV);
   g.T = p->kmeans_iters;
+  g.warm = p->warm_start;
+  g.T_warm = p->warm_iters > 0 ? p->warm_iters : p->kmeans_iters;
   g.M = std::min(p->n_probes, NV);
   g.r = p->resid_rank;
   g.bf16 = s->dtype == SPARSEPR_BF16;
@@ -229,6 +235,7 @@ struct sparsepr_plan_s {
   char* base;
   size_t bytes;
   bool planned;
+  bool have_centroids = false;  // a previous sparsepr_plan call left its centroids
   // event timing (sparsepr_set_profiling): a ring of event sets, so timed
   // loops of up to kRing calls need no host synchronisation
   static constexpr int kRing = 64;
@@ -287,6 +294,8 @@ void sparsepr_params_default(sparsepr_params* p) {
   p->eps_q = 1e-6f;
   p->eps_x = 1e-6f;
   p->n_dense_prefix = 0;
+  p->warm_start = 0;
+  p->warm_iters = 0;
 }
 
 sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const sparsepr_params* params,
@@ -349,11 +358,12 @@ sparsepr_status sparsepr_plan(sparsepr_plan_t plan, const void* q, const void* k
     ev = plan->ev_plan[plan->n_plan++];
     (void)hipEventRecord(ev[0], (hipStream_t)stream);
   }
-  launch_plan(plan->g, plan->w, q, k, (hipStream_t)stream);
+  launch_plan(plan->g, plan->w, q, k, (hipStream_t)stream, plan->g.warm && plan->have_centroids);
   if (ev) (void)hipEventRecord(ev[1], (hipStream_t)stream);
   const sparsepr_status st = hip_check(hipGetLastError(), "sparsepr_plan launch");
   if (st != SPARSEPR_OK) return st;
   plan->planned = true;
+  plan->have_centroids = true;
   return ok();
 }
 

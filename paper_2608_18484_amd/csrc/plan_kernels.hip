@@ -1311,7 +1311,7 @@ __global__ __launch_bounds__(256) void k_probe_weights(Geom g, Work w) {
 }
 
 // Final per-head counters: k-means assignments performed, nonempty groups.
-__global__ __launch_bounds__(256) void k_plan_stats(Geom g, Work w, int with_kmeans) {
+__global__ __launch_bounds__(256) void k_plan_stats(Geom g, Work w, int with_kmeans, int iters) {
   __shared__ int red[2][4];
   const int bh = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
@@ -1334,7 +1334,7 @@ __global__ __launch_bounds__(256) void k_plan_stats(Geom g, Work w, int with_kme
       for (int sel = 0; sel < 2; ++sel) {
         const int32_t* chg = w.kmstate + (size_t)bh * 2 * (g.T + 1) + sel * (g.T + 1);
         int n = 1;
-        for (int it = 1; it < g.T && chg[it - 1] != 0; ++it) ++n;
+        for (int it = 1; it < iters && chg[it - 1] != 0; ++it) ++n;
         st[sel == 0 ? ST_ITK : ST_ITQ] = n;
       }
       int64_t rescans = 0;
@@ -1386,13 +1386,15 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   k_km_fallback<MAXR><<<dim3(64, BH), 256, 0, s>>>(a, it);
 }
 
-static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s) {
+static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm) {
   const int BH = g.BH;
   KmArgs a = a0;
   a.RP = (a.R + 15) / 16 * 16;
   a.CP = (a.C + 31) / 32 * 32;
-  k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
-  for (int it = 0; it < g.T; ++it) {
+  // warm start: the centroids left by the previous call are the initial ones
+  if (!warm) k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
+  const int iters = warm ? g.T_warm : g.T;
+  for (int it = 0; it < iters; ++it) {
     if (a.R <= 32)
       assign_step<32>(g, a, it, s);
     else if (a.R <= 64)
@@ -1422,7 +1424,8 @@ static void project(const Geom& g, const Work& w, const void* x, const float* F,
 }
 
 template <int D>
-static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s) {
+static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s,
+                   bool warm) {
   const int BH = g.BH;
   k_plan_init<<<BH, 64, 0, s>>>(g, w);
   // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1)
@@ -1432,7 +1435,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
-  run_kmeans(g, ak, s);
+  run_kmeans(g, ak, s, warm);
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
                                                          w.kbar);
@@ -1442,7 +1445,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
-  run_kmeans(g, aq, s);
+  run_kmeans(g, aq, s, warm);
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
                                                          w.qbar);
   // Routing (Sec. 4.3)
@@ -1465,14 +1468,15 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
     k_probe_d2<<<dim3((g.NV + 255) / 256, BH), 256, 0, s>>>(g, w);
     k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
   }
-  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 1);
+  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 1, warm ? g.T_warm : g.T);
 }
 
-void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s) {
+void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s,
+                 bool warm) {
   if (g.d == 64)
-    plan_d<64>(g, w, q, k, s);
+    plan_d<64>(g, w, q, k, s, warm);
   else
-    plan_d<128>(g, w, q, k, s);
+    plan_d<128>(g, w, q, k, s, warm);
 }
 
 void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s) {
@@ -1490,7 +1494,7 @@ void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s) {
   k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);
   k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
   if (g.M > 0) k_probe_weights<<<BH, 256, 0, s>>>(g, w);
-  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 0);
+  k_plan_stats<<<BH, 256, 0, s>>>(g, w, 0, g.T);
 }
 
 }  // namespace sparsepr

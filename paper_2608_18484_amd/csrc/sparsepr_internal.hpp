@@ -31,7 +31,9 @@ struct Geom {
   int CK, CQ;             // video groups
   int CKt, CQt;           // + the dense-prefix group when ntext > 0
   int Ms;                 // sampled queries (clamped to NV)
-  int T;                  // k-means iterations
+  int T;                  // k-means iterations (cold start; sizes the per-iteration state)
+  int T_warm;             // k-means iterations when warm-started (<= T)
+  int warm;               // warm start requested
   int M;                  // probes per head, min(n_probes, NV)
   int r;                  // residual rank
   int bf16;               // 1: bf16 tensors, 0: fp32
@@ -125,7 +127,8 @@ enum {
 };
 
 // ---- plan kernels -------------------------------------------------------
-void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s);
+void launch_plan(const Geom& g, const Work& w, const void* q, const void* k, hipStream_t s,
+                 bool warm);
 // Rebuild permutations, route lists, chunks and probe weights from labels,
 // z and probes already placed in the workspace for head bh (import path).
 void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s);

@@ -35,7 +35,8 @@ class Params(ctypes.Structure):
                 ("target_exec_density", ctypes.c_float), ("n_probes", ctypes.c_int32),
                 ("resid_rank", ctypes.c_int32), ("ridge", ctypes.c_float),
                 ("eps_q", ctypes.c_float), ("eps_x", ctypes.c_float),
-                ("n_dense_prefix", ctypes.c_int32)]
+                ("n_dense_prefix", ctypes.c_int32), ("warm_start", ctypes.c_int32),
+                ("warm_iters", ctypes.c_int32)]
 
 
 class Stats(ctypes.Structure):

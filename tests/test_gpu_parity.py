@@ -248,3 +248,46 @@ def test_key_segments_match_single_pass(orc, monkeypatch, ntext):
     ref, _ = _replay(orc, r2, ex, 0, 0)
     err = rel_l2(r2["out"][0, 0], ref)
     assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("ntext", [0, 96])
+def test_warm_started_kmeans(orc, ntext):
+    # Warm start (App. C.1): the second call on a plan starts both k-means from
+    # the first call's final centroids.  Labels and centroids must be bit-exact
+    # with the oracle's warm-started k-means on the GPU's coordinates, and the
+    # output must match the oracle's replay of the second plan.
+    from paper_2608_18484_amd import sparsepr as S
+    wl = medium(heads=2).with_(n_text=ntext)
+    q, k, v, _ = W.make_inputs(wl)
+    rng = np.random.default_rng(5)
+    # a nearby second input (as between consecutive denoising steps)
+    q2, k2, v2 = (W.bf16_round(x + 0.05 * np.std(x) * rng.standard_normal(x.shape).astype(np.float32))
+                  for x in (q, k, v))
+    p = params_for(wl, warm_start=1, warm_iters=2)
+    tq, tk, tv = to_device(q, k, v, wl.dtype)
+    op = S.SparsePR(S.shape_of(tq), p)
+    out = torch.empty_like(tq)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    first = [op.export(h, fields=["cent_k", "cent_q"]) for h in range(2)]
+    assert op.stats()["kmeans_iters_kv"] > 2  # the first call starts cold
+    tq2, tk2, tv2 = to_device(q2, k2, v2, wl.dtype)
+    op.plan(tq2, tk2)
+    op.attend(tq2, tk2, tv2, out)
+    torch.cuda.synchronize()
+    st = op.stats()
+    assert st["kmeans_iters_kv"] <= 2 and st["kmeans_iters_q"] <= 2
+    nt = ntext
+    outn = out.float().cpu().numpy()
+    for h in range(2):
+        ex = op.export(h)
+        lab_k, cent_k, _, _ = orc.kmeans(ex["phi_k"], p.n_kv_groups, 2, init=first[h]["cent_k"])
+        assert np.array_equal(ex["labels_kv"][nt:], lab_k)
+        assert np.array_equal(ex["cent_k"], cent_k)
+        lab_q, cent_q, _, _ = orc.kmeans(ex["phi_q"], p.n_q_groups, 2, init=first[h]["cent_q"])
+        assert np.array_equal(ex["labels_q"][nt:], lab_q)
+        assert np.array_equal(ex["cent_q"], cent_q)
+        r2 = dict(q=q2, k=k2, v=v2, p=p)
+        ref, _ = _replay(orc, r2, ex, 0, h)
+        err = rel_l2(outn[0, h], ref)
+        assert err < 2e-2, (h, err)

@@ -289,6 +289,38 @@ def test_kmeans_converged_labels_are_fixed_point(orc):
     assert np.array_equal(orc.kmeans_assign(x, cent), lab)
 
 
+def test_kmeans_warm_start_from_strided_points_is_cold_start(orc):
+    # Warm start (App. C.1) from the cold start's own initial centroids is the cold start
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((600, 5)).astype(np.float32)
+    c = 7
+    init = x[(np.arange(c) * len(x)) // c]
+    lab0, cent0, _, it0 = orc.kmeans(x, c, 5)
+    lab1, cent1, _, it1 = orc.kmeans(x, c, 5, init=init)
+    assert it0 == it1 and np.array_equal(lab0, lab1) and np.array_equal(cent0, cent1)
+
+
+def test_kmeans_warm_start_continues_the_iterations(orc):
+    # T1 cold assignments then T2 warm ones from the resulting centroids give
+    # the labels and centroids of T1 + T2 cold assignments
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((900, 3)).astype(np.float32)
+    c = 12
+    lab_a, cent_a, _, _ = orc.kmeans(x, c, 3)
+    lab_b, cent_b, _, _ = orc.kmeans(x, c, 2, init=cent_a)
+    lab_c, cent_c, _, _ = orc.kmeans(x, c, 5)
+    assert np.array_equal(lab_b, lab_c) and np.array_equal(cent_b, cent_c)
+
+
+def test_kmeans_warm_start_at_a_fixed_point_stops(orc):
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((500, 4)).astype(np.float32)
+    lab, cent, _, it = orc.kmeans(x, 5, 200)
+    assert it < 200
+    lab2, cent2, _, it2 = orc.kmeans(x, 5, 10, init=cent)
+    assert it2 <= 2 and np.array_equal(lab2, lab) and np.array_equal(cent2, cent)
+
+
 # --------------------------------------------------------------------------
 # Group-major permutation (Sec. 4.3)
 # --------------------------------------------------------------------------
