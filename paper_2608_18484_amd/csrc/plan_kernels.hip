@@ -657,9 +657,10 @@ __global__ __launch_bounds__(64) void k_sort_scatter(KmArgs a, int it) {
         const uint64_t below = m & ((1ull << lane) - 1ull);
         perm[pos[Lf] + __popcll(below)] = a.row0 + j;
       }
-      __syncthreads();
+      // the block is one wave: its LDS accesses complete in program order,
+      // so the update below is seen by the next reads without a barrier
+      // (a barrier would also wait for the permutation stores)
       if (lane == first) pos[Lf] += __popcll(m);
-      __syncthreads();
       active &= ~m;
     }
   }
@@ -680,18 +681,15 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   const float* pts = a.pts + (size_t)bh * a.n * a.R;
   const int R = a.R;
   for (int k = lane; k < R; k += 64) {
-    // members loaded four at a time, added in ascending order
+    // members loaded eight at a time, added in ascending order
     double sum = 0.0;
     int m = s0;
-    for (; m + 4 <= s1; m += 4) {
-      const float v0 = pts[(size_t)(perm[m] - a.row0) * R + k];
-      const float v1 = pts[(size_t)(perm[m + 1] - a.row0) * R + k];
-      const float v2 = pts[(size_t)(perm[m + 2] - a.row0) * R + k];
-      const float v3 = pts[(size_t)(perm[m + 3] - a.row0) * R + k];
-      sum += (double)v0;
-      sum += (double)v1;
-      sum += (double)v2;
-      sum += (double)v3;
+    for (; m + 8 <= s1; m += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = pts[(size_t)(perm[m + u] - a.row0) * R + k];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += (double)v[u];
     }
     for (; m < s1; ++m) sum += (double)pts[(size_t)(perm[m] - a.row0) * R + k];
     a.cent[((size_t)bh * a.C + b) * R + k] = (float)(sum / (double)(s1 - s0));
