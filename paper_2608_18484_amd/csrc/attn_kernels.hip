@@ -53,6 +53,7 @@ struct AttnArgs {
   // [seg_lo, seg_hi) are processed; (O, m, l) carry over between segments
   float* mlst;
   int seg_lo, seg_hi, seg_first, seg_last;
+  int heads_per_xcd;  // MODE_SPARSE block order (see k_attn_mfma)
 };
 
 // Where the rows and keys of one block come from.
@@ -212,16 +213,26 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const uint16_t* Kp;
   const uint16_t* Vp;
   if (MODE == MODE_SPARSE) {
-    // XCD-aware order: hardware block b runs on XCD b % 8; XCD x takes the
-    // contiguous slice [x*per, (x+1)*per) of the head's chunks, so spatially
-    // adjacent query groups (which route to overlapping K/V groups) share an
-    // L2, and all XCDs work on the same head at a time.
-    bh = blockIdx.y;
-    const int nch = A.nchunks[bh];
-    const int per = (nch + 7) / 8;
-    const int x = blockIdx.x & 7, y = blockIdx.x >> 3;
-    const int cx = x * per + y;
-    if (y >= per || cx >= nch) return;
+    // XCD-aware order: hardware block b runs on XCD b % 8.
+    //  * heads_per_xcd (head count a multiple of 8): grid (8 * nchunk_max,
+    //    BH / 8); XCD x runs every chunk of heads x, x + 8, ... in turn, so
+    //    its L2 only ever holds one head's K/V segment and all of that
+    //    head's query groups reuse it.
+    //  * otherwise: grid (8 * ceil(nchunk_max / 8), BH); XCD x takes the
+    //    contiguous slice [x*per, (x+1)*per) of each head's chunks.
+    int cx;
+    if (A.heads_per_xcd) {
+      bh = blockIdx.y * 8 + (blockIdx.x & 7);
+      cx = blockIdx.x >> 3;
+      if (cx >= A.nchunks[bh]) return;
+    } else {
+      bh = blockIdx.y;
+      const int nch = A.nchunks[bh];
+      const int per = (nch + 7) / 8;
+      const int x = blockIdx.x & 7, y = blockIdx.x >> 3;
+      cx = x * per + y;
+      if (y >= per || cx >= nch) return;
+    }
     const int4 c = A.chunks[(size_t)bh * g.nchunk_max + cx];
     w.a = c.x;
     w.rbase = A.offq[(size_t)bh * (g.CQt + 1) + c.x] + c.y;
@@ -1090,7 +1101,10 @@ static void attend_d(const Geom& g, const Work& w, const void* q, const void* k,
       as.seg_hi = (int)((int64_t)g.N * (sg + 1) / g.nseg);
       as.seg_first = sg == 0;
       as.seg_last = sg == g.nseg - 1;
-      k_attn_mfma<D, MODE_SPARSE><<<dim3(8 * g.nchunk_per_xcd, g.BH), 128, 0, s>>>(g, as);
+      as.heads_per_xcd = g.BH % 8 == 0;
+      const dim3 grid = as.heads_per_xcd ? dim3(8 * g.nchunk_max, g.BH / 8)
+                                         : dim3(8 * g.nchunk_per_xcd, g.BH);
+      k_attn_mfma<D, MODE_SPARSE><<<grid, 128, 0, s>>>(g, as);
     }
   } else
     k_attn_f32<D, MODE_SPARSE><<<dim3(g.nchunk_max, g.BH), 64, 0, s>>>(g, a);

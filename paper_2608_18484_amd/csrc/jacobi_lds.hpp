@@ -59,33 +59,51 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
         rot[tid] = JacobiRot<T>{c, s, p, q};
       }
       __syncthreads();
+      // All of a thread's loads are issued before any of its stores: its
+      // 2x2 blocks and eigenvector row pairs are disjoint from every other
+      // thread's, so one LDS round trip serves the whole update.
+      constexpr int NB = P * P / NT, NVR = D * P / NT;
       const int j = tid % P;
       const JacobiRot<T> rj = rot[j];
+      JacobiRot<T> ri[NB];
+      T x[NB][4], vp[NVR], vq[NVR];
 #pragma unroll
-      for (int k = 0; k < P * P / NT; ++k) {
+      for (int k = 0; k < NB; ++k) ri[k] = rot[tid / P + k * (NT / P)];
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int p = ri[k].p, q = ri[k].q;
+        x[k][0] = A[p * LD + rj.p];
+        x[k][1] = A[p * LD + rj.q];
+        x[k][2] = A[q * LD + rj.p];
+        x[k][3] = A[q * LD + rj.q];
+      }
+#pragma unroll
+      for (int k = 0; k < NVR; ++k) {
+        const int row = tid / P + k * (NT / P);
+        vp[k] = V[row * LD + rj.p];
+        vq[k] = V[row * LD + rj.q];
+      }
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
         const int i = tid / P + k * (NT / P);
-        const JacobiRot<T> ri = rot[i];
-        if (ri.s == T(0) && rj.s == T(0)) continue;
-        const int p = ri.p, q = ri.q, p2 = rj.p, q2 = rj.q;
-        const T x00 = A[p * LD + p2], x01 = A[p * LD + q2];
-        const T x10 = A[q * LD + p2], x11 = A[q * LD + q2];
-        const T y00 = x00 * rj.c - x01 * rj.s, y01 = x00 * rj.s + x01 * rj.c;
-        const T y10 = x10 * rj.c - x11 * rj.s, y11 = x10 * rj.s + x11 * rj.c;
-        T z00 = ri.c * y00 - ri.s * y10, z01 = ri.c * y01 - ri.s * y11;
-        T z10 = ri.s * y00 + ri.c * y10, z11 = ri.s * y01 + ri.c * y11;
+        if (ri[k].s == T(0) && rj.s == T(0)) continue;
+        const int p = ri[k].p, q = ri[k].q;
+        const T y00 = x[k][0] * rj.c - x[k][1] * rj.s, y01 = x[k][0] * rj.s + x[k][1] * rj.c;
+        const T y10 = x[k][2] * rj.c - x[k][3] * rj.s, y11 = x[k][2] * rj.s + x[k][3] * rj.c;
+        T z00 = ri[k].c * y00 - ri[k].s * y10, z01 = ri[k].c * y01 - ri[k].s * y11;
+        T z10 = ri[k].s * y00 + ri[k].c * y10, z11 = ri[k].s * y01 + ri[k].c * y11;
         if (i == j) z01 = z10 = T(0);
-        A[p * LD + p2] = z00;
-        A[p * LD + q2] = z01;
-        A[q * LD + p2] = z10;
-        A[q * LD + q2] = z11;
+        A[p * LD + rj.p] = z00;
+        A[p * LD + rj.q] = z01;
+        A[q * LD + rj.p] = z10;
+        A[q * LD + rj.q] = z11;
       }
       if (rj.s != T(0)) {
 #pragma unroll
-        for (int k = 0; k < D * P / NT; ++k) {
+        for (int k = 0; k < NVR; ++k) {
           const int row = tid / P + k * (NT / P);
-          const T vp = V[row * LD + rj.p], vq = V[row * LD + rj.q];
-          V[row * LD + rj.p] = rj.c * vp - rj.s * vq;
-          V[row * LD + rj.q] = rj.s * vp + rj.c * vq;
+          V[row * LD + rj.p] = rj.c * vp[k] - rj.s * vq[k];
+          V[row * LD + rj.q] = rj.s * vp[k] + rj.c * vq[k];
         }
       }
       __syncthreads();
