@@ -28,6 +28,15 @@
  *    four; accumulation is always at least float32.
  *  - Every batch x head pair is an independent SparsePR call with the same
  *    parameters; all of them are processed by each launch.
+ *  - Grouped-query attention (heads_kv < heads): query heads h*G .. h*G+G-1
+ *    (G = heads / heads_kv) attend to K/V head h, and share its partition,
+ *    routes and probe rows (Sec. 4.3: K/V partition and routing metadata are
+ *    shared across the associated query heads; App. B.1: M_K per K/V head).
+ *    The plan of a K/V head pools its G query heads: M_K averages their
+ *    strided-sample metrics, the query-response coordinates phi_Q average
+ *    their per-head normalised coordinates, and the route scores use the
+ *    query-group means averaged over them.  Every query head then runs its
+ *    own sparse attention, exact probe rows, fit and correction.
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    Work is enqueued asynchronously on it; the caller keeps Q, K, V, the
  *    output and the workspace alive until that work has completed.  Only
@@ -62,11 +71,14 @@ typedef enum { SPARSEPR_F32 = 0, SPARSEPR_BF16 = 1 } sparsepr_dtype;
 
 /* Tensor geometry.  Self-attention only: n_q == n_kv.  d == d_v in {64, 128}. */
 typedef struct {
-  int32_t batch, heads;
+  int32_t batch, heads;                 /* heads = query heads (Q and the output) */
   int32_t n_q, n_kv;
   int32_t d, d_v;
-  int64_t stride_b, stride_h, stride_n; /* element strides shared by Q, K, V and O */
+  int64_t stride_b, stride_h, stride_n; /* element strides of Q and O; stride_n also of K, V */
   int32_t dtype;                        /* sparsepr_dtype */
+  int32_t heads_kv;                     /* K/V heads, a divisor of heads; 0 = heads */
+  int64_t kv_stride_b, kv_stride_h;     /* batch and head strides of K and V; 0 = stride_b,
+                                           stride_h (required when heads_kv < heads) */
 } sparsepr_shape;
 
 /* Per-call method parameters (paper defaults from App. C.2 where it gives them). */
@@ -93,7 +105,10 @@ typedef struct {
                                   [1, kmeans_iters]; 0 = kmeans_iters; 0 */
 } sparsepr_params;
 
-/* Realised accounting of one call (Sec. 4.3: rho_exec = rho_route + M/N_q). */
+/* Realised accounting of one call (Sec. 4.3: rho_exec = rho_route + M/N_q).
+ * Pair and probe counts are summed over query heads (every query head of a
+ * group evaluates its K/V head's cells); cells, groups and k-means figures
+ * over plans (K/V heads). */
 typedef struct {
   double rho_route;          /* routed pairs / (n_q n_kv), mean over heads */
   double rho_exec;           /* rho_route + probes / n_q, mean over heads */
@@ -176,7 +191,8 @@ sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const spars
  * (INVALID_ARGUMENT otherwise): batch, heads >= 1; n_q == n_kv >= 1;
  * 0 <= n_dense_prefix < n_q; 1 <= C_k, C_q <= n_v; 1 <= r_k, r_q;
  * 1 <= M_s; 0 <= M; 1 <= r <= d_v; 0 < rho <= 1; ridge >= 0; eps >= 0;
- * stride_n >= d.  UNSUPPORTED: d != d_v, d not in {64, 128}, C_k or C_q
+ * stride_n >= d; heads_kv a divisor of heads, with kv_stride_b and
+ * kv_stride_h given when heads_kv < heads.  UNSUPPORTED: d != d_v, d not in {64, 128}, C_k or C_q
  * above 8191, n_q above 2^24, strides not multiples of 8 elements,
  * n_kv * stride_n * element size of 4 GiB or more (one head's K/V rows are
  * addressed with 32-bit byte offsets). */
@@ -207,12 +223,14 @@ sparsepr_status sparsepr_dense_attend(const sparsepr_shape* shape, const void* q
 /* Synchronise `stream` and read the realised accounting of the last call. */
 sparsepr_status sparsepr_get_stats(sparsepr_plan_t plan, sparsepr_stats* out, void* stream);
 
-/* Copy head `bh` (= b * heads + h) of the current plan (and, after attend,
- * of its outputs) into caller host buffers.  Synchronises `stream`. */
+/* Copy the plan used by query head `bh` (= b * heads + h), i.e. that of K/V
+ * head b * heads_kv + h / G, and, after attend, query head bh's own outputs
+ * into caller host buffers.  Synchronises `stream`. */
 sparsepr_status sparsepr_plan_export(sparsepr_plan_t plan, int32_t bh, sparsepr_plan_host* out,
                                      void* stream);
 
-/* Replace head `bh` of the plan by labels_q, labels_kv, routes and probes
+/* Replace the plan used by query head `bh` (that of its K/V head, shared by
+ * the whole group) by labels_q, labels_kv, routes and probes
  * from host memory (all four required).  Group-major permutations, offsets,
  * route lists and coverage weights are rebuilt on the device.  Errors:
  * INVALID_ARGUMENT for out-of-range labels or probes. */

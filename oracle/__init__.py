@@ -96,6 +96,34 @@ def key_metric(q, m_s):
     return out
 
 
+def key_metric_pooled(q, m_s):
+    """M_K pooled over the query heads of q [G, n, d] (their mean)."""
+    q = _f32(q)
+    nh, n, d = q.shape
+    out = np.zeros((d, d), np.float64)
+    lib().or_key_metric_pooled(_p(q), nh, n, d, m_s, _p(out))
+    return out
+
+
+def project_pooled(x, f, eps=1e-6):
+    """Mean over the heads of x [G, n, d] of the normalised query coordinates."""
+    x, f = _f32(x), _f64(f)
+    nh, n, d = x.shape
+    r = f.shape[1]
+    phi = np.zeros((n, r), np.float32)
+    lib().or_project_pooled(_p(x), nh, n, d, _p(f), r, ctypes.c_double(eps), _p(phi))
+    return phi
+
+
+def group_mean_pooled(x, labels, c):
+    """Group means over the heads and members of x [G, n, d]."""
+    x = _f32(x)
+    nh, n, d = x.shape
+    mean = np.zeros((c, d), np.float32)
+    lib().or_group_mean_pooled(_p(x), nh, n, d, _p(_i32(labels)), c, _p(mean))
+    return mean
+
+
 def sym_eig(a):
     a = _f64(a)
     n = a.shape[0]
@@ -234,9 +262,12 @@ def correct_rows(x, ft):
 
 
 def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_probes):
-    """Whole Response-Coupled Partitioning + routing + probe choice for one head."""
+    """Whole Response-Coupled Partitioning + routing + probe choice for one
+    K/V head.  q is [n, d], or [G, n, d] for the G query heads that share the
+    K/V head under grouped-query attention (the plan pools them)."""
     q, k = _f32(q), _f32(k)
-    n, d = q.shape
+    nqh = 1 if q.ndim == 2 else q.shape[0]
+    n, d = q.shape[-2:]
     nv = n - n_text
     rk, rq = min(r_k, d), min(r_q, d)
     cq_t, ck_t = c_q + (n_text > 0), c_k + (n_text > 0)
@@ -250,7 +281,7 @@ def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_pro
         "cqphi": np.zeros((c_q, rq), np.float32), "prio": np.zeros((c_q, c_k), np.float32),
         "stats": np.zeros(7, np.int64),
     }
-    lib().or_plan(_p(q), _p(k), n, d, n_text, n_sampled, r_k, r_q, c_k, c_q, iters,
+    lib().or_plan(_p(q), nqh, _p(k), n, d, n_text, n_sampled, r_k, r_q, c_k, c_q, iters,
                   ctypes.c_double(density), n_probes, _p(out["labels_q"]), _p(out["labels_kv"]),
                   _p(out["z"]), _p(out["probes"]), _p(out["w"]), _p(out["fk"]), _p(out["fq"]),
                   _p(out["phik"]), _p(out["phiq"]), _p(out["kbar"]), _p(out["qbar"]),

@@ -707,14 +707,73 @@ void or_correct_rows(const double* x, int n_rows, int dv, const double* mu_x, co
 /* Whole call                                                                */
 /* ------------------------------------------------------------------------ */
 
-int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, int r_k, int r_q,
-            int ck, int cq, int iters, double density, int m, int32_t* labels_q,
+/* Grouped-query pooling (Sec. 4.3 shares the K/V partition and routes
+ * across a K/V head's query heads; App. B.1 builds M_K per K/V head).  The
+ * readings: the metric, the query coordinates and the query-group means are
+ * the plain means over the nqh query heads. */
+void or_key_metric_pooled(const float* q, int nqh, int n, int d, int m_s, double* mk) {
+  double* one = (double*)malloc(sizeof(double) * (size_t)d * d);
+  for (int a = 0; a < d * d; ++a) mk[a] = 0.0;
+  for (int h = 0; h < nqh; ++h) {
+    or_key_metric(q + (size_t)h * n * d, n, d, m_s, one);
+    for (int a = 0; a < d * d; ++a) mk[a] += one[a];
+  }
+  for (int a = 0; a < d * d; ++a) mk[a] /= (double)nqh;
+  free(one);
+}
+
+void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, double eps,
+                       float* phi) {
+#pragma omp parallel for schedule(static)
+  for (int i = 0; i < n; ++i) {
+    double acc[256];
+    for (int c = 0; c < r; ++c) acc[c] = 0.0;
+    for (int h = 0; h < nqh; ++h) {
+      const float* xi = x + ((size_t)h * n + i) * d;
+      double y[256];
+      double ss = 0.0;
+      for (int c = 0; c < r; ++c) {
+        double s = 0.0;
+        for (int a = 0; a < d; ++a) s += f[a * r + c] * (double)xi[a];
+        y[c] = s;
+        ss += s * s;
+      }
+      double den = sqrt(ss / (double)r); /* eq. query_response_feature */
+      if (den < eps) den = eps;
+      for (int c = 0; c < r; ++c) acc[c] += y[c] / den;
+    }
+    for (int c = 0; c < r; ++c) phi[(size_t)i * r + c] = (float)(acc[c] / (double)nqh);
+  }
+}
+
+void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* labels, int c,
+                          float* mean) {
+  double* sum = (double*)calloc((size_t)c * d, sizeof(double));
+  int64_t* cnt = (int64_t*)calloc((size_t)c, sizeof(int64_t));
+  for (int h = 0; h < nqh; ++h)
+    for (int j = 0; j < n; ++j) {
+      const int b = labels[j];
+      cnt[b] += 1;
+      for (int a = 0; a < d; ++a) sum[(size_t)b * d + a] += (double)x[((size_t)h * n + j) * d + a];
+    }
+  for (int b = 0; b < c; ++b)
+    for (int a = 0; a < d; ++a)
+      mean[(size_t)b * d + a] = cnt[b] ? (float)(sum[(size_t)b * d + a] / (double)cnt[b]) : 0.0f;
+  free(cnt);
+  free(sum);
+}
+
+int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
+            int r_q, int ck, int cq, int iters, double density, int m, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk_out,
             double* fq_out, float* phik_out, float* phiq_out, float* kbar_out, float* qbar_out,
             float* cqphi_out, float* prio_out, int64_t* stats) {
   const int nv = n - n_text;
-  const float* qv = q + (size_t)n_text * d;
   const float* kv = k + (size_t)n_text * d;
+  /* the video rows of every query head, one nv x d block each */
+  float* qv = (float*)malloc(sizeof(float) * (size_t)nqh * nv * d);
+  for (int h = 0; h < nqh; ++h)
+    memcpy(qv + (size_t)h * nv * d, q + ((size_t)h * n + n_text) * d, sizeof(float) * (size_t)nv * d);
   if (r_k > d) r_k = d;
   if (r_q > d) r_q = d;
   const int cq_t = cq + (n_text > 0), ck_t = ck + (n_text > 0);
@@ -727,7 +786,7 @@ int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, i
   float* centk = (float*)malloc(sizeof(float) * (size_t)ck * r_k);
   int32_t* labk = (int32_t*)malloc(sizeof(int32_t) * nv);
   int32_t* cntk = (int32_t*)malloc(sizeof(int32_t) * ck);
-  or_key_metric(qv, nv, d, m_s, mk);
+  or_key_metric_pooled(qv, nqh, nv, d, m_s, mk);
   or_response_basis(mk, d, r_k, tau, fk, NULL);
   or_project(kv, nv, d, fk, r_k, 0, 0.0, phik);
   const int itk = or_kmeans(phik, nv, r_k, ck, iters, labk, centk, cntk);
@@ -744,7 +803,7 @@ int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, i
   or_group_mean(kv, nv, d, labk, ck, kbar, cnt_dummy);
   or_query_metric(kbar, cntk, ck, d, mq);
   or_response_basis(mq, d, r_q, tau, fq, NULL);
-  or_project(qv, nv, d, fq, r_q, 1, 1e-6, phiq);
+  or_project_pooled(qv, nqh, nv, d, fq, r_q, 1e-6, phiq);
   const int itq = or_kmeans(phiq, nv, r_q, cq, iters, labq, centq, cntq);
 
   /* Routing (Sec. 4.3) */
@@ -752,7 +811,8 @@ int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, i
   int32_t* cntq2 = (int32_t*)malloc(sizeof(int32_t) * cq);
   float* prio = (float*)malloc(sizeof(float) * (size_t)cq * ck);
   uint8_t* zv = (uint8_t*)malloc((size_t)cq * ck);
-  or_group_mean(qv, nv, d, labq, cq, qbar, cntq2);
+  or_group_mean_pooled(qv, nqh, nv, d, labq, cq, qbar);
+  (void)cntq2;
   or_route_priorities(qbar, cntq, cq, kbar, cntk, ck, d, prio);
   const int meff = m < nv ? m : nv;
   /* the probe rows' cost against all keys is reserved first */
@@ -819,6 +879,7 @@ int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, i
   free(phik);
   free(fk);
   free(mk);
+  free(qv);
   return 0;
 }
 

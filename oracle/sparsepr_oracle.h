@@ -147,12 +147,32 @@ void or_correct_rows(const double* x, int n_rows, int dv, const double* mu_x, co
  *   stats[0] routed pairs, [1] forced pairs (incl. text), [2] routed cells,
  *   [3] forced cells, [4] probes, [5] k-means assignments (K/V),
  *   [6] k-means assignments (Q).
- * Any diagnostic pointer may be NULL. */
-int or_plan(const float* q, const float* k, int n, int d, int n_text, int m_s, int r_k, int r_q,
-            int ck, int cq, int iters, double density, int m, int32_t* labels_q,
+ * Any diagnostic pointer may be NULL.
+ *
+ * Grouped-query attention (Sec. 4.3: the K/V partition and routing metadata
+ * are shared by the query heads of a K/V head; App. B.1: M_K per K/V head):
+ * q holds the nqh query heads of one K/V head, one n x d block each, and the
+ * plan pools them -- M_K is the mean of their metrics (or_key_metric_pooled),
+ * phi_Q the mean of their normalised coordinates (or_project_pooled), and
+ * the query-group means feeding the route scores the mean over heads and
+ * members (or_group_mean_pooled).  nqh = 1 is the single-head plan. */
+int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
+            int r_q, int ck, int cq, int iters, double density, int m, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk, double* fq,
             float* phik, float* phiq, float* kbar, float* qbar, float* cqphi, float* prio,
             int64_t* stats);
+
+/* Pooled forms for grouped-query attention, over nqh query heads stored as
+ * consecutive n x d blocks of x (nqh = 1 gives the single-head functions):
+ *   M_K = (1/nqh) sum_h Q_s,h^T Q_s,h / M_s;
+ *   phi_i = (1/nqh) sum_h F^T x_h,i / max(sqrt(|F^T x_h,i|^2 / r), eps)
+ *     (eq. query_response_feature per head, then averaged; float output);
+ *   mean_b = sum_h sum_{j in b} x_h,j / (nqh |b|), 0 for an empty group. */
+void or_key_metric_pooled(const float* q, int nqh, int n, int d, int m_s, double* mk);
+void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, double eps,
+                       float* phi);
+void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* labels, int c,
+                          float* mean);
 
 /* Whole attend for one head given a plan: sparse rows, exact probes, fit,
  * correction, output in original row order (Eq. final_reconstructed_output).

@@ -44,11 +44,15 @@ std::string ptrs(const void* dst, const void* src, size_t n) {
   return buf;
 }
 
-// Per-head byte sizes of every workspace array, in layout order.
+// Per-head byte sizes of every workspace array, in layout order.  Plan
+// arrays are [BH][...] (one per K/V head); the attend outputs are
+// [G][BH][...] (one per query head, query head j < G of every K/V head
+// forming slab j, so that the view of slab j is again [BH][...]).
 struct Layout {
   struct Item {
     size_t field;     // byte offset of the pointer member inside Work
     size_t per_head;  // bytes per head
+    bool per_query;   // one per query head instead of per K/V head
   };
   std::vector<Item> items;
   size_t total = 0;
@@ -59,7 +63,10 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 void describe(const Geom& g, Work* w, Layout& L) {
   const size_t d = g.d, dv = g.dv, N = g.N, NV = g.NV, M = std::max(g.M, 1), r = g.r;
   auto add = [&](void* field, size_t bytes) {
-    L.items.push_back({(size_t)((char*)field - (char*)w), bytes});
+    L.items.push_back({(size_t)((char*)field - (char*)w), bytes, false});
+  };
+  auto addq = [&](void* field, size_t bytes) {
+    L.items.push_back({(size_t)((char*)field - (char*)w), bytes, true});
   };
   add(&w->gram_k, d * d * 8);
   add(&w->gram_q, d * d * 8);
@@ -106,29 +113,33 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->picks, M * 4);
   add(&w->kperm, g.bf16 ? N * d * 2 : 0);
   add(&w->vperm, g.bf16 ? N * dv * 2 : 0);
-  add(&w->osp, N * dv * 4);
-  add(&w->odp, M * dv * 4);
-  add(&w->part, M * g.nsplit * (dv + 2) * 4);
-  add(&w->mlst, N * 4 * 4);
-  add(&w->fitv, 3 * dv * 4);
-  add(&w->fity, dv * r * 4);
-  add(&w->fitpsi, dv * r * 4);
-  add(&w->fitscr, (2 * M * dv + M * r + dv * r + M) * 8);
-  add(&w->fitgram, 2 * dv * dv * 8);
+  addq(&w->osp, N * dv * 4);
+  addq(&w->odp, M * dv * 4);
+  addq(&w->part, M * g.nsplit * (dv + 2) * 4);
+  addq(&w->mlst, N * 4 * 4);
+  addq(&w->fitv, 3 * dv * 4);
+  addq(&w->fity, dv * r * 4);
+  addq(&w->fitpsi, dv * r * 4);
+  addq(&w->fitscr, (2 * M * dv + M * r + dv * r + M) * 8);
+  addq(&w->fitgram, 2 * dv * dv * 8);
+  addq(&w->fitvec, (!g.bf16 && dv > 64) ? dv * (dv + 1) * 8 : 0);
   add(&w->stats, 16 * 8);
   size_t off = 0;
-  for (auto& it : L.items) off += align256((size_t)g.BH * it.per_head);
+  for (auto& it : L.items) off += align256((size_t)g.BH * it.per_head * (it.per_query ? g.G : 1));
   L.total = off;
 }
 
 // Bind the layout to a base address: whole-batch view, or the view of a
-// single head (bh >= 0) in which that head appears as head 0.
-void bind(const Geom& g, Work* w, const Layout& L, char* base, int bh) {
+// single K/V head (bh >= 0) in which that head appears as head 0; the attend
+// outputs are those of query head j of each K/V head's group.
+void bind(const Geom& g, Work* w, const Layout& L, char* base, int bh, int j = 0) {
   size_t off = 0;
   for (auto& it : L.items) {
-    char* ptr = base + off + (bh >= 0 ? (size_t)bh * it.per_head : 0);
+    const size_t head = bh >= 0 ? (size_t)bh : 0;
+    const size_t idx = it.per_query ? (size_t)j * g.BH + head : (bh >= 0 ? head : 0);
+    char* ptr = base + off + idx * it.per_head;
     std::memcpy((char*)w + it.field, &ptr, sizeof ptr);  // every Work member is a pointer
-    off += align256((size_t)g.BH * it.per_head);
+    off += align256((size_t)g.BH * it.per_head * (it.per_query ? g.G : 1));
   }
 }
 
@@ -145,6 +156,22 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   if (s->stride_n < s->d || s->stride_h < 0 || s->stride_b < 0)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "strides must be non-negative and stride_n >= d");
   if (s->stride_n % 8 != 0 || s->stride_h % 8 != 0 || s->stride_b % 8 != 0)
+    return fail(SPARSEPR_ERR_UNSUPPORTED, "strides must be multiples of 8 elements");
+  // grouped-query attention: heads_kv K/V heads, each shared by heads / heads_kv
+  // consecutive query heads
+  const int hkv = s->heads_kv > 0 ? s->heads_kv : s->heads;
+  if (s->heads_kv < 0 || s->heads % hkv != 0)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "heads_kv must be 0 or a divisor of heads");
+  int64_t kvsb = s->kv_stride_b, kvsh = s->kv_stride_h;
+  if (hkv == s->heads) {
+    if (kvsb == 0) kvsb = s->stride_b;
+    if (kvsh == 0) kvsh = s->stride_h;
+  } else if (kvsb <= 0 || kvsh <= 0) {
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "kv_stride_b and kv_stride_h are required when heads_kv < heads");
+  }
+  if (kvsb < 0 || kvsh < 0)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "kv strides must be non-negative");
+  if (kvsb % 8 != 0 || kvsh % 8 != 0)
     return fail(SPARSEPR_ERR_UNSUPPORTED, "strides must be multiples of 8 elements");
   // the attention kernels address one head's K/V rows with 32-bit byte offsets
   if ((int64_t)s->n_kv * s->stride_n * (s->dtype == SPARSEPR_BF16 ? 2 : 4) >= (int64_t(1) << 32))
@@ -176,7 +203,10 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g = Geom{};
   g.B = s->batch;
   g.H = s->heads;
-  g.BH = s->batch * s->heads;
+  g.Hkv = hkv;
+  g.G = s->heads / hkv;
+  g.gq = 0;
+  g.BH = s->batch * hkv;
   g.N = N;
   g.ntext = p->n_dense_prefix;
   g.NV = NV;
@@ -198,6 +228,8 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.sb = s->stride_b;
   g.sh = s->stride_h;
   g.sn = s->stride_n;
+  g.kvsb = kvsb;
+  g.kvsh = kvsh;
   g.rho = p->target_exec_density;
   g.ridge = p->ridge;
   g.eps_q = p->eps_q;
@@ -230,7 +262,8 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
 
 struct sparsepr_plan_s {
   Geom g;
-  Work w;
+  Work w;                // whole-batch view (attend outputs of query head 0 of each group)
+  std::vector<Work> wq;  // the same with the attend outputs of query head j, j < G
   Layout L;
   char* base;
   size_t bytes;
@@ -333,6 +366,8 @@ sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr
   p->base = (char*)workspace;
   p->bytes = bytes;
   bind(g, &p->w, p->L, p->base, -1);
+  p->wq.resize(g.G);
+  for (int j = 0; j < g.G; ++j) bind(g, &p->wq[j], p->L, p->base, -1, j);
   // no work item and no probe until a plan exists
   st = hip_check(hipMemset(p->w.nchunks, 0, sizeof(int32_t) * g.BH), "hipMemset");
   if (st == SPARSEPR_OK) st = hip_check(hipMemset(p->w.nprobes, 0, sizeof(int32_t) * g.BH), "hipMemset");
@@ -381,7 +416,7 @@ sparsepr_status sparsepr_attend(sparsepr_plan_t plan, const void* q, const void*
     }
     ev = plan->ev_att[plan->n_att++];
   }
-  launch_attend(plan->g, plan->w, q, k, v, out, (hipStream_t)stream, ev);
+  launch_attend(plan->g, plan->wq.data(), q, k, v, out, (hipStream_t)stream, ev);
   const sparsepr_status st = hip_check(hipGetLastError(), "sparsepr_attend launch");
   if (st != SPARSEPR_OK) return st;
   return ok();
@@ -428,14 +463,15 @@ sparsepr_status sparsepr_get_stats(sparsepr_plan_t plan, sparsepr_stats* out, vo
   const double nn = (double)g.N * (double)g.N;
   for (int bh = 0; bh < g.BH; ++bh) {
     const int64_t* h = &s[(size_t)bh * 16];
-    out->routed_pairs += h[ST_ROUTED_PAIRS];
-    out->exec_pairs += h[ST_ROUTED_PAIRS] + h[ST_NPROBES] * (int64_t)g.N;
-    out->forced_pairs += h[ST_FORCED_PAIRS];
+    // every query head sharing the K/V head evaluates the plan's pairs
+    out->routed_pairs += h[ST_ROUTED_PAIRS] * g.G;
+    out->exec_pairs += (h[ST_ROUTED_PAIRS] + h[ST_NPROBES] * (int64_t)g.N) * g.G;
+    out->forced_pairs += h[ST_FORCED_PAIRS] * g.G;
     out->routed_cells += (int32_t)h[ST_ROUTED_CELLS];
     out->forced_cells += (int32_t)h[ST_FORCED_CELLS];
     out->nonempty_q_groups += (int32_t)h[ST_NE_Q];
     out->nonempty_kv_groups += (int32_t)h[ST_NE_K];
-    out->n_probes += (int32_t)h[ST_NPROBES];
+    out->n_probes += (int32_t)h[ST_NPROBES] * g.G;
     out->kmeans_iters_kv = std::max(out->kmeans_iters_kv, (int32_t)h[ST_ITK]);
     out->kmeans_iters_q = std::max(out->kmeans_iters_q, (int32_t)h[ST_ITQ]);
     out->status_flags |= (int32_t)h[ST_FLAGS];
@@ -452,11 +488,13 @@ sparsepr_status sparsepr_plan_export(sparsepr_plan_t plan, int32_t bh, sparsepr_
                                      void* stream) {
   if (!plan || !out) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan and out must not be NULL");
   const Geom& g = plan->g;
-  if (bh < 0 || bh >= g.BH) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "bh out of range");
+  if (bh < 0 || bh >= g.B * g.H) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "bh out of range");
   sparsepr_status st = hip_check(hipStreamSynchronize((hipStream_t)stream), "hipStreamSynchronize");
   if (st != SPARSEPR_OK) return st;
+  // query head bh = b*H + h uses the plan of K/V head b*Hkv + h/G
+  const int hq = bh % g.H;
   Work h;
-  bind(g, &h, plan->L, plan->base, bh);
+  bind(g, &h, plan->L, plan->base, (bh / g.H) * g.Hkv + hq / g.G, hq % g.G);
   int32_t np = 0;
   st = hip_check(hipMemcpy(&np, h.nprobes, 4, hipMemcpyDeviceToHost),
                  ("export n_probes" + ptrs(&np, h.nprobes, 4)).c_str());
@@ -526,7 +564,7 @@ sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const spa
                                      void* stream) {
   if (!plan || !in) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "plan and in must not be NULL");
   const Geom& g = plan->g;
-  if (bh < 0 || bh >= g.BH) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "bh out of range");
+  if (bh < 0 || bh >= g.B * g.H) return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "bh out of range");
   if (!in->labels_q || !in->labels_kv || !in->routes || (in->n_probes > 0 && !in->probes))
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "labels_q, labels_kv, routes and probes are required");
   if (in->n_probes < 0 || in->n_probes > g.M)
@@ -559,7 +597,7 @@ sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const spa
   sparsepr_status st = hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
   if (st != SPARSEPR_OK) return st;
   Work h;
-  bind(g, &h, plan->L, plan->base, bh);
+  bind(g, &h, plan->L, plan->base, (bh / g.H) * g.Hkv + (bh % g.H) / g.G);
   const int32_t np = in->n_probes;
   struct Cp {
     void* dst;
@@ -580,7 +618,8 @@ sparsepr_status sparsepr_plan_import(sparsepr_plan_t plan, int32_t bh, const spa
   }
   Geom g1 = g;
   g1.B = 1;
-  g1.H = 1;
+  g1.H = g.G;
+  g1.Hkv = 1;
   g1.BH = 1;
   (void)hipGetLastError();
   launch_rebuild(g1, h, 0, s);

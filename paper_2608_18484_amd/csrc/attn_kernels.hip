@@ -245,12 +245,12 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   } else {
     bh = (MODE == MODE_PROBE) ? blockIdx.z : blockIdx.y;
     if (!get_work<MODE>(g, A, bh, w)) return;
-    const int64_t base = head_base(g, bh);
+    const int64_t base = kv_base(g, bh);
     Kp = (const uint16_t*)A.k + base;
     Vp = (const uint16_t*)A.v + base;
   }
   const int64_t ksn = (MODE == MODE_SPARSE) ? D : g.sn;  // row stride of Kp/Vp
-  const int64_t qbase = head_base(g, bh);
+  const int64_t qbase = q_base(g, bh, g.gq);  // also the output's, in MODE_DENSE
   const uint16_t* Qp = (const uint16_t*)A.q + qbase;
 
   // query row of this lane and its B operands
@@ -563,7 +563,7 @@ __global__ __launch_bounds__(256) void k_permute_kv(Geom g, const void* k, const
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int p = blockIdx.x * RPB + tid / CH, c = tid % CH;
   if (p >= g.N) return;
-  const int64_t base = head_base(g, bh);
+  const int64_t base = kv_base(g, bh);
   const int src = permk[(size_t)bh * g.N + p];
   const uint4 kv = *(const uint4*)((const uint16_t*)k + base + (int64_t)src * g.sn + c * 8);
   const uint4 vv = *(const uint4*)((const uint16_t*)v + base + (int64_t)src * g.sn + c * 8);
@@ -582,10 +582,10 @@ __global__ __launch_bounds__(64) void k_attn_f32(Geom g, AttnArgs A) {
   Work1 w;
   if (!get_work<MODE>(g, A, bh, w)) return;
   const int tid = threadIdx.x;
-  const int64_t base = head_base(g, bh);
+  const int64_t base = kv_base(g, bh), qbase = q_base(g, bh, g.gq);
   const float* Kp = (const float*)A.k + base;
   const float* Vp = (const float*)A.v + base;
-  const float* Qp = (const float*)A.q + base;
+  const float* Qp = (const float*)A.q + qbase;
   const bool qvalid = tid < w.nrows;
   const int qrow = qvalid ? row_of<MODE>(g, A, bh, w, tid) : 0;
   float qv[D], o[D];
@@ -654,7 +654,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(Geom g, AttnArgs A) {
     float* dst = A.osp + ((size_t)bh * g.N + qrow) * D;
     for (int c = 0; c < D; ++c) dst[c] = o[c] / l_run;
   } else {
-    float* dst = (float*)A.out + base + (int64_t)qrow * g.sn;
+    float* dst = (float*)A.out + qbase + (int64_t)qrow * g.sn;
     for (int c = 0; c < D; ++c) dst[c] = o[c] / l_run;
   }
 }
@@ -817,11 +817,13 @@ __global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
 // Psi = leading r eigenvectors of H with sigma > 1e-6 sigma_1 (Jacobi in
 // LDS); then (xbar^T W xbar + lambda I) Y = xbar^T W (Rbar Psi) by Cholesky,
 // so Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
-template <int D>
+// T is the Jacobi's precision.  Double A and V of a 128 x 128 problem do not
+// both fit in LDS; V (VG) then lives in the head's global scratch.
+template <int D, typename T>
 __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
-  using T = typename std::conditional<D <= 64, double, float>::type;
   constexpr int LD = D + 1;
-  constexpr size_t JAC = 2 * D * LD * sizeof(T), CHOL = (size_t)D * D * sizeof(double);
+  constexpr bool VG = 2 * D * LD * sizeof(T) > 140 * 1024;
+  constexpr size_t JAC = (VG ? 1 : 2) * D * LD * sizeof(T), CHOL = (size_t)D * D * sizeof(double);
   __shared__ __attribute__((aligned(16))) unsigned char smem[JAC > CHOL ? JAC : CHOL];
   __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
@@ -836,10 +838,10 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   const double* H = w.fitgram + ((size_t)bh * 2 + 0) * D * D;
   const double* Sg = w.fitgram + ((size_t)bh * 2 + 1) * D * D;
   T* Am = (T*)smem;
-  T* Vm = Am + D * LD;
+  T* Vm = VG ? (T*)(w.fitvec + (size_t)bh * D * LD) : Am + D * LD;
   for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
   __syncthreads();
-  jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag);
+  jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
   if (tid < D) {
     const T li = Am[tid * LD + tid];
     int rank = 0;
@@ -1012,7 +1014,7 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
     }
   }
   if (!valid) return;
-  const int64_t dst = head_base(g, bh) + (int64_t)row * g.sn + qtr * CW;
+  const int64_t dst = q_base(g, bh, g.gq) + (int64_t)row * g.sn + qtr * CW;
   float o[CW];
 #pragma unroll
   for (int c = 0; c < CW; ++c) o[c] = text ? x[c] : x[c] + fv[2 * D + qtr * CW + c] + acc[c];
@@ -1043,7 +1045,7 @@ __global__ __launch_bounds__(128) void k_probe_scatter(Geom g, Work w, void* out
   if (p >= w.nprobes[bh] || c >= g.dv) return;
   const int row = w.probes[(size_t)bh * g.M + p];
   const float v = w.odp[((size_t)bh * g.M + p) * g.dv + c];
-  const int64_t idx = head_base(g, bh) + (int64_t)row * g.sn + c;
+  const int64_t idx = q_base(g, bh, g.gq) + (int64_t)row * g.sn + c;
   if (g.bf16) {
     const __bf16 b = (__bf16)v;
     ((uint16_t*)out)[idx] = __builtin_bit_cast(uint16_t, b);
@@ -1082,56 +1084,78 @@ static AttnArgs make_args(const Work* w, const void* q, const void* k, const voi
 }
 
 template <int D>
-static void attend_d(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+static void attend_d(const Geom& g, const Work* wq, const void* q, const void* k, const void* v,
                      void* out, hipStream_t s, hipEvent_t* ev) {
-  const AttnArgs a = make_args(&w, q, k, v, out);
   const dim3 gp((g.M + 63) / 64, g.nsplit, g.BH);
+  // query head j of every K/V head: its own Geom (Q and output rows) and
+  // workspace view (attend outputs); the plan and the group-major K/V are shared
+  auto gj = [&](int j) {
+    Geom h = g;
+    h.gq = j;
+    return h;
+  };
   if (g.bf16) {
     constexpr int CH = D / 8;
     k_permute_kv<D><<<dim3((g.N + 256 / CH - 1) / (256 / CH), g.BH), 256, 0, s>>>(
-        g, k, v, w.permk, w.kperm, w.vperm);
+        g, k, v, wq[0].permk, wq[0].kperm, wq[0].vperm);
   }
   if (ev) (void)hipEventRecord(ev[0], s);
-  if (g.bf16) {
-    // one launch per key segment, so that all blocks in flight read the same
-    // slice of K/V and it stays in L2
-    for (int sg = 0; sg < g.nseg; ++sg) {
-      AttnArgs as = a;
-      as.seg_lo = (int)((int64_t)g.N * sg / g.nseg);
-      as.seg_hi = (int)((int64_t)g.N * (sg + 1) / g.nseg);
-      as.seg_first = sg == 0;
-      as.seg_last = sg == g.nseg - 1;
-      as.heads_per_xcd = g.BH % 8 == 0;
-      const dim3 grid = as.heads_per_xcd ? dim3(8 * g.nchunk_max, g.BH / 8)
-                                         : dim3(8 * g.nchunk_per_xcd, g.BH);
-      k_attn_mfma<D, MODE_SPARSE><<<grid, 128, 0, s>>>(g, as);
+  for (int j = 0; j < g.G; ++j) {
+    const AttnArgs a = make_args(&wq[j], q, k, v, out);
+    if (g.bf16) {
+      // one launch per key segment, so that all blocks in flight read the same
+      // slice of K/V and it stays in L2
+      for (int sg = 0; sg < g.nseg; ++sg) {
+        AttnArgs as = a;
+        as.seg_lo = (int)((int64_t)g.N * sg / g.nseg);
+        as.seg_hi = (int)((int64_t)g.N * (sg + 1) / g.nseg);
+        as.seg_first = sg == 0;
+        as.seg_last = sg == g.nseg - 1;
+        as.heads_per_xcd = g.BH % 8 == 0;
+        const dim3 grid = as.heads_per_xcd ? dim3(8 * g.nchunk_max, g.BH / 8)
+                                           : dim3(8 * g.nchunk_per_xcd, g.BH);
+        k_attn_mfma<D, MODE_SPARSE><<<grid, 128, 0, s>>>(gj(j), as);
+      }
+    } else {
+      k_attn_f32<D, MODE_SPARSE><<<dim3(g.nchunk_max, g.BH), 64, 0, s>>>(gj(j), a);
     }
-  } else
-    k_attn_f32<D, MODE_SPARSE><<<dim3(g.nchunk_max, g.BH), 64, 0, s>>>(g, a);
+  }
   if (ev) (void)hipEventRecord(ev[1], s);
   if (g.M > 0) {
-    if (g.bf16)
-      k_attn_mfma<D, MODE_PROBE><<<gp, 128, 0, s>>>(g, a);
-    else
-      k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(g, a);
-    k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w.part, w.nprobes, w.odp);
+    for (int j = 0; j < g.G; ++j) {
+      const AttnArgs a = make_args(&wq[j], q, k, v, out);
+      if (g.bf16)
+        k_attn_mfma<D, MODE_PROBE><<<gp, 128, 0, s>>>(gj(j), a);
+      else
+        k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(gj(j), a);
+      k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, wq[j].part, wq[j].nprobes, wq[j].odp);
+    }
   }
   if (ev) (void)hipEventRecord(ev[2], s);
-  k_fit_prep<D><<<g.BH, 256, 0, s>>>(g, w);
-  k_fit_gram<D><<<dim3((D / 32) * (D / 32), 2, g.BH), 256, 0, s>>>(g, w);
-  k_fit_solve<D><<<g.BH, 1024, 0, s>>>(g, w);
+  for (int j = 0; j < g.G; ++j) {
+    k_fit_prep<D><<<g.BH, 256, 0, s>>>(g, wq[j]);
+    k_fit_gram<D><<<dim3((D / 32) * (D / 32), 2, g.BH), 256, 0, s>>>(g, wq[j]);
+    // float inputs (whose outputs are held to float rounding) get the
+    // double solve; bf16 inputs the float one
+    if (D <= 64 || !g.bf16)
+      k_fit_solve<D, double><<<g.BH, 1024, 0, s>>>(g, wq[j]);
+    else
+      k_fit_solve<D, float><<<g.BH, 1024, 0, s>>>(g, wq[j]);
+  }
   if (ev) (void)hipEventRecord(ev[3], s);
-  k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(g, w, out);
-  if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(g, w, out);
+  for (int j = 0; j < g.G; ++j) {
+    k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(gj(j), wq[j], out);
+    if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(gj(j), wq[j], out);
+  }
   if (ev) (void)hipEventRecord(ev[4], s);
 }
 
-void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+void launch_attend(const Geom& g, const Work* wq, const void* q, const void* k, const void* v,
                    void* out, hipStream_t s, hipEvent_t* ev) {
   if (g.d == 64)
-    attend_d<64>(g, w, q, k, v, out, s, ev);
+    attend_d<64>(g, wq, q, k, v, out, s, ev);
   else
-    attend_d<128>(g, w, q, k, v, out, s, ev);
+    attend_d<128>(g, wq, q, k, v, out, s, ev);
 }
 
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
@@ -1139,16 +1163,20 @@ void launch_dense(const Geom& g, const void* q, const void* k, const void* v, vo
   (void)part;
   const AttnArgs a = make_args(nullptr, q, k, v, out);
   const dim3 gd((g.N + 63) / 64, g.BH);
-  if (g.d == 64) {
-    if (g.bf16)
-      k_attn_mfma<64, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
-    else
-      k_attn_f32<64, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
-  } else {
-    if (g.bf16)
-      k_attn_mfma<128, MODE_DENSE><<<gd, 128, 0, s>>>(g, a);
-    else
-      k_attn_f32<128, MODE_DENSE><<<gd, 64, 0, s>>>(g, a);
+  for (int j = 0; j < g.G; ++j) {  // every query head of each K/V head
+    Geom h = g;
+    h.gq = j;
+    if (g.d == 64) {
+      if (g.bf16)
+        k_attn_mfma<64, MODE_DENSE><<<gd, 128, 0, s>>>(h, a);
+      else
+        k_attn_f32<64, MODE_DENSE><<<gd, 64, 0, s>>>(h, a);
+    } else {
+      if (g.bf16)
+        k_attn_mfma<128, MODE_DENSE><<<gd, 128, 0, s>>>(h, a);
+      else
+        k_attn_f32<128, MODE_DENSE><<<gd, 64, 0, s>>>(h, a);
+    }
   }
 }
 

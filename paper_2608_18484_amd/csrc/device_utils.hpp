@@ -16,10 +16,17 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t u) {
   return __uint_as_float(((uint32_t)u) << 16);
 }
 
-// Element offset of head bh = b*H + h in a [B, H, N, d] tensor.
-__device__ __forceinline__ int64_t head_base(const Geom& g, int bh) {
-  const int b = bh / g.H, h = bh - b * g.H;
-  return (int64_t)b * g.sb + (int64_t)h * g.sh;
+// Element offset of K/V head bh = b*Hkv + h in the [B, Hkv, N, d] K and V.
+__device__ __forceinline__ int64_t kv_base(const Geom& g, int bh) {
+  const int b = bh / g.Hkv, h = bh - b * g.Hkv;
+  return (int64_t)b * g.kvsb + (int64_t)h * g.kvsh;
+}
+
+// Element offset, in the [B, H, N, d] Q and output, of query head j < G of
+// K/V head bh: query heads h*G .. h*G + G - 1 share K/V head h.
+__device__ __forceinline__ int64_t q_base(const Geom& g, int bh, int j) {
+  const int b = bh / g.Hkv, h = bh - b * g.Hkv;
+  return (int64_t)b * g.sb + (int64_t)(h * g.G + j) * g.sh;
 }
 
 // Load element `idx` of a bf16 or fp32 tensor as float.

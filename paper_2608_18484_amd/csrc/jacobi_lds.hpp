@@ -9,6 +9,8 @@
 // NT a multiple of D/2 every thread keeps the same column pair j for the
 // whole step, so its rotation is read from LDS once.  On return A's diagonal
 // holds the eigenvalues and V's columns the eigenvectors (row stride D + 1).
+// A is in LDS; V is in LDS or, when both do not fit, in the block's own
+// global scratch (the block barriers order those accesses as well).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -22,7 +24,7 @@ struct alignas(16) JacobiRot {
 };
 
 template <int D, typename T, int NT>
-__device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
+__device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop) {
   constexpr int LD = D + 1, P = D / 2;
   static_assert(NT % P == 0 && (P * P) % NT == 0 && (D * P) % NT == 0, "thread mapping");
   const int tid = threadIdx.x;
@@ -108,10 +110,9 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
       }
       __syncthreads();
     }
-    // Stop once the off-diagonal part is small relative to the whole matrix:
-    // convergence is quadratic, and in float the eigenvectors reach their
-    // rounding floor about when the relative off-diagonal norm drops below
-    // 1e-4 (the remaining sweeps would rotate noise).
+    // Stop once the off-diagonal norm falls below `stop` times the matrix
+    // norm (convergence is quadratic, so one more sweep takes a relative
+    // off-diagonal norm of 1e-4 to the float rounding floor).
     {
       __shared__ T red[2][NT / 64];
       T off = 0, tot = 0;
@@ -137,7 +138,6 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag) {
           o2 += red[0][w];
           t2 += red[1][w];
         }
-        const T stop = sizeof(T) == 8 ? T(1e-12) : T(1e-4);
         if (o2 <= stop * stop * t2) *flag = 0;
       }
     }

@@ -35,7 +35,10 @@ __global__ void k_plan_init(Geom g, Work w) {
 
 // ---------------------------------------------------------------------------
 // Key-response metric M_K = Q_s^T Q_s / M_s over the strided query sample
-// s_i = floor(i * n_v / M_s) (Sec. 4.1; App. B.1 eq. app_key_metric).
+// s_i = floor(i * n_v / M_s) (Sec. 4.1; App. B.1 eq. app_key_metric).  With
+// grouped-query attention the sample is pooled over the G query heads that
+// share the K/V head (App. B.1 builds M_K per K/V head): the G per-head
+// metrics are averaged.
 // ---------------------------------------------------------------------------
 
 template <int D>
@@ -44,33 +47,35 @@ __global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, doubl
   constexpr int SB = 32;
   __shared__ float qs[SB][D];
   const int bh = blockIdx.x, tid = threadIdx.x;
-  const int64_t base = head_base(g, bh);
   const int e0 = tid * ENT, ra = e0 / D, cb = e0 % D;
   double acc[ENT];
 #pragma unroll
   for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
-  for (int s0 = 0; s0 < g.Ms; s0 += SB) {
-    for (int t = tid; t < SB * D; t += 256) {
-      const int i = s0 + t / D, c = t % D;
-      float v = 0.f;
-      if (i < g.Ms) {
-        const int64_t row = g.ntext + ((int64_t)i * g.NV) / g.Ms;
-        v = load_x(q, g.bf16, base + row * g.sn + c);
+  for (int j = 0; j < g.G; ++j) {
+    const int64_t base = q_base(g, bh, j);
+    for (int s0 = 0; s0 < g.Ms; s0 += SB) {
+      for (int t = tid; t < SB * D; t += 256) {
+        const int i = s0 + t / D, c = t % D;
+        float v = 0.f;
+        if (i < g.Ms) {
+          const int64_t row = g.ntext + ((int64_t)i * g.NV) / g.Ms;
+          v = load_x(q, g.bf16, base + row * g.sn + c);
+        }
+        qs[t / D][c] = v;
       }
-      qs[t / D][c] = v;
-    }
-    __syncthreads();
-    const int cnt = min(SB, g.Ms - s0);
-    for (int i = 0; i < cnt; ++i) {
-      const double a = qs[i][ra];
+      __syncthreads();
+      const int cnt = min(SB, g.Ms - s0);
+      for (int i = 0; i < cnt; ++i) {
+        const double a = qs[i][ra];
 #pragma unroll
-      for (int e = 0; e < ENT; ++e) acc[e] += a * (double)qs[i][cb + e];
+        for (int e = 0; e < ENT; ++e) acc[e] += a * (double)qs[i][cb + e];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   double* out = gram + (size_t)bh * D * D;
 #pragma unroll
-  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / (double)g.Ms;
+  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / ((double)g.Ms * (double)g.G);
 }
 
 // Sort the eigenvalues on A's diagonal in descending order (ties by index):
@@ -110,7 +115,10 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   const double* G = gram + (size_t)bh * D * D;
   for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
   __syncthreads();
-  jacobi_eig_lds<D, T, 1024>(A, V, rot, &flag);
+  // In float the basis reaches its rounding floor at a relative off-diagonal
+  // norm of about 1e-4 (measured on the long-video key metric: the weighted
+  // projector then differs from a double solve by 2.7e-5).
+  jacobi_eig_lds<D, T, 1024>(A, V, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
   eig_order<D, T>(A, order);
   const double l1 = A[order[0] * LD + order[0]];
   if (tid < D) {
@@ -137,7 +145,10 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 // Response coordinates phi = F^T x (eq. key_response_feature), optionally
 // divided by max(RMS, eps) (eq. query_response_feature).  64 rows per block;
 // thread (ty, tx) computes rows ty + 16u (u < 4) x columns [tx*CPT, tx*CPT +
-// CPT), so each LDS read of F feeds four rows.
+// CPT), so each LDS read of F feeds four rows.  Keys (rms = 0) come from the
+// K/V head; queries (rms = 1) from its G query heads, whose normalised
+// coordinates are averaged (grouped-query attention shares one query
+// partition per K/V head; G = 1 is the single-head case).
 // ---------------------------------------------------------------------------
 
 template <int D, int MAXR>
@@ -158,64 +169,78 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
       fs[i] = c < R ? Fh[k * R + c] : 0.f;
     }
   }
-  const int64_t base = head_base(g, bh);
-  for (int i = tid; i < ROWS * D / 8; i += 256) {
-    const int rr = i / (D / 8), c8 = i % (D / 8);
-    const int row = r0 + rr;
-    float v[8];
-    if (row < g.NV) {
-      const int64_t off = base + (int64_t)(g.ntext + row) * g.sn + c8 * 8;
-      if (g.bf16) {
-        const uint4 u = *(const uint4*)((const uint16_t*)x + off);
-        const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[2 * e] = __uint_as_float(wds[e] << 16);
-          v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
-        }
-      } else {
-        const float4 u0 = *(const float4*)((const float*)x + off);
-        const float4 u1 = *(const float4*)((const float*)x + off + 4);
-        v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
-        v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
-  }
-  __syncthreads();
   const int ty = tid >> 4, tx = tid & 15;
-  float acc[4][CPT];
+  const int nsrc = rms ? g.G : 1;
+  float pooled[4][CPT];
 #pragma unroll
   for (int u = 0; u < 4; ++u)
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) acc[u][c] = 0.f;
-  for (int k = 0; k < D; ++k) {
-    float xv[4], fv[CPT];
+    for (int c = 0; c < CPT; ++c) pooled[u][c] = 0.f;
+  for (int j = 0; j < nsrc; ++j) {
+    const int64_t base = rms ? q_base(g, bh, j) : kv_base(g, bh);
+    if (j > 0) __syncthreads();
+    for (int i = tid; i < ROWS * D / 8; i += 256) {
+      const int rr = i / (D / 8), c8 = i % (D / 8);
+      const int row = r0 + rr;
+      float v[8];
+      if (row < g.NV) {
+        const int64_t off = base + (int64_t)(g.ntext + row) * g.sn + c8 * 8;
+        if (g.bf16) {
+          const uint4 u = *(const uint4*)((const uint16_t*)x + off);
+          const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) xv[u] = xs[ty + 16 * u][k];
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] = __uint_as_float(wds[e] << 16);
+            v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+          }
+        } else {
+          const float4 u0 = *(const float4*)((const float*)x + off);
+          const float4 u1 = *(const float4*)((const float*)x + off + 4);
+          v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
+          v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
+        }
+      } else {
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) fv[c] = fs[k * MAXR + tx * CPT + c];
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
+    }
+    __syncthreads();
+    float acc[4][CPT];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) acc[u][c] = fmaf(xv[u], fv[c], acc[u][c]);
+      for (int c = 0; c < CPT; ++c) acc[u][c] = 0.f;
+    for (int k = 0; k < D; ++k) {
+      float xv[4], fv[CPT];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) xv[u] = xs[ty + 16 * u][k];
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) fv[c] = fs[k * MAXR + tx * CPT + c];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) acc[u][c] = fmaf(xv[u], fv[c], acc[u][c]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float den = 1.f;
+      if (rms) {
+        float ss = 0.f;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) ss = fmaf(acc[u][c], acc[u][c], ss);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
+        den = fmaxf(sqrtf(ss / (float)R), eps);
+      }
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) pooled[u][c] += acc[u][c] / den;
+    }
   }
   bool bad = false;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    float den = 1.f;
-    if (rms) {
-      float ss = 0.f;
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) ss = fmaf(acc[u][c], acc[u][c], ss);
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
-      den = fmaxf(sqrtf(ss / (float)R), eps);
-    }
     const int row = r0 + ty + 16 * u;
     // the k-means operands of the same coordinates: bf16 hi + lo halves
     // (zero-padded to RP) and the row norm (its error-bound input)
@@ -224,7 +249,7 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int col = tx * CPT + c;
-      vv[c] = col < R ? acc[u][c] / den : 0.f;
+      vv[c] = col < R ? (nsrc == 1 ? pooled[u][c] : pooled[u][c] / (float)nsrc) : 0.f;
       ssq = fmaf(vv[c], vv[c], ssq);
     }
 #pragma unroll
@@ -715,14 +740,16 @@ __global__ void k_prefix_group(KmArgs a) {
 
 __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const int32_t* perm,
                                                     const int32_t* off, int C, int offstride,
-                                                    float* mean) {
+                                                    float* mean, int query) {
   // One wave per group; lane l owns channels 2l and 2l + 1.  The members'
   // rows are fetched 64 at a time (lane i holds member m0 + i), their values
-  // loaded eight at a time and added in ascending member order.
+  // loaded eight at a time and added in ascending member order.  Key means
+  // come from the K/V head; query means (`query`) are pooled over its G query
+  // heads, head by head.
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + wv;
   if (b >= C) return;
-  const int64_t base = head_base(g, bh);
+  const int nsrc = query ? g.G : 1;
   const int32_t* o = off + (size_t)bh * offstride;
   const int32_t* p = perm + (size_t)bh * g.N;
   const int s0 = o[b], s1 = o[b + 1];
@@ -731,7 +758,7 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
   const int c = 2 * lane;
   const bool cin = c < g.d;
   double s0d = 0.0, s1d = 0.0;
-  auto ld2 = [&](int row) -> float2 {
+  auto ld2 = [&](int64_t base, int row) -> float2 {
     if (!cin) return make_float2(0.f, 0.f);
     const int64_t idx = base + (int64_t)row * g.sn + c;
     if (g.bf16) {
@@ -740,28 +767,31 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
     }
     return *(const float2*)((const float*)x + idx);
   };
-  for (int m0 = s0; m0 < s1; m0 += 64) {
-    const int cm = min(64, s1 - m0);
-    const int pv = lane < cm ? p[m0 + lane] : 0;
-    int i = 0;
-    for (; i + 8 <= cm; i += 8) {
-      float2 v[8];
+  for (int j = 0; j < nsrc; ++j) {
+    const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
+    for (int m0 = s0; m0 < s1; m0 += 64) {
+      const int cm = min(64, s1 - m0);
+      const int pv = lane < cm ? p[m0 + lane] : 0;
+      int i = 0;
+      for (; i + 8 <= cm; i += 8) {
+        float2 v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = ld2(__builtin_amdgcn_readlane(pv, i + u));
+        for (int u = 0; u < 8; ++u) v[u] = ld2(base, __builtin_amdgcn_readlane(pv, i + u));
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        s0d += (double)v[u].x;
-        s1d += (double)v[u].y;
+        for (int u = 0; u < 8; ++u) {
+          s0d += (double)v[u].x;
+          s1d += (double)v[u].y;
+        }
       }
-    }
-    for (; i < cm; ++i) {
-      const float2 v = ld2(__builtin_amdgcn_readlane(pv, i));
-      s0d += (double)v.x;
-      s1d += (double)v.y;
+      for (; i < cm; ++i) {
+        const float2 v = ld2(base, __builtin_amdgcn_readlane(pv, i));
+        s0d += (double)v.x;
+        s1d += (double)v.y;
+      }
     }
   }
   if (!cin) return;
-  const double n = (double)(s1 - s0);
+  const double n = (double)(s1 - s0) * (double)nsrc;
   float* dst = mean + ((size_t)bh * C + b) * g.d + c;
   dst[0] = (s1 > s0) ? (float)(s0d / n) : 0.f;
   dst[1] = (s1 > s0) ? (float)(s1d / n) : 0.f;
@@ -1436,7 +1466,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   run_kmeans(g, ak, s, warm);
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
-                                                         w.kbar);
+                                                         w.kbar, 0);
   k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
   k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
   project<D>(g, w, q, w.fq, g.rq, 1, g.eps_q, w.phiq, s);
@@ -1445,7 +1475,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
   run_kmeans(g, aq, s, warm);
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
-                                                         w.qbar);
+                                                         w.qbar, 1);
   // Routing (Sec. 4.3)
   k_route_prio<D><<<dim3((g.CQ + 63) / 64, BH), 256, 0, s>>>(w.qbar, w.kbar, g, w.offq, w.offk,
                                                              w.prio, w.forced);

@@ -24,7 +24,9 @@ constexpr int kSelBins = 256;
 constexpr int kSelPasses = 8;
 
 struct Geom {
-  int B, H, BH;           // batch, heads, batch*heads
+  int B, H, BH;           // batch, query heads, batch * K/V heads (one plan each)
+  int Hkv, G;             // K/V heads; query heads per K/V head (H = Hkv * G)
+  int gq;                 // attend: which query head of each K/V head's group
   int N, NV, ntext;       // rows, video rows, dense-prefix rows
   int d, dv;              // head dims (equal)
   int rk, rq;             // response ranks, clamped to d
@@ -37,7 +39,8 @@ struct Geom {
   int M;                  // probes per head, min(n_probes, NV)
   int r;                  // residual rank
   int bf16;               // 1: bf16 tensors, 0: fp32
-  int64_t sb, sh, sn;     // element strides of Q, K, V, O
+  int64_t sb, sh, sn;     // element strides of Q and O (sn also of K and V)
+  int64_t kvsb, kvsh;     // batch and head strides of K and V
   float rho, ridge, eps_q, eps_x;
   int64_t budget;         // video x video pair budget after the probe reservation
   int nchunk_max;         // attention work items per head (upper bound)
@@ -107,6 +110,7 @@ struct Work {
   float* fitpsi;      // [BH][dv][r]
   double* fitscr;     // [BH][2*M*dv + M*r + dv*r + M] fit scratch
   double* fitgram;    // [BH][2][dv][dv] Rbar^T W Rbar and xbar^T W xbar + lambda I
+  double* fitvec;     // [BH][dv][dv+1] eigenvectors of a double fit solve kept out of LDS
   int64_t* stats;     // [BH][16]
 };
 
@@ -135,8 +139,10 @@ void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s);
 // ---- attend kernels -----------------------------------------------------
 // Optional events recorded between the phases of attend (null = none):
 // ev[0] before the sparse attention, ev[1] after it, ev[2] after the probe
-// rows, ev[3] after the fit, ev[4] after the correction.
-void launch_attend(const Geom& g, const Work& w, const void* q, const void* k, const void* v,
+// rows, ev[3] after the fit, ev[4] after the correction.  wq[j] (j < G) is the
+// workspace view holding the attend outputs of query head j of every K/V
+// head; each phase runs for the G query heads in turn.
+void launch_attend(const Geom& g, const Work* wq, const void* q, const void* k, const void* v,
                    void* out, hipStream_t s, hipEvent_t* ev = nullptr);
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
                   float* part, hipStream_t s);

@@ -25,7 +25,9 @@ class Shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("n_q", ctypes.c_int32),
                 ("n_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("d_v", ctypes.c_int32),
                 ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
-                ("stride_n", ctypes.c_int64), ("dtype", ctypes.c_int32)]
+                ("stride_n", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("heads_kv", ctypes.c_int32), ("kv_stride_b", ctypes.c_int64),
+                ("kv_stride_h", ctypes.c_int64)]
 
 
 class Params(ctypes.Structure):
@@ -117,15 +119,23 @@ def default_params(**kw) -> Params:
     return p
 
 
-def shape_of(t, dtype=None) -> Shape:
-    """Shape struct for a [B, H, N, d] torch tensor (last dim contiguous)."""
+def shape_of(t, dtype=None, kv=None) -> Shape:
+    """Shape struct for a [B, H, N, d] torch tensor (last dim contiguous).
+    `kv`: the [B, H_kv, N, d] K tensor (V must share its strides) for
+    grouped-query attention, where H_kv divides H."""
     import torch
     b, h, n, d = t.shape
     sb, sh, sn, sd = t.stride()
     if sd != 1:
         raise ValueError("last dimension must be contiguous")
     dt = dtype if dtype is not None else (BF16 if t.dtype == torch.bfloat16 else F32)
-    return Shape(b, h, n, n, d, d, sb, sh, sn, dt)
+    hkv, ksb, ksh = 0, 0, 0
+    if kv is not None:
+        bk, hkv, nk, dk = kv.shape
+        ksb, ksh, ksn, ksd = kv.stride()
+        if (bk, nk, dk) != (b, n, d) or ksn != sn or ksd != 1:
+            raise ValueError("K/V must be [B, H_kv, N, d] with Q's row stride")
+    return Shape(b, h, n, n, d, d, sb, sh, sn, dt, hkv, ksb, ksh)
 
 
 def _ptr(t):
@@ -214,7 +224,8 @@ class SparsePR:
         }
 
     def export(self, bh: int = 0, fields=None, stream=None) -> dict:
-        """Copy head bh of the plan (and attend outputs) to numpy arrays."""
+        """Copy the plan used by query head bh (and that head's attend outputs)
+        to numpy arrays."""
         sizes = self._sizes()
         want = [name for name, kind in HOST_FIELDS if kind is not None and
                 (fields is None or name in fields)]
@@ -249,7 +260,8 @@ class SparsePR:
         return out
 
     def import_plan(self, bh: int, labels_q, labels_kv, routes, probes, stream=None):
-        """Replace head bh's plan by host arrays (labels, route matrix, probes)."""
+        """Replace the plan used by query head bh (shared by its K/V head's
+        group) by host arrays (labels, route matrix, probes)."""
         lq = np.ascontiguousarray(labels_q, np.int32)
         lk = np.ascontiguousarray(labels_kv, np.int32)
         z = np.ascontiguousarray(routes, np.uint8)

@@ -79,6 +79,10 @@ def test_workspace_size_ok_and_monotone():
     assert st == 0 and n1 > 0
     st, n2, _ = _ws(tiny_shape(heads=4, stride_b=4 * 65536), S.default_params(n_probes=32))
     assert st == 0 and n2 > 3 * n1
+    # grouped-query attention: plans per K/V head, attend outputs per query head
+    st, n3, _ = _ws(tiny_shape(heads=4, stride_b=4 * 65536, heads_kv=2, kv_stride_b=2 * 65536,
+                               kv_stride_h=65536), S.default_params(n_probes=32))
+    assert st == 0 and n1 < n3 < n2
 
 
 @pytest.mark.parametrize("shape_kw,param_kw,status,needle", [
@@ -97,6 +101,11 @@ def test_workspace_size_ok_and_monotone():
     ({}, dict(ridge=-1.0), 1, "ridge"),
     ({}, dict(n_dense_prefix=1024), 1, "n_dense_prefix"),
     ({}, dict(kmeans_iters=0), 1, "kmeans_iters"),
+    (dict(heads=4, stride_b=4 * 65536, heads_kv=3), {}, 1, "heads_kv"),
+    (dict(heads=4, stride_b=4 * 65536, heads_kv=-1), {}, 1, "heads_kv"),
+    (dict(heads=4, stride_b=4 * 65536, heads_kv=2), {}, 1, "kv_stride"),
+    (dict(heads=4, stride_b=4 * 65536, heads_kv=2, kv_stride_b=2 * 65536, kv_stride_h=65540), {}, 2,
+     "multiples of 8"),
 ])
 def test_validation_errors(shape_kw, param_kw, status, needle):
     st, _, msg = _ws(tiny_shape(**shape_kw), S.default_params(**param_kw))

@@ -291,3 +291,74 @@ def test_warm_started_kmeans(orc, ntext):
         ref, _ = _replay(orc, r2, ex, 0, h)
         err = rel_l2(outn[0, h], ref)
         assert err < 2e-2, (h, err)
+
+
+def _run_gqa(wl, g):
+    """Grouped-query attention: query heads h*g .. h*g+g-1 share K/V head h
+    (K and V are every g-th generated head)."""
+    from paper_2608_18484_amd import sparsepr as S
+    q, k, v, _ = W.make_inputs(wl)
+    k, v = np.ascontiguousarray(k[:, ::g]), np.ascontiguousarray(v[:, ::g])
+    tq, tk, tv = to_device(q, k, v, wl.dtype)
+    p = params_for(wl)
+    op = S.SparsePR(S.shape_of(tq, kv=tk), p)
+    out = torch.empty_like(tq)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    torch.cuda.synchronize()
+    return dict(q=q, k=k, v=v, p=p, op=op, out=out.float().cpu().numpy())
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("f32", 128), ("bf16", 128)])
+def test_gqa_pooled_plan_and_outputs(orc, dtype, d):
+    g, hkv = 2, 2
+    wl = medium(heads=g * hkv, dtype=dtype).with_(d=d)
+    r = _run_gqa(wl, g)
+    p, op = r["p"], r["op"]
+    ck, cq, iters = p.n_kv_groups, p.n_q_groups, p.kmeans_iters
+    n = wl.n
+    pairs = 0
+    for hk in range(hkv):
+        qg, kk, vv = r["q"][0, hk * g:(hk + 1) * g], r["k"][0, hk], r["v"][0, hk]
+        ex = op.export(hk * g)
+        # the plan pools the group's query heads (App. B.1 per K/V head)
+        assert rel_l2(ex["m_k"], orc.key_metric_pooled(qg, p.n_sampled_queries)) < 1e-5
+        assert rel_l2(ex["phi_k"], orc.project(kk, ex["f_k"].astype(np.float64))) < 1e-5
+        lab_k, cent_k, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, iters)
+        assert np.array_equal(ex["labels_kv"], lab_k) and np.array_equal(ex["cent_k"], cent_k)
+        kbar, _ = orc.group_mean(kk, lab_k, ck)
+        assert np.array_equal(ex["kbar"], kbar)
+        phiq = orc.project_pooled(qg, ex["f_q"].astype(np.float64), eps=p.eps_q)
+        assert rel_l2(ex["phi_q"], phiq) < 1e-5
+        lab_q, cent_q, cnt_q, _ = orc.kmeans(ex["phi_q"], cq, iters)
+        assert np.array_equal(ex["labels_q"], lab_q) and np.array_equal(ex["cent_q"], cent_q)
+        assert np.array_equal(ex["qbar"], orc.group_mean_pooled(qg, lab_q, cq))
+        prio = orc.route_priorities(ex["qbar"], cnt_q, ex["kbar"], cnt_k)
+        assert np.max(np.abs(ex["route_prio"] - prio)) < 2e-5 * (1 + np.max(np.abs(prio)))
+        m = min(p.n_probes, n)
+        budget = int(np.floor(float(np.float32(p.target_exec_density)) * n * n)) - m * n
+        z, _ = orc.route_select(ex["route_prio"], cnt_q, cnt_k, budget)
+        assert np.array_equal(ex["routes"], z)
+        probes, w = orc.probe_select(ex["phi_q"], lab_q, ex["cent_q"], p.n_probes)
+        assert np.array_equal(ex["probes"], probes)
+        nq, nk = np.bincount(lab_q, minlength=cq), np.bincount(lab_k, minlength=ck)
+        pairs += int((nq[:, None] * nk[None, :] * z).sum()) * g
+        # every query head of the group runs on that plan with its own rows
+        for j in range(g):
+            exj = op.export(hk * g + j, fields=["labels_q", "routes", "probes", "o_sparse"])
+            assert np.array_equal(exj["labels_q"], ex["labels_q"])
+            assert np.array_equal(exj["routes"], ex["routes"])
+            assert np.array_equal(exj["probes"], ex["probes"])
+            qj = r["q"][0, hk * g + j]
+            osp = orc.sparse_rows(qj, kk, vv, ex["labels_q"], ex["labels_kv"], ex["routes"])
+            assert rel_l2(exj["o_sparse"], osp) < (1e-6 if dtype == "f32" else 1e-2)
+            kw = oracle_kwargs(p)
+            ref, _ = orc.attend(qj, kk, vv, ex["labels_q"], ex["labels_kv"], ex["routes"], ex["probes"],
+                                ex["probe_weights"].astype(np.float64), r=kw["r"], lam=kw["lam"],
+                                eps=float(np.float32(p.eps_x)))
+            err = rel_l2(r["out"][0, hk * g + j], ref)
+            assert err < (1e-5 if dtype == "f32" else 2e-2), (hk, j, err)
+    st = op.stats()
+    assert st["routed_pairs"] == pairs
+    assert st["exec_pairs"] == pairs + st["n_probes"] * n
+    assert st["n_probes"] == g * hkv * min(p.n_probes, n)

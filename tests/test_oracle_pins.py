@@ -622,3 +622,76 @@ def test_route_priorities_normalised(orc):
         o1 = np.argsort(-prio[a, live], kind="stable")
         o2 = np.argsort(-logits[a, live], kind="stable")
         assert np.array_equal(o1, o2)
+
+
+# --------------------------------------------------------------------------
+# Grouped-query attention: the plan of a K/V head pools its query heads
+# (Sec. 4.3 shares the K/V partition and routes across them; App. B.1 builds
+# M_K per K/V head).
+# --------------------------------------------------------------------------
+
+def gqa_heads(g=3, n=700, seed=5):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((g, n, 64)).astype(np.float32)
+    if g > 1:
+        q[1] *= 1.7  # heads of different scale, so a plain mean is not a rescaling
+    return q
+
+
+def test_pooled_key_metric_is_mean_of_head_metrics(orc):
+    q = gqa_heads()
+    g, n, d = q.shape
+    ms = 50
+    rows = (np.arange(ms) * n) // ms
+    ref = np.mean([q[h][rows].astype(np.float64).T @ q[h][rows].astype(np.float64) / ms
+                   for h in range(g)], axis=0)
+    assert rel(orc.key_metric_pooled(q, ms), ref) < 1e-14
+
+
+def test_pooled_query_coordinates_against_numpy(orc):
+    q = gqa_heads()
+    rng = np.random.default_rng(6)
+    f = rng.standard_normal((64, 24))
+    y = np.einsum("hnd,dr->hnr", q.astype(np.float64), f)
+    den = np.maximum(np.sqrt((y ** 2).mean(axis=2, keepdims=True)), 1e-6)
+    ref = (y / den).mean(axis=0)
+    got = orc.project_pooled(q, f)
+    assert got.dtype == np.float32
+    assert np.max(np.abs(got - ref)) < 1e-6 * np.max(np.abs(ref))
+
+
+def test_pooled_group_means_against_numpy(orc):
+    q = gqa_heads()
+    g, n, d = q.shape
+    rng = np.random.default_rng(7)
+    lab = random_partition(rng, n, 9)
+    lab[lab == 4] = 5  # one empty group
+    ref = np.zeros((9, d))
+    for b in range(9):
+        if np.any(lab == b):
+            ref[b] = q[:, lab == b].astype(np.float64).reshape(-1, d).mean(axis=0)
+    got = orc.group_mean_pooled(q, lab, 9)
+    assert np.all(got[4] == 0)
+    assert np.max(np.abs(got - ref)) < 1e-6 * np.max(np.abs(ref))
+
+
+def test_pooled_forms_reduce_to_single_head(orc):
+    q = gqa_heads(g=1)[0]
+    rng = np.random.default_rng(8)
+    f = rng.standard_normal((64, 24))
+    lab = random_partition(rng, q.shape[0], 9)
+    assert np.array_equal(orc.key_metric_pooled(q[None], 50), orc.key_metric(q, 50))
+    assert np.array_equal(orc.project_pooled(q[None], f), orc.project(q, f, rms=True))
+    assert np.array_equal(orc.group_mean_pooled(q[None], lab, 9), orc.group_mean(q, lab, 9)[0])
+
+
+def test_gqa_plan_of_duplicated_heads_is_single_head_plan(orc):
+    # two identical query heads: every pooled quantity equals the single-head
+    # one exactly (sums of two equal terms halve exactly), so the whole plan does
+    q, k, v = tiny_head()
+    _, p1 = orc.run(q, k, v, **TINY)
+    kw = {key: TINY[key] for key in ("n_sampled", "r_k", "r_q", "c_k", "c_q", "iters", "density",
+                                     "n_probes")}
+    p2 = orc.plan(np.stack([q, q]), k, **kw)
+    for key in ("labels_q", "labels_kv", "z", "probes", "w"):
+        assert np.array_equal(p1[key], p2[key]), key
