@@ -120,6 +120,9 @@ def main():
                     help="steady state of consecutive calls: both k-means start from the previous "
                          "call's centroids and run 2 assignments; calls alternate between the "
                          "inputs and a copy perturbed by 5%% noise (as between denoising steps)")
+    ap.add_argument("--kv-heads", type=int, default=0,
+                    help="grouped-query attention: K/V heads (a divisor of the query heads; "
+                         "K/V are every G-th generated head); 0 = one per query head")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one plain fp32 copy (x * 1 over 256 MiB in, 256 MiB out) before the "
                          "timed region, so hardware counters of a known traffic can calibrate "
@@ -141,6 +144,13 @@ def main():
     log(f"inputs {tuple(q.shape)} {q.dtype} generated in {time.perf_counter() - t0:.1f}s")
 
     p = params_for(S, wl, args.density)
+    gqa = args.kv_heads > 0 and args.kv_heads != wl.heads
+    if gqa:
+        if wl.heads % args.kv_heads:
+            print("--kv-heads must divide the query heads", file=sys.stderr)
+            sys.exit(2)
+        g = wl.heads // args.kv_heads
+        k, v = k[:, ::g].contiguous(), v[:, ::g].contiguous()
     inputs = [(q, k, v)]
     if args.warm_start:
         p.warm_start, p.warm_iters = 1, 2
@@ -153,7 +163,7 @@ def main():
             return (xf + 0.05 * xf.std() * noise).to(x.dtype)
 
         inputs.append(tuple(nudge(x) for x in (q, k, v)))
-    op = S.SparsePR(S.shape_of(q), p)
+    op = S.SparsePR(S.shape_of(q, kv=k if gqa else None), p)
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream()
     ncall = [0]
@@ -229,6 +239,7 @@ def main():
                    "n": wl.n, "heads": wl.batch * wl.heads, "d": d,
                    "target_exec_density": args.density, "kv_groups": wl.groups()[0],
                    "q_groups": wl.groups()[1], "probes": wl.n_probes, "resid_rank": wl.resid_rank,
+                   "kv_heads": wl.batch * (args.kv_heads if gqa else wl.heads),
                    "ridge": wl.ridge, "kmeans_iters": wl.kmeans_iters,
                    "kmeans_start": ("warm: 2 assignments from the previous call's centroids, "
                                     "inputs alternating with a 5%-noise copy")

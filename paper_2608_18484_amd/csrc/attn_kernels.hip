@@ -660,12 +660,15 @@ __global__ __launch_bounds__(64) void k_attn_f32(Geom g, AttnArgs A) {
 }
 
 // Merge the key splits of the probe rows: O = sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m).
+// Kernels from here on take every query head in one launch: block index
+// bq = j * BH + bh is query head j of K/V head bh, whose attend outputs are
+// entry bq of the [G][BH] arrays and whose plan is entry bh.
 __global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
                                                      const int32_t* nprobes, float* odp) {
-  const int p = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  const int p = blockIdx.x, bq = blockIdx.y, bh = bq % g.BH, c = threadIdx.x;
   if (p >= nprobes[bh] || c >= g.dv) return;
   const int D = g.dv;
-  const float* src = part + ((size_t)bh * g.M + p) * g.nsplit * (D + 2);
+  const float* src = part + ((size_t)bq * g.M + p) * g.nsplit * (D + 2);
   float m = -INFINITY;
   for (int s = 0; s < g.nsplit; ++s) m = fmaxf(m, src[(size_t)s * (D + 2) + D]);
   float l = 0.f, o = 0.f;
@@ -675,7 +678,7 @@ __global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
     l += e[D + 1] * f;
     o += e[c] * f;
   }
-  odp[((size_t)bh * g.M + p) * D + c] = o / l;
+  odp[((size_t)bq * g.M + p) * D + c] = o / l;
 }
 
 // ---------------------------------------------------------------------------
@@ -713,12 +716,12 @@ __device__ __forceinline__ FitScratch fit_scratch(const Geom& g, const Work& w, 
 template <int D>
 __global__ __launch_bounds__(256) void k_fit_prep(Geom g, Work w) {
   __shared__ double swsh;
-  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int bq = blockIdx.x, bh = bq % g.BH, tid = threadIdx.x;
   const int np = w.nprobes[bh];
   const int r = g.r;
-  float* fv = w.fitv + (size_t)bh * 3 * D;
-  float* Y = w.fity + (size_t)bh * D * r;
-  float* Psi = w.fitpsi + (size_t)bh * D * r;
+  float* fv = w.fitv + (size_t)bq * 3 * D;
+  float* Y = w.fity + (size_t)bq * D * r;
+  float* Psi = w.fitpsi + (size_t)bq * D * r;
   for (int i = tid; i < D * r; i += 256) {
     Y[i] = 0.f;
     Psi[i] = 0.f;
@@ -732,11 +735,11 @@ __global__ __launch_bounds__(256) void k_fit_prep(Geom g, Work w) {
     if (tid == 0) w.stats[(size_t)bh * 16 + ST_FIT_RANK] = 0;
     return;
   }
-  const FitScratch f = fit_scratch(g, w, bh);
+  const FitScratch f = fit_scratch(g, w, bq);
   const int32_t* pr = w.probes + (size_t)bh * g.M;
   const float* pwt = w.pw + (size_t)bh * g.M;
-  const float* osp = w.osp + (size_t)bh * g.N * D;
-  const float* odp = w.odp + (size_t)bh * g.M * D;
+  const float* osp = w.osp + (size_t)bq * g.N * D;
+  const float* odp = w.odp + (size_t)bq * g.M * D;
   if (tid == 0) {
     double s = 0.0;
     for (int p = 0; p < np; ++p) s += (double)pwt[p];
@@ -780,11 +783,11 @@ __global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
   constexpr int PB = 64;
   __shared__ double sa[PB][33], sb[PB][33];
   __shared__ double swt[PB];
-  const int bh = blockIdx.z, which = blockIdx.y, tid = threadIdx.x;
+  const int bq = blockIdx.z, bh = bq % g.BH, which = blockIdx.y, tid = threadIdx.x;
   const int np = w.nprobes[bh];
   if (np == 0) return;
   const int ti = blockIdx.x / (D / 32), tj = blockIdx.x % (D / 32);
-  const FitScratch f = fit_scratch(g, w, bh);
+  const FitScratch f = fit_scratch(g, w, bq);
   const double* src = which == 0 ? f.rb : f.xb;
   const int li = tid / 8, lj = (tid % 8) * 4;
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
@@ -804,7 +807,7 @@ __global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
       for (int e = 0; e < 4; ++e) acc[e] += a * sb[p][lj + e];
     }
   }
-  double* G = w.fitgram + ((size_t)bh * 2 + which) * D * D;
+  double* G = w.fitgram + ((size_t)bq * 2 + which) * D * D;
   const int i = ti * 32 + li;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -828,17 +831,17 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
   __shared__ int flag, rank_s, fail;
-  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int bq = blockIdx.x, bh = bq % g.BH, tid = threadIdx.x;
   const int np = w.nprobes[bh];
   if (np == 0) return;
   const int r = g.r;
-  float* Y = w.fity + (size_t)bh * D * r;
-  float* Psi = w.fitpsi + (size_t)bh * D * r;
-  const FitScratch f = fit_scratch(g, w, bh);
-  const double* H = w.fitgram + ((size_t)bh * 2 + 0) * D * D;
-  const double* Sg = w.fitgram + ((size_t)bh * 2 + 1) * D * D;
+  float* Y = w.fity + (size_t)bq * D * r;
+  float* Psi = w.fitpsi + (size_t)bq * D * r;
+  const FitScratch f = fit_scratch(g, w, bq);
+  const double* H = w.fitgram + ((size_t)bq * 2 + 0) * D * D;
+  const double* Sg = w.fitgram + ((size_t)bq * 2 + 1) * D * D;
   T* Am = (T*)smem;
-  T* Vm = VG ? (T*)(w.fitvec + (size_t)bh * D * LD) : Am + D * LD;
+  T* Vm = VG ? (T*)(w.fitvec + (size_t)bq * D * LD) : Am + D * LD;
   for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
   __syncthreads();
   jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
@@ -946,17 +949,17 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
   __shared__ float ts[ROWS][RS + 1];
   __shared__ __attribute__((aligned(16))) float fy[D][RS];
   __shared__ __attribute__((aligned(16))) float fp[D][RS];
-  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int bq = blockIdx.y, bh = bq % g.BH, tid = threadIdx.x;
   const int r0 = blockIdx.x * ROWS;
   const int r = g.r;
   const int rw = tid >> 2, qtr = tid & 3;
   const int row = r0 + rw;
   const bool valid = row < g.N;
   const bool text = row < g.ntext;
-  const float* fv = w.fitv + (size_t)bh * 3 * D;
-  const float* Y = w.fity + (size_t)bh * D * r;
-  const float* Psi = w.fitpsi + (size_t)bh * D * r;
-  const float* src = w.osp + ((size_t)bh * g.N + (valid ? row : 0)) * D + qtr * CW;
+  const float* fv = w.fitv + (size_t)bq * 3 * D;
+  const float* Y = w.fity + (size_t)bq * D * r;
+  const float* Psi = w.fitpsi + (size_t)bq * D * r;
+  const float* src = w.osp + ((size_t)bq * g.N + (valid ? row : 0)) * D + qtr * CW;
   float x[CW], acc[CW];
 #pragma unroll
   for (int c4 = 0; c4 < CW / 4; ++c4) {
@@ -1014,7 +1017,7 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
     }
   }
   if (!valid) return;
-  const int64_t dst = q_base(g, bh, g.gq) + (int64_t)row * g.sn + qtr * CW;
+  const int64_t dst = q_base(g, bh, bq / g.BH) + (int64_t)row * g.sn + qtr * CW;
   float o[CW];
 #pragma unroll
   for (int c = 0; c < CW; ++c) o[c] = text ? x[c] : x[c] + fv[2 * D + qtr * CW + c] + acc[c];
@@ -1041,11 +1044,11 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
 
 // Probe rows take their exact dense rows (eq. final_reconstructed_output).
 __global__ __launch_bounds__(128) void k_probe_scatter(Geom g, Work w, void* out) {
-  const int p = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  const int p = blockIdx.x, bq = blockIdx.y, bh = bq % g.BH, c = threadIdx.x;
   if (p >= w.nprobes[bh] || c >= g.dv) return;
   const int row = w.probes[(size_t)bh * g.M + p];
-  const float v = w.odp[((size_t)bh * g.M + p) * g.dv + c];
-  const int64_t idx = q_base(g, bh, g.gq) + (int64_t)row * g.sn + c;
+  const float v = w.odp[((size_t)bq * g.M + p) * g.dv + c];
+  const int64_t idx = q_base(g, bh, bq / g.BH) + (int64_t)row * g.sn + c;
   if (g.bf16) {
     const __bf16 b = (__bf16)v;
     ((uint16_t*)out)[idx] = __builtin_bit_cast(uint16_t, b);
@@ -1121,6 +1124,9 @@ static void attend_d(const Geom& g, const Work* wq, const void* q, const void* k
     }
   }
   if (ev) (void)hipEventRecord(ev[1], s);
+  // the kernels below take all G * BH query heads in one launch (view of
+  // query head 0, whose [G][BH] arrays continue with the other query heads)
+  const int BQ = g.BH * g.G;
   if (g.M > 0) {
     for (int j = 0; j < g.G; ++j) {
       const AttnArgs a = make_args(&wq[j], q, k, v, out);
@@ -1128,25 +1134,21 @@ static void attend_d(const Geom& g, const Work* wq, const void* q, const void* k
         k_attn_mfma<D, MODE_PROBE><<<gp, 128, 0, s>>>(gj(j), a);
       else
         k_attn_f32<D, MODE_PROBE><<<gp, 64, 0, s>>>(gj(j), a);
-      k_probe_merge<<<dim3(g.M, g.BH), 128, 0, s>>>(g, wq[j].part, wq[j].nprobes, wq[j].odp);
     }
+    k_probe_merge<<<dim3(g.M, BQ), 128, 0, s>>>(g, wq[0].part, wq[0].nprobes, wq[0].odp);
   }
   if (ev) (void)hipEventRecord(ev[2], s);
-  for (int j = 0; j < g.G; ++j) {
-    k_fit_prep<D><<<g.BH, 256, 0, s>>>(g, wq[j]);
-    k_fit_gram<D><<<dim3((D / 32) * (D / 32), 2, g.BH), 256, 0, s>>>(g, wq[j]);
-    // float inputs (whose outputs are held to float rounding) get the
-    // double solve; bf16 inputs the float one
-    if (D <= 64 || !g.bf16)
-      k_fit_solve<D, double><<<g.BH, 1024, 0, s>>>(g, wq[j]);
-    else
-      k_fit_solve<D, float><<<g.BH, 1024, 0, s>>>(g, wq[j]);
-  }
+  k_fit_prep<D><<<BQ, 256, 0, s>>>(g, wq[0]);
+  k_fit_gram<D><<<dim3((D / 32) * (D / 32), 2, BQ), 256, 0, s>>>(g, wq[0]);
+  // float inputs (whose outputs are held to float rounding) get the double
+  // solve; bf16 inputs the float one
+  if (D <= 64 || !g.bf16)
+    k_fit_solve<D, double><<<BQ, 1024, 0, s>>>(g, wq[0]);
+  else
+    k_fit_solve<D, float><<<BQ, 1024, 0, s>>>(g, wq[0]);
   if (ev) (void)hipEventRecord(ev[3], s);
-  for (int j = 0; j < g.G; ++j) {
-    k_correct<D><<<dim3((g.N + 63) / 64, g.BH), 256, 0, s>>>(gj(j), wq[j], out);
-    if (g.M > 0) k_probe_scatter<<<dim3(g.M, g.BH), 128, 0, s>>>(gj(j), wq[j], out);
-  }
+  k_correct<D><<<dim3((g.N + 63) / 64, BQ), 256, 0, s>>>(g, wq[0], out);
+  if (g.M > 0) k_probe_scatter<<<dim3(g.M, BQ), 128, 0, s>>>(g, wq[0], out);
   if (ev) (void)hipEventRecord(ev[4], s);
 }
 

@@ -277,11 +277,12 @@ class SparsePR:
 
 
 def dense_attention(q, k, v, out=None, stream=None):
-    """Dense attention (Sec. 3) for every head on the probe kernels."""
+    """Dense attention (Sec. 3) for every query head on the probe kernels
+    (K and V may have fewer heads: grouped-query attention)."""
     import torch
     if out is None:
         out = torch.empty_like(q)
-    sh = shape_of(q)
+    sh = shape_of(q, kv=k if k.shape[1] != q.shape[1] else None)
     _check(lib().sparsepr_dense_attend(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                        None, ctypes.c_size_t(0), _stream(stream)))
     return out
