@@ -122,7 +122,7 @@ void describe(const Geom& g, Work* w, Layout& L) {
   addq(&w->fitpsi, dv * r * 4);
   addq(&w->fitscr, (2 * M * dv + M * r + dv * r + M) * 8);
   addq(&w->fitgram, 2 * dv * dv * 8);
-  addq(&w->fitvec, (!g.bf16 && dv > 64) ? dv * (dv + 1) * 8 : 0);
+  addq(&w->fitvec, (!g.bf16 && dv > 64) ? dv * (dv + 4) * 8 : 0);
   add(&w->stats, 16 * 8);
   size_t off = 0;
   for (auto& it : L.items) off += align256((size_t)g.BH * it.per_head * (it.per_query ? g.G : 1));

@@ -824,9 +824,10 @@ __global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
 // both fit in LDS; V (VG) then lives in the head's global scratch.
 template <int D, typename T>
 __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
-  constexpr int LD = D + 1;
-  constexpr bool VG = 2 * D * LD * sizeof(T) > 140 * 1024;
-  constexpr size_t JAC = (VG ? 1 : 2) * D * LD * sizeof(T), CHOL = (size_t)D * D * sizeof(double);
+  constexpr int LD = D + 1, LV = jacobi_vt_ld<D>();
+  constexpr bool VG = (size_t)D * (LD + LV) * sizeof(T) > 140 * 1024;
+  constexpr size_t JAC = (size_t)D * (LD + (VG ? 0 : LV)) * sizeof(T),
+                   CHOL = (size_t)D * D * sizeof(double);
   __shared__ __attribute__((aligned(16))) unsigned char smem[JAC > CHOL ? JAC : CHOL];
   __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
@@ -841,7 +842,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   const double* H = w.fitgram + ((size_t)bq * 2 + 0) * D * D;
   const double* Sg = w.fitgram + ((size_t)bq * 2 + 1) * D * D;
   T* Am = (T*)smem;
-  T* Vm = VG ? (T*)(w.fitvec + (size_t)bq * D * LD) : Am + D * LD;
+  T* Vm = VG ? (T*)(w.fitvec + (size_t)bq * D * LV) : Am + D * LD;  // transposed (jacobi_eig_lds)
   for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
   __syncthreads();
   jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
@@ -874,12 +875,12 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   const int rk = rank_s;
   for (int i = tid; i < D * rk; i += 1024) {
     const int row = i / rk, t = i % rk;
-    Psi[row * r + t] = (float)Vm[row * LD + order[t]];
+    Psi[row * r + t] = (float)Vm[order[t] * LV + row];
   }
   for (int i = tid; i < np * rk; i += 1024) {
     const int p = i / rk, t = i % rk;
     double acc = 0.0;
-    for (int c = 0; c < D; ++c) acc += f.rb[(size_t)p * D + c] * (double)Vm[c * LD + order[t]];
+    for (int c = 0; c < D; ++c) acc += f.rb[(size_t)p * D + c] * (double)Vm[order[t] * LV + c];
     f.rp[(size_t)p * r + t] = acc;
   }
   __syncthreads();

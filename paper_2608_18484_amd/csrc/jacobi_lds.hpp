@@ -4,13 +4,16 @@
 //
 // Each step applies the D/2 disjoint rotations of the round-robin (circle)
 // ordering.  One thread per pair computes the rotation; then A <- J^T A J is
-// applied as independent 2x2 blocks (pair i rows x pair j columns) and
-// V <- V J as independent row pairs, in one pass with one barrier.  With
-// NT a multiple of D/2 every thread keeps the same column pair j for the
-// whole step, so its rotation is read from LDS once.  On return A's diagonal
-// holds the eigenvalues and V's columns the eigenvectors (row stride D + 1).
-// A is in LDS; V is in LDS or, when both do not fit, in the block's own
-// global scratch (the block barriers order those accesses as well).
+// applied as independent 2x2 blocks (pair i rows x pair j columns) and the
+// eigenvector matrix as independent row pairs of its transpose, in one pass
+// with one barrier.  With NT a multiple of D/2 every thread keeps the same
+// column pair j for the whole step, so its rotation is read from LDS once.
+// On return A's diagonal (row stride D + 1) holds the eigenvalues and row k
+// of VT (row stride D + 4, 16-byte aligned) the eigenvector of A[k][k]: the
+// transposed layout turns each rotation of two eigenvector columns into two
+// contiguous rows, updated four elements per access.  A is in LDS; VT is in
+// LDS or, when both do not fit, in the block's own global scratch (the block
+// barriers order those accesses as well).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -23,14 +26,20 @@ struct alignas(16) JacobiRot {
   int p, q;
 };
 
+template <int D>
+constexpr int jacobi_vt_ld() {
+  return D + 4;
+}
+
 template <int D, typename T, int NT>
-__device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop) {
-  constexpr int LD = D + 1, P = D / 2;
-  static_assert(NT % P == 0 && (P * P) % NT == 0 && (D * P) % NT == 0, "thread mapping");
+__device__ void jacobi_eig_lds(T* A, T* VT, JacobiRot<T>* rot, int* flag, T stop) {
+  constexpr int LD = D + 1, LV = jacobi_vt_ld<D>(), P = D / 2;
+  static_assert(NT % P == 0 && (P * P) % NT == 0, "thread mapping");
+  typedef T T4 __attribute__((ext_vector_type(4)));
   const int tid = threadIdx.x;
   for (int i = tid; i < D * D; i += NT) {
     const int r = i / D, c = i % D;
-    V[r * LD + c] = (r == c) ? T(1) : T(0);
+    VT[r * LV + c] = (r == c) ? T(1) : T(0);
   }
   __syncthreads();
   for (int sweep = 0; sweep < 20; ++sweep) {
@@ -49,12 +58,25 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop)
         const T app = A[p * LD + p], aqq = A[q * LD + q], apq = A[p * LD + q];
         T c = 1, s = 0;
         const T tol = sizeof(T) == 8 ? T(1e-15) : T(3e-7);
-        if (apq != T(0) && fabs(apq) > tol * sqrt(fabs(app * aqq))) {
+        // rotate unless |apq| <= tol * sqrt(|app aqq|) (compared squared)
+        if (apq != T(0) && apq * apq > tol * tol * fabs(app * aqq)) {
+          // tan of the rotation angle: the smaller root of t^2 + 2 theta t - 1
           const T theta = (aqq - app) / (T(2) * apq);
           const T at = fabs(theta);
-          const T t = (at > T(1e10)) ? T(0.5) / theta
-                                     : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
-          c = T(1) / sqrt(t * t + T(1));
+          T t;
+          if constexpr (sizeof(T) == 4) {
+            // hardware reciprocal, square root and reciprocal square root
+            // (each about 1 ulp): the chain of this one wave is what every
+            // other wave waits for, and c = rsq(1 + t^2), s = t c keeps
+            // c^2 + s^2 = 1 to the same rounding as exact operations would
+            t = (at > T(1e10)) ? T(0.5) * __builtin_amdgcn_rcpf(theta)
+                               : copysign(__builtin_amdgcn_rcpf(at + __builtin_amdgcn_sqrtf(fmaf(theta, theta, 1.f))), theta);
+            c = __builtin_amdgcn_rsqf(fmaf(t, t, 1.f));
+          } else {
+            t = (at > T(1e10)) ? T(0.5) / theta
+                               : copysign(T(1), theta) / (at + sqrt(theta * theta + T(1)));
+            c = T(1) / sqrt(t * t + T(1));
+          }
           s = t * c;
           *flag = 1;
         }
@@ -64,11 +86,11 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop)
       // All of a thread's loads are issued before any of its stores: its
       // 2x2 blocks and eigenvector row pairs are disjoint from every other
       // thread's, so one LDS round trip serves the whole update.
-      constexpr int NB = P * P / NT, NVR = D * P / NT;
+      constexpr int NB = P * P / NT, NVI = (P * (D / 4) + NT - 1) / NT;
       const int j = tid % P;
       const JacobiRot<T> rj = rot[j];
       JacobiRot<T> ri[NB];
-      T x[NB][4], vp[NVR], vq[NVR];
+      T x[NB][4];
 #pragma unroll
       for (int k = 0; k < NB; ++k) ri[k] = rot[tid / P + k * (NT / P)];
 #pragma unroll
@@ -79,11 +101,18 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop)
         x[k][2] = A[q * LD + rj.p];
         x[k][3] = A[q * LD + rj.q];
       }
+      // eigenvector rows: item e = (pair e / (D/4), four elements e % (D/4))
+      T4 vp[NVI], vq[NVI];
+      JacobiRot<T> rv[NVI];
 #pragma unroll
-      for (int k = 0; k < NVR; ++k) {
-        const int row = tid / P + k * (NT / P);
-        vp[k] = V[row * LD + rj.p];
-        vq[k] = V[row * LD + rj.q];
+      for (int k = 0; k < NVI; ++k) {
+        const int e = tid + k * NT;
+        if (e < P * (D / 4)) {
+          rv[k] = rot[e / (D / 4)];
+          const int c4 = (e % (D / 4)) * 4;
+          vp[k] = *(const T4*)(VT + rv[k].p * LV + c4);
+          vq[k] = *(const T4*)(VT + rv[k].q * LV + c4);
+        }
       }
 #pragma unroll
       for (int k = 0; k < NB; ++k) {
@@ -100,12 +129,13 @@ __device__ void jacobi_eig_lds(T* A, T* V, JacobiRot<T>* rot, int* flag, T stop)
         A[q * LD + rj.p] = z10;
         A[q * LD + rj.q] = z11;
       }
-      if (rj.s != T(0)) {
 #pragma unroll
-        for (int k = 0; k < NVR; ++k) {
-          const int row = tid / P + k * (NT / P);
-          V[row * LD + rj.p] = rj.c * vp[k] - rj.s * vq[k];
-          V[row * LD + rj.q] = rj.s * vp[k] + rj.c * vq[k];
+      for (int k = 0; k < NVI; ++k) {
+        const int e = tid + k * NT;
+        if (e < P * (D / 4) && rv[k].s != T(0)) {
+          const int c4 = (e % (D / 4)) * 4;
+          *(T4*)(VT + rv[k].p * LV + c4) = rv[k].c * vp[k] - rv[k].s * vq[k];
+          *(T4*)(VT + rv[k].q * LV + c4) = rv[k].s * vp[k] + rv[k].c * vq[k];
         }
       }
       __syncthreads();

@@ -104,8 +104,9 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
                                                     float* evals) {
   using T = typename std::conditional<D <= 64, double, float>::type;
   constexpr int LD = D + 1;
+  constexpr int LV = jacobi_vt_ld<D>();
   __shared__ T A[D * LD];
-  __shared__ T V[D * LD];
+  __shared__ __attribute__((aligned(16))) T VT[D * LV];
   __shared__ JacobiRot<T> rot[D / 2];
   __shared__ int order[D];
   __shared__ double lam[D];
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   // In float the basis reaches its rounding floor at a relative off-diagonal
   // norm of about 1e-4 (measured on the long-video key metric: the weighted
   // projector then differs from a double solve by 2.7e-5).
-  jacobi_eig_lds<D, T, 1024>(A, V, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
+  jacobi_eig_lds<D, T, 1024>(A, VT, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
   eig_order<D, T>(A, order);
   const double l1 = A[order[0] * LD + order[0]];
   if (tid < D) {
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   for (int i = tid; i < D * r; i += blockDim.x) {
     const int row = i / r, t = i % r;
     const double wgt = meanv > 0.0 ? sqrt(lam[t] / meanv) : 0.0;
-    Fo[i] = (float)((double)V[row * LD + order[t]] * wgt);
+    Fo[i] = (float)((double)VT[order[t] * LV + row] * wgt);
   }
   if (tid < D) evals[(size_t)bh * D + tid] = (float)lam[tid];
 }

@@ -110,7 +110,7 @@ struct Work {
   float* fitpsi;      // [BH][dv][r]
   double* fitscr;     // [BH][2*M*dv + M*r + dv*r + M] fit scratch
   double* fitgram;    // [BH][2][dv][dv] Rbar^T W Rbar and xbar^T W xbar + lambda I
-  double* fitvec;     // [BH][dv][dv+1] eigenvectors of a double fit solve kept out of LDS
+  double* fitvec;     // [BH][dv][dv+4] eigenvectors (transposed) of a double fit solve kept out of LDS
   int64_t* stats;     // [BH][16]
 };
 
