@@ -123,6 +123,16 @@ def main():
     ap.add_argument("--kv-heads", type=int, default=0,
                     help="grouped-query attention: K/V heads (a divisor of the query heads; "
                          "K/V are every G-th generated head); 0 = one per query head")
+    ap.add_argument("--partition", default="response", choices=["response", "semantic", "key-response"],
+                    help="partition ablation (Sec. 5.2): response-coupled (the method), semantic "
+                         "(k-means on the raw keys and queries), key-response K/V groups with "
+                         "semantic query groups")
+    ap.add_argument("--probe-rule", default="stratified", choices=["stratified", "random", "uniform"],
+                    help="probe-selection ablation (Table probe_estimator_ablation)")
+    ap.add_argument("--ridge-only", action="store_true",
+                    help="estimator ablation: ridge fit without the probe-residual subspace")
+    ap.add_argument("--n-probes", type=int, default=-1,
+                    help="probe rows per head (default: the workload's; 0 disables the repair)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one plain fp32 copy (x * 1 over 256 MiB in, 256 MiB out) before the "
                          "timed region, so hardware counters of a known traffic can calibrate "
@@ -144,6 +154,11 @@ def main():
     log(f"inputs {tuple(q.shape)} {q.dtype} generated in {time.perf_counter() - t0:.1f}s")
 
     p = params_for(S, wl, args.density)
+    p.partition = {"response": 0, "semantic": 1, "key-response": 2}[args.partition]
+    p.probe_rule = {"stratified": 0, "random": 1, "uniform": 2}[args.probe_rule]
+    p.ridge_only = int(args.ridge_only)
+    if args.n_probes >= 0:
+        p.n_probes = args.n_probes
     gqa = args.kv_heads > 0 and args.kv_heads != wl.heads
     if gqa:
         if wl.heads % args.kv_heads:
@@ -238,8 +253,10 @@ def main():
                                f"N={wl.n}, {wl.batch}x{wl.heads} heads, d={d}",
                    "n": wl.n, "heads": wl.batch * wl.heads, "d": d,
                    "target_exec_density": args.density, "kv_groups": wl.groups()[0],
-                   "q_groups": wl.groups()[1], "probes": wl.n_probes, "resid_rank": wl.resid_rank,
+                   "q_groups": wl.groups()[1], "probes": p.n_probes, "resid_rank": wl.resid_rank,
                    "kv_heads": wl.batch * (args.kv_heads if gqa else wl.heads),
+                   "partition": args.partition, "probe_rule": args.probe_rule,
+                   "estimator": "ridge only" if args.ridge_only else "ridge + probe-residual subspace",
                    "ridge": wl.ridge, "kmeans_iters": wl.kmeans_iters,
                    "kmeans_start": ("warm: 2 assignments from the previous call's centroids, "
                                     "inputs alternating with a 5%-noise copy")

@@ -103,7 +103,39 @@ typedef struct {
                                   steps); the first call on a plan starts cold; 0 */
   int32_t warm_iters;          /* assignments of a warm-started k-means, in
                                   [1, kmeans_iters]; 0 = kmeans_iters; 0 */
+  /* Ablation variants of Sec. 5.2 (Tables partition_repair_ablation and
+   * probe_estimator_ablation); the defaults are the method itself. */
+  int32_t partition;           /* SPARSEPR_PARTITION_*; RESPONSE */
+  int32_t probe_rule;          /* SPARSEPR_PROBES_*; STRATIFIED */
+  uint32_t probe_seed;         /* seed of SPARSEPR_PROBES_RANDOM; 0 */
+  int32_t ridge_only;          /* 1: ridge estimator without the probe-residual
+                                  output subspace (Psi = I, so the correction is
+                                  xbar B_lambda); 0 */
 } sparsepr_params;
+
+/* partition: how the K/V and query groups are formed.
+ *   RESPONSE      response-coupled partitioning (Sec. 4.1, App. B);
+ *   SEMANTIC      the reference partition of Sec. 3.1: k-means on the raw
+ *                 keys (values inherit their key's group) and, separately,
+ *                 on the raw queries;
+ *   KEY_RESPONSE  K/V groups from the key-response coordinates phi_K, query
+ *                 groups from k-means on the raw queries (Sec. 5.2). */
+#define SPARSEPR_PARTITION_RESPONSE 0
+#define SPARSEPR_PARTITION_SEMANTIC 1
+#define SPARSEPR_PARTITION_KEY_RESPONSE 2
+/* probe_rule: which rows are evaluated exactly (Table probe_estimator_ablation).
+ *   STRATIFIED  query-group-stratified selection (App. A.2, Algorithm
+ *               app_probe_selection) with coverage weights |G_a| / m_a;
+ *   RANDOM      M distinct video rows uniformly at random: the M rows with the
+ *               smallest SplitMix64(probe_seed * 2^32 + row) (the mixing
+ *               function of Steele, Lea and Flood 2014), in that order;
+ *   UNIFORM     evenly spaced video rows floor((2i + 1) n_v / (2M)), i < M
+ *               (tokens are in raster order, so these spread over space and
+ *               time).
+ * RANDOM and UNIFORM weigh every probe equally, w_p = n_v / M. */
+#define SPARSEPR_PROBES_STRATIFIED 0
+#define SPARSEPR_PROBES_RANDOM 1
+#define SPARSEPR_PROBES_UNIFORM 2
 
 /* Realised accounting of one call (Sec. 4.3: rho_exec = rho_route + M/N_q).
  * Pair and probe counts are summed over query heads (every query head of a

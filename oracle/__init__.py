@@ -105,14 +105,33 @@ def key_metric_pooled(q, m_s):
     return out
 
 
-def project_pooled(x, f, eps=1e-6):
-    """Mean over the heads of x [G, n, d] of the normalised query coordinates."""
+def project_pooled(x, f, eps=1e-6, rms=True):
+    """Mean over the heads of x [G, n, d] of the (normalised) query coordinates."""
     x, f = _f32(x), _f64(f)
     nh, n, d = x.shape
     r = f.shape[1]
     phi = np.zeros((n, r), np.float32)
-    lib().or_project_pooled(_p(x), nh, n, d, _p(f), r, ctypes.c_double(eps), _p(phi))
+    lib().or_project_pooled(_p(x), nh, n, d, _p(f), r, int(rms), ctypes.c_double(eps), _p(phi))
     return phi
+
+
+def splitmix64(x):
+    lib().or_splitmix64.restype = ctypes.c_uint64
+    return int(lib().or_splitmix64(ctypes.c_uint64(x)))
+
+
+def probe_uniform(n, m):
+    probes = np.zeros(max(m, 1), np.int32)
+    w = np.zeros(max(m, 1), np.float64)
+    k = lib().or_probe_uniform(n, m, _p(probes), _p(w))
+    return probes[:k], w[:k]
+
+
+def probe_random(n, m, seed):
+    probes = np.zeros(max(m, 1), np.int32)
+    w = np.zeros(max(m, 1), np.float64)
+    k = lib().or_probe_random(n, m, ctypes.c_uint32(seed), _p(probes), _p(w))
+    return probes[:k], w[:k]
 
 
 def group_mean_pooled(x, labels, c):
@@ -236,7 +255,7 @@ def probe_select(phi, labels, cent, m):
     return probes[:np_], w[:np_]
 
 
-def fit(x, od, w, r, lam, eps=1e-6):
+def fit(x, od, w, r, lam, eps=1e-6, ridge_only=False):
     x, od, w = _f64(x), _f64(od), _f64(w)
     m, dv = x.shape if x.ndim == 2 else (0, od.shape[-1])
     mu_x = np.zeros(dv)
@@ -246,7 +265,8 @@ def fit(x, od, w, r, lam, eps=1e-6):
     psi = np.zeros((dv, max(r, 1)))
     g = np.zeros((dv, dv))
     rank = ctypes.c_int(0)
-    st = lib().or_fit(_p(x), _p(od), _p(w), m, dv, r, ctypes.c_double(lam), ctypes.c_double(eps),
+    st = lib().or_fit(_p(x), _p(od), _p(w), m, dv, r, int(ridge_only), ctypes.c_double(lam),
+                      ctypes.c_double(eps),
                       _p(mu_x), _p(s_x), _p(mu_r), _p(b), _p(psi), _p(g), ctypes.byref(rank))
     return {"status": st, "mu_x": mu_x, "s_x": s_x, "mu_r": mu_r, "b": b,
             "psi": psi[:, :rank.value], "g": g, "rank": rank.value}
@@ -261,7 +281,8 @@ def correct_rows(x, ft):
     return out
 
 
-def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_probes):
+def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_probes,
+         partition=0, probe_rule=0, probe_seed=0):
     """Whole Response-Coupled Partitioning + routing + probe choice for one
     K/V head.  q is [n, d], or [G, n, d] for the G query heads that share the
     K/V head under grouped-query attention (the plan pools them)."""
@@ -270,6 +291,10 @@ def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_pro
     n, d = q.shape[-2:]
     nv = n - n_text
     rk, rq = min(r_k, d), min(r_q, d)
+    if partition == 1:
+        rk = d
+    if partition != 0:
+        rq = d
     cq_t, ck_t = c_q + (n_text > 0), c_k + (n_text > 0)
     out = {
         "labels_q": np.zeros(n, np.int32), "labels_kv": np.zeros(n, np.int32),
@@ -282,7 +307,8 @@ def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_pro
         "stats": np.zeros(7, np.int64),
     }
     lib().or_plan(_p(q), nqh, _p(k), n, d, n_text, n_sampled, r_k, r_q, c_k, c_q, iters,
-                  ctypes.c_double(density), n_probes, _p(out["labels_q"]), _p(out["labels_kv"]),
+                  ctypes.c_double(density), n_probes, int(partition), int(probe_rule),
+                  ctypes.c_uint32(probe_seed), _p(out["labels_q"]), _p(out["labels_kv"]),
                   _p(out["z"]), _p(out["probes"]), _p(out["w"]), _p(out["fk"]), _p(out["fq"]),
                   _p(out["phik"]), _p(out["phiq"]), _p(out["kbar"]), _p(out["qbar"]),
                   _p(out["cqphi"]), _p(out["prio"]), _p(out["stats"]))
@@ -295,7 +321,8 @@ def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_pro
     return out
 
 
-def attend(q, k, v, labels_q, labels_kv, z, probes, w, *, n_text=0, r, lam, eps=1e-6):
+def attend(q, k, v, labels_q, labels_kv, z, probes, w, *, n_text=0, r, lam, eps=1e-6,
+           ridge_only=False):
     """Sparse attention + exact probes + fit + correction for one head (double)."""
     q, k, v = _f32(q), _f32(k), _f32(v)
     n, d = q.shape
@@ -308,7 +335,7 @@ def attend(q, k, v, labels_q, labels_kv, z, probes, w, *, n_text=0, r, lam, eps=
     fo = np.zeros(3 * dv + dv * dv, np.float64)
     st = lib().or_attend(_p(q), _p(k), _p(v), n, d, dv, n_text, _p(_i32(labels_q)),
                          _p(_i32(labels_kv)), z.shape[0], z.shape[1], _p(z),
-                         _p(probes) if m else None, _p(w) if m else None, m, r,
+                         _p(probes) if m else None, _p(w) if m else None, m, r, int(ridge_only),
                          ctypes.c_double(lam), ctypes.c_double(eps), _p(out), _p(fo))
     fit_out = {"status": st, "mu_x": fo[:dv], "s_x": fo[dv:2 * dv], "mu_r": fo[2 * dv:3 * dv],
                "g": fo[3 * dv:].reshape(dv, dv)}
@@ -319,8 +346,13 @@ def run(q, k, v, **params):
     """plan + attend for one head; returns (output, plan)."""
     pl = plan(q, k, n_text=params.get("n_text", 0), n_sampled=params["n_sampled"],
               r_k=params["r_k"], r_q=params["r_q"], c_k=params["c_k"], c_q=params["c_q"],
-              iters=params["iters"], density=params["density"], n_probes=params["n_probes"])
+              iters=params["iters"], density=params["density"], n_probes=params["n_probes"],
+              partition=params.get("partition", 0), probe_rule=params.get("probe_rule", 0),
+              probe_seed=params.get("probe_seed", 0))
+    ridge_only = bool(params.get("ridge_only", False))
+    dv = np.shape(v)[-1]
     out, ft = attend(q, k, v, pl["labels_q"], pl["labels_kv"], pl["z"], pl["probes"], pl["w"],
-                     n_text=params.get("n_text", 0), r=params["r"], lam=params["lam"])
+                     n_text=params.get("n_text", 0), r=dv if ridge_only else params["r"],
+                     lam=params["lam"], ridge_only=ridge_only)
     pl["fit"] = ft
     return out, pl

@@ -562,9 +562,58 @@ static int cholesky(double* a, int n) {
   return 0;
 }
 
+/* Probe rules of the ablation (Table probe_estimator_ablation), equal
+ * weights n_v / M.  Readings: "uniform spatiotemporal" = evenly spaced rows of
+ * the raster token order, floor((2i + 1) n / (2m)); "random" = the m rows with
+ * the smallest SplitMix64 keys (Steele, Lea and Flood 2014) of seed * 2^32 +
+ * row, a uniformly random subset, in key order. */
+uint64_t or_splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+int or_probe_uniform(int n, int m, int32_t* probes, double* w) {
+  if (m > n) m = n;
+  for (int i = 0; i < m; ++i) {
+    probes[i] = (int32_t)(((int64_t)(2 * i + 1) * n) / (2 * (int64_t)m));
+    w[i] = (double)(float)((float)n / (float)m);
+  }
+  return m;
+}
+
+typedef struct {
+  uint64_t key;
+  int32_t row;
+} KeyRow;
+
+static int keyrow_cmp(const void* a, const void* b) {
+  const KeyRow* x = (const KeyRow*)a;
+  const KeyRow* y = (const KeyRow*)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  return x->row < y->row ? -1 : (x->row > y->row);
+}
+
+int or_probe_random(int n, int m, uint32_t seed, int32_t* probes, double* w) {
+  if (m > n) m = n;
+  KeyRow* kr = (KeyRow*)malloc(sizeof(KeyRow) * (size_t)(n > 0 ? n : 1));
+  for (int i = 0; i < n; ++i) {
+    kr[i].key = or_splitmix64(((uint64_t)seed << 32) | (uint32_t)i);
+    kr[i].row = i;
+  }
+  qsort(kr, (size_t)n, sizeof(KeyRow), keyrow_cmp);
+  for (int i = 0; i < m; ++i) {
+    probes[i] = kr[i].row;
+    w[i] = (double)(float)((float)n / (float)m);
+  }
+  free(kr);
+  return m;
+}
+
 int or_fit(const double* x, const double* od, const double* w, int m, int dv, int r,
-           double lambda, double eps, double* mu_x, double* s_x, double* mu_r, double* b,
-           double* psi, double* g, int* rank) {
+           int ridge_only, double lambda, double eps, double* mu_x, double* s_x, double* mu_r,
+           double* b, double* psi, double* g, int* rank) {
   int status = 0;
   for (int c = 0; c < dv; ++c) mu_x[c] = s_x[c] = mu_r[c] = 0.0;
   memset(b, 0, sizeof(double) * (size_t)dv * dv);
@@ -637,6 +686,21 @@ int or_fit(const double* x, const double* od, const double* w, int m, int dv, in
       }
       free(y);
     }
+  }
+  if (ridge_only) {
+    /* the ridge estimator alone (Table probe_estimator_ablation): Psi = I,
+     * so the correction map is B_lambda itself (psi holds the first r
+     * columns of I) */
+    for (int i = 0; i < dv && i < r; ++i) psi[i * r + i] = 1.0;
+    *rank = dv;
+    if (status == 0) memcpy(g, b, sizeof(double) * (size_t)dv * dv);
+    free(rhs);
+    free(s);
+    free(wt);
+    free(rb);
+    free(xb);
+    free(res);
+    return status;
   }
   /* eq. app_probe_residual_basis: right singular vectors of W^1/2 Rbar are
    * the eigenvectors of (W^1/2 Rbar)^T (W^1/2 Rbar); sigma = sqrt(eigenvalue).
@@ -722,8 +786,8 @@ void or_key_metric_pooled(const float* q, int nqh, int n, int d, int m_s, double
   free(one);
 }
 
-void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, double eps,
-                       float* phi) {
+void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, int rms,
+                       double eps, float* phi) {
 #pragma omp parallel for schedule(static)
   for (int i = 0; i < n; ++i) {
     double acc[256];
@@ -738,8 +802,11 @@ void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, i
         y[c] = s;
         ss += s * s;
       }
-      double den = sqrt(ss / (double)r); /* eq. query_response_feature */
-      if (den < eps) den = eps;
+      double den = 1.0;
+      if (rms) { /* eq. query_response_feature */
+        den = sqrt(ss / (double)r);
+        if (den < eps) den = eps;
+      }
       for (int c = 0; c < r; ++c) acc[c] += y[c] / den;
     }
     for (int c = 0; c < r; ++c) phi[(size_t)i * r + c] = (float)(acc[c] / (double)nqh);
@@ -764,7 +831,8 @@ void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* 
 }
 
 int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
-            int r_q, int ck, int cq, int iters, double density, int m, int32_t* labels_q,
+            int r_q, int ck, int cq, int iters, double density, int m, int partition,
+            int probe_rule, uint32_t probe_seed, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk_out,
             double* fq_out, float* phik_out, float* phiq_out, float* kbar_out, float* qbar_out,
             float* cqphi_out, float* prio_out, int64_t* stats) {
@@ -776,6 +844,9 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
     memcpy(qv + (size_t)h * nv * d, q + ((size_t)h * n + n_text) * d, sizeof(float) * (size_t)nv * d);
   if (r_k > d) r_k = d;
   if (r_q > d) r_q = d;
+  /* the semantic partitions cluster the raw rows (Sec. 3.1, Sec. 5.2) */
+  if (partition == 1) r_k = d;
+  if (partition != 0) r_q = d;
   const int cq_t = cq + (n_text > 0), ck_t = ck + (n_text > 0);
   const double tau = 1e-6;
 
@@ -786,8 +857,13 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
   float* centk = (float*)malloc(sizeof(float) * (size_t)ck * r_k);
   int32_t* labk = (int32_t*)malloc(sizeof(int32_t) * nv);
   int32_t* cntk = (int32_t*)malloc(sizeof(int32_t) * ck);
-  or_key_metric_pooled(qv, nqh, nv, d, m_s, mk);
-  or_response_basis(mk, d, r_k, tau, fk, NULL);
+  if (partition == 1) { /* semantic K/V groups: phi_K = k */
+    memset(mk, 0, sizeof(double) * (size_t)d * d);
+    for (int a = 0; a < d * d; ++a) fk[a] = (a / d == a % d) ? 1.0 : 0.0;
+  } else {
+    or_key_metric_pooled(qv, nqh, nv, d, m_s, mk);
+    or_response_basis(mk, d, r_k, tau, fk, NULL);
+  }
   or_project(kv, nv, d, fk, r_k, 0, 0.0, phik);
   const int itk = or_kmeans(phik, nv, r_k, ck, iters, labk, centk, cntk);
 
@@ -801,9 +877,15 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
   int32_t* cntq = (int32_t*)malloc(sizeof(int32_t) * cq);
   int32_t* cnt_dummy = (int32_t*)malloc(sizeof(int32_t) * ck);
   or_group_mean(kv, nv, d, labk, ck, kbar, cnt_dummy);
-  or_query_metric(kbar, cntk, ck, d, mq);
-  or_response_basis(mq, d, r_q, tau, fq, NULL);
-  or_project_pooled(qv, nqh, nv, d, fq, r_q, 1e-6, phiq);
+  if (partition == 0) {
+    or_query_metric(kbar, cntk, ck, d, mq);
+    or_response_basis(mq, d, r_q, tau, fq, NULL);
+    or_project_pooled(qv, nqh, nv, d, fq, r_q, 1, 1e-6, phiq);
+  } else { /* semantic query groups: phi_Q = q (pooled over the query heads) */
+    memset(mq, 0, sizeof(double) * (size_t)d * d);
+    for (int a = 0; a < d * d; ++a) fq[a] = (a / d == a % d) ? 1.0 : 0.0;
+    or_project_pooled(qv, nqh, nv, d, fq, r_q, 0, 0.0, phiq);
+  }
   const int itq = or_kmeans(phiq, nv, r_q, cq, iters, labq, centq, cntq);
 
   /* Routing (Sec. 4.3) */
@@ -821,7 +903,13 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
   or_route_select(prio, cntq, cq, cntk, ck, budget, zv, rs);
 
   /* Probes (App. A.2) */
-  const int np = or_probe_select(phiq, nv, r_q, labq, cq, centq, m, probes, w);
+  int np;
+  if (probe_rule == 1)
+    np = or_probe_random(nv, m, probe_seed, probes, w);
+  else if (probe_rule == 2)
+    np = or_probe_uniform(nv, m, probes, w);
+  else
+    np = or_probe_select(phiq, nv, r_q, labq, cq, centq, m, probes, w);
   for (int p = 0; p < np; ++p) probes[p] += n_text;
 
   /* Assemble labels and the full route matrix.  Reading for text tokens:
@@ -886,7 +974,7 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
 int or_attend(const float* q, const float* k, const float* v, int n, int d, int dv, int n_text,
               const int32_t* labels_q, const int32_t* labels_kv, int cq_t, int ck_t,
               const uint8_t* z, const int32_t* probes, const double* w, int m, int r,
-              double lambda, double eps, double* out, double* fit_out) {
+              int ridge_only, double lambda, double eps, double* out, double* fit_out) {
   (void)cq_t;
   int64_t* rows = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
   for (int i = 0; i < n; ++i) rows[i] = i;
@@ -908,7 +996,8 @@ int or_attend(const float* q, const float* k, const float* v, int n, int d, int 
   double* g = (double*)malloc(sizeof(double) * (size_t)dv * dv);
   double* psi = (double*)malloc(sizeof(double) * (size_t)dv * (r > 0 ? r : 1));
   int rank = 0;
-  const int st = or_fit(x, od, w, m, dv, r, lambda, eps, mu_x, s_x, mu_r, b, psi, g, &rank);
+  const int st =
+      or_fit(x, od, w, m, dv, r, ridge_only, lambda, eps, mu_x, s_x, mu_r, b, psi, g, &rank);
   /* eq. final_reconstructed_output; text rows are exact already */
   const int nv = n - n_text;
   if (m > 0) {

@@ -126,11 +126,25 @@ int or_probe_select(const float* phi, int n, int r, const int32_t* labels, int c
  * x, od: m x dv (sparse and dense outputs of the probes), w: coverage weights.
  * Outputs mu_x, s_x, mu_r (dv), b (dv x dv, the ridge solution),
  * psi (dv x r, columns beyond *rank are 0), g = b psi psi^T (dv x dv).
+ * ridge_only: the estimator without the probe-residual subspace (Table
+ * probe_estimator_ablation): Psi = I, g = b, *rank = dv (pass r = dv). 
  * Returns 0, or 1 when the regularised normal matrix is not positive
  * definite (then b = g = 0). */
 int or_fit(const double* x, const double* od, const double* w, int m, int dv, int r,
-           double lambda, double eps, double* mu_x, double* s_x, double* mu_r, double* b,
-           double* psi, double* g, int* rank);
+           int ridge_only, double lambda, double eps, double* mu_x, double* s_x, double* mu_r,
+           double* b, double* psi, double* g, int* rank);
+
+/* Probe rules of the ablation (Sec. 5.2, Table probe_estimator_ablation),
+ * over rows [0, n), equal weights n / m (as float):
+ *   or_probe_uniform: rows floor((2i + 1) n / (2m)), i < m (evenly spaced in
+ *     the raster token order);
+ *   or_probe_random: the m rows with the smallest or_splitmix64(seed * 2^32 +
+ *     row) (the SplitMix64 mixing function of Steele, Lea and Flood 2014), in
+ *     increasing key order.
+ * Return the number of probes, min(m, n). */
+uint64_t or_splitmix64(uint64_t x);
+int or_probe_uniform(int n, int m, int32_t* probes, double* w);
+int or_probe_random(int n, int m, uint32_t seed, int32_t* probes, double* w);
 
 /* Corrected rows (eq. probe_residual_estimate): out = x + mu_r + ((x-mu_x)/s_x) g. */
 void or_correct_rows(const double* x, int n_rows, int dv, const double* mu_x, const double* s_x,
@@ -155,9 +169,16 @@ void or_correct_rows(const double* x, int n_rows, int dv, const double* mu_x, co
  * plan pools them -- M_K is the mean of their metrics (or_key_metric_pooled),
  * phi_Q the mean of their normalised coordinates (or_project_pooled), and
  * the query-group means feeding the route scores the mean over heads and
- * members (or_group_mean_pooled).  nqh = 1 is the single-head plan. */
+ * members (or_group_mean_pooled).  nqh = 1 is the single-head plan.
+ *
+ * Ablation variants (Sec. 5.2): partition 0 = response-coupled, 1 = semantic
+ * (k-means on the raw keys and on the raw queries, Sec. 3.1; r_k = r_q = d),
+ * 2 = key-response K/V groups with semantic query groups (r_q = d);
+ * probe_rule 0 = or_probe_select, 1 = or_probe_random(probe_seed),
+ * 2 = or_probe_uniform. */
 int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
-            int r_q, int ck, int cq, int iters, double density, int m, int32_t* labels_q,
+            int r_q, int ck, int cq, int iters, double density, int m, int partition,
+            int probe_rule, uint32_t probe_seed, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk, double* fq,
             float* phik, float* phiq, float* kbar, float* qbar, float* cqphi, float* prio,
             int64_t* stats);
@@ -166,11 +187,12 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
  * consecutive n x d blocks of x (nqh = 1 gives the single-head functions):
  *   M_K = (1/nqh) sum_h Q_s,h^T Q_s,h / M_s;
  *   phi_i = (1/nqh) sum_h F^T x_h,i / max(sqrt(|F^T x_h,i|^2 / r), eps)
- *     (eq. query_response_feature per head, then averaged; float output);
+ *     (eq. query_response_feature per head, then averaged; float output;
+ *     rms = 0 leaves out the division);
  *   mean_b = sum_h sum_{j in b} x_h,j / (nqh |b|), 0 for an empty group. */
 void or_key_metric_pooled(const float* q, int nqh, int n, int d, int m_s, double* mk);
-void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, double eps,
-                       float* phi);
+void or_project_pooled(const float* x, int nqh, int n, int d, const double* f, int r, int rms,
+                       double eps, float* phi);
 void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* labels, int c,
                           float* mean);
 
@@ -182,7 +204,7 @@ void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* 
 int or_attend(const float* q, const float* k, const float* v, int n, int d, int dv, int n_text,
               const int32_t* labels_q, const int32_t* labels_kv, int cq_t, int ck_t,
               const uint8_t* z, const int32_t* probes, const double* w, int m, int r,
-              double lambda, double eps, double* out, double* fit_out);
+              int ridge_only, double lambda, double eps, double* out, double* fit_out);
 
 #ifdef __cplusplus
 }

@@ -194,6 +194,15 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "warm_start must be 0 or 1");
   if (p->warm_iters < 0 || p->warm_iters > p->kmeans_iters)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "warm_iters must be in [0, kmeans_iters]");
+  if (p->partition < SPARSEPR_PARTITION_RESPONSE || p->partition > SPARSEPR_PARTITION_KEY_RESPONSE)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "partition must be one of SPARSEPR_PARTITION_*");
+  if (p->probe_rule < SPARSEPR_PROBES_STRATIFIED || p->probe_rule > SPARSEPR_PROBES_UNIFORM)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "probe_rule must be one of SPARSEPR_PROBES_*");
+  if (p->ridge_only != 0 && p->ridge_only != 1)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "ridge_only must be 0 or 1");
+  if (p->probe_rule == SPARSEPR_PROBES_RANDOM && p->n_probes > 1024 &&
+      s->n_q - p->n_dense_prefix > 1024)
+    return fail(SPARSEPR_ERR_UNSUPPORTED, "the random probe rule takes at most 1024 probes");
   if (p->resid_rank < 1 || p->resid_rank > s->d_v)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "resid_rank must be in [1, d_v]");
   if (!(p->target_exec_density > 0.f) || !(p->target_exec_density <= 1.f))
@@ -212,8 +221,13 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.NV = NV;
   g.d = s->d;
   g.dv = s->d_v;
-  g.rk = std::min(p->r_k, s->d);
-  g.rq = std::min(p->r_q, s->d);
+  g.partition = p->partition;
+  g.probe_rule = p->probe_rule;
+  g.probe_seed = p->probe_seed;
+  g.ridge_only = p->ridge_only;
+  // the semantic partitions cluster the raw d-dimensional rows
+  g.rk = p->partition == SPARSEPR_PARTITION_SEMANTIC ? s->d : std::min(p->r_k, s->d);
+  g.rq = p->partition != SPARSEPR_PARTITION_RESPONSE ? s->d : std::min(p->r_q, s->d);
   g.CK = CK;
   g.CQ = CQ;
   g.CKt = CK + (g.ntext > 0);
@@ -223,7 +237,7 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.warm = p->warm_start;
   g.T_warm = p->warm_iters > 0 ? p->warm_iters : p->kmeans_iters;
   g.M = std::min(p->n_probes, NV);
-  g.r = p->resid_rank;
+  g.r = p->ridge_only ? s->d_v : p->resid_rank;  // ridge only: Psi = I, all d_v directions
   g.bf16 = s->dtype == SPARSEPR_BF16;
   g.sb = s->stride_b;
   g.sh = s->stride_h;
@@ -329,6 +343,10 @@ void sparsepr_params_default(sparsepr_params* p) {
   p->n_dense_prefix = 0;
   p->warm_start = 0;
   p->warm_iters = 0;
+  p->partition = SPARSEPR_PARTITION_RESPONSE;
+  p->probe_rule = SPARSEPR_PROBES_STRATIFIED;
+  p->probe_seed = 0;
+  p->ridge_only = 0;
 }
 
 sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const sparsepr_params* params,

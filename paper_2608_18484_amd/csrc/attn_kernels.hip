@@ -843,35 +843,46 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   const double* Sg = w.fitgram + ((size_t)bq * 2 + 1) * D * D;
   T* Am = (T*)smem;
   T* Vm = VG ? (T*)(w.fitvec + (size_t)bq * D * LV) : Am + D * LD;  // transposed (jacobi_eig_lds)
-  for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
-  __syncthreads();
-  jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
-  if (tid < D) {
-    const T li = Am[tid * LD + tid];
-    int rank = 0;
-    for (int j = 0; j < D; ++j) {
-      const T lj = Am[j * LD + j];
-      rank += (lj > li) || (lj == li && j < tid);
+  if (g.ridge_only) {
+    // ridge estimator alone (Table probe_estimator_ablation): Psi = I
+    for (int e = tid; e < D * D; e += 1024) Vm[(e / D) * LV + (e % D)] = (e / D == e % D) ? T(1) : T(0);
+    if (tid < D) order[tid] = tid;
+    if (tid == 0) {
+      rank_s = D;
+      fail = 0;
     }
-    order[rank] = tid;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    const double l1 = Am[order[0] * LD + order[0]];
-    const double s1 = l1 > 0.0 ? sqrt(l1) : 0.0;
-    int rk = 0;
-    for (int t = 0; t < r && t < D; ++t) {
-      const double lt = Am[order[t] * LD + order[t]];
-      const double st = lt > 0.0 ? sqrt(lt) : 0.0;
-      if (s1 > 0.0 && st > 1e-6 * s1)
-        ++rk;
-      else
-        break;
+    __syncthreads();
+  } else {
+    for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
+    __syncthreads();
+    jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
+    if (tid < D) {
+      const T li = Am[tid * LD + tid];
+      int rank = 0;
+      for (int j = 0; j < D; ++j) {
+        const T lj = Am[j * LD + j];
+        rank += (lj > li) || (lj == li && j < tid);
+      }
+      order[rank] = tid;
     }
-    rank_s = rk;
-    fail = 0;
+    __syncthreads();
+    if (tid == 0) {
+      const double l1 = Am[order[0] * LD + order[0]];
+      const double s1 = l1 > 0.0 ? sqrt(l1) : 0.0;
+      int rk = 0;
+      for (int t = 0; t < r && t < D; ++t) {
+        const double lt = Am[order[t] * LD + order[t]];
+        const double st = lt > 0.0 ? sqrt(lt) : 0.0;
+        if (s1 > 0.0 && st > 1e-6 * s1)
+          ++rk;
+        else
+          break;
+      }
+      rank_s = rk;
+      fail = 0;
+    }
+    __syncthreads();
   }
-  __syncthreads();
   const int rk = rank_s;
   for (int i = tid; i < D * rk; i += 1024) {
     const int row = i / rk, t = i % rk;

@@ -146,16 +146,17 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 // Response coordinates phi = F^T x (eq. key_response_feature), optionally
 // divided by max(RMS, eps) (eq. query_response_feature).  64 rows per block;
 // thread (ty, tx) computes rows ty + 16u (u < 4) x columns [tx*CPT, tx*CPT +
-// CPT), so each LDS read of F feeds four rows.  Keys (rms = 0) come from the
-// K/V head; queries (rms = 1) from its G query heads, whose normalised
-// coordinates are averaged (grouped-query attention shares one query
-// partition per K/V head; G = 1 is the single-head case).
+// CPT), so each LDS read of F feeds four rows.  Keys come from the K/V head;
+// queries (`query`) from its G query heads, whose (normalised) coordinates
+// are averaged (grouped-query attention shares one query partition per K/V
+// head; G = 1 is the single-head case).
 // ---------------------------------------------------------------------------
 
 template <int D, int MAXR>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
-                                                 int rms, float eps, float* phi, int64_t* stats,
-                                                 uint16_t* xhi, uint16_t* xlo, float* xn, int RP) {
+                                                 int query, int rms, float eps, float* phi,
+                                                 int64_t* stats, uint16_t* xhi, uint16_t* xlo,
+                                                 float* xn, int RP) {
   constexpr int ROWS = 64, CPT = MAXR / 16;
   __shared__ float xs[ROWS][D + 1];
   __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
@@ -171,14 +172,14 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
     }
   }
   const int ty = tid >> 4, tx = tid & 15;
-  const int nsrc = rms ? g.G : 1;
+  const int nsrc = query ? g.G : 1;
   float pooled[4][CPT];
 #pragma unroll
   for (int u = 0; u < 4; ++u)
 #pragma unroll
     for (int c = 0; c < CPT; ++c) pooled[u][c] = 0.f;
   for (int j = 0; j < nsrc; ++j) {
-    const int64_t base = rms ? q_base(g, bh, j) : kv_base(g, bh);
+    const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
     if (j > 0) __syncthreads();
     for (int i = tid; i < ROWS * D / 8; i += 256) {
       const int rr = i / (D / 8), c8 = i % (D / 8);
@@ -1324,10 +1325,111 @@ __global__ __launch_bounds__(256) void k_probe_select(Geom g, Work w) {
   }
 }
 
-// Coverage weights of imported probes: w_p = |G_a| / m_a.
+// Probe rules other than the stratified one (Table probe_estimator_ablation),
+// both with equal weights w_p = n_v / M.
+// UNIFORM: evenly spaced video rows floor((2i + 1) n_v / (2M)).
+__global__ __launch_bounds__(256) void k_probe_uniform(Geom g, Work w) {
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int M = g.M;  // <= n_v, so the rows are distinct
+  for (int i = tid; i < M; i += 256) {
+    w.probes[(size_t)bh * M + i] = g.ntext + (int)(((int64_t)(2 * i + 1) * g.NV) / (2 * (int64_t)M));
+    w.pw[(size_t)bh * M + i] = (float)g.NV / (float)M;
+  }
+  if (tid == 0) {
+    w.nprobes[bh] = M;
+    w.stats[(size_t)bh * 16 + ST_NPROBES] = M;
+  }
+}
+
+// The mixing function of SplitMix64 (Steele, Lea and Flood 2014), a
+// bijection of 64-bit words.
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// RANDOM: the M video rows with the smallest keys SplitMix64(seed * 2^32 +
+// row), in key order -- a uniformly random M-subset in random order.  The
+// M-th smallest key is found by an 8-bit radix select (the keys of distinct
+// rows are distinct), then the M rows at or below it are ranked by key.
+__global__ __launch_bounds__(1024) void k_probe_random(Geom g, Work w) {
+  __shared__ int hist[256];
+  __shared__ uint64_t sel_key[1024];
+  __shared__ int sel_row[1024];
+  __shared__ int nsel;
+  __shared__ unsigned long long prefix_s;
+  __shared__ int need_s;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const int M = min(g.M, 1024);  // validated: M <= 1024 for this rule
+  const uint64_t seed = (uint64_t)g.probe_seed << 32;
+  if (tid == 0) {
+    prefix_s = 0;
+    need_s = M;
+    nsel = 0;
+  }
+  __syncthreads();
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    for (int b = tid; b < 256; b += 1024) hist[b] = 0;
+    __syncthreads();
+    const uint64_t prefix = prefix_s;
+    for (int i = tid; i < g.NV; i += 1024) {
+      const uint64_t k = splitmix64(seed | (uint32_t)i);
+      if (pass == 0 || (k >> (shift + 8)) == (prefix >> (shift + 8)))
+        atomicAdd(&hist[(int)((k >> shift) & 255)], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int need = need_s, cum = 0, digit = 255;
+      for (int b = 0; b < 256; ++b) {
+        if (cum + hist[b] >= need) {
+          digit = b;
+          break;
+        }
+        cum += hist[b];
+      }
+      need_s = need - cum;
+      prefix_s = prefix | ((uint64_t)digit << shift);
+    }
+    __syncthreads();
+  }
+  const uint64_t kth = prefix_s;  // the M-th smallest key
+  for (int i = tid; i < g.NV; i += 1024) {
+    const uint64_t k = splitmix64(seed | (uint32_t)i);
+    if (k <= kth) {
+      const int slot = atomicAdd(&nsel, 1);
+      if (slot < M) {
+        sel_key[slot] = k;
+        sel_row[slot] = i;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < M) {
+    const uint64_t k = sel_key[tid];
+    int rank = 0;
+    for (int o = 0; o < M; ++o) rank += sel_key[o] < k;
+    w.probes[(size_t)bh * g.M + rank] = g.ntext + sel_row[tid];
+    w.pw[(size_t)bh * g.M + rank] = (float)g.NV / (float)M;
+  }
+  if (tid == 0) {
+    w.nprobes[bh] = M;
+    w.stats[(size_t)bh * 16 + ST_NPROBES] = M;
+  }
+}
+
+// Weights of imported probes: coverage weights w_p = |G_a| / m_a for the
+// stratified rule, n_v / (number of probes) for the others.
 __global__ __launch_bounds__(256) void k_probe_weights(Geom g, Work w) {
   const int bh = blockIdx.x, tid = threadIdx.x;
   const int np = w.nprobes[bh];
+  if (g.probe_rule != SPARSEPR_PROBES_STRATIFIED) {
+    for (int p = tid; p < np; p += 256) w.pw[(size_t)bh * g.M + p] = (float)g.NV / (float)np;
+    if (tid == 0) w.stats[(size_t)bh * 16 + ST_NPROBES] = np;
+    return;
+  }
   const int32_t* lab = w.labq + (size_t)bh * g.N;
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
   for (int p = tid; p < np; p += 256) {
@@ -1412,7 +1514,8 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  k_km_fallback<MAXR><<<dim3(64, BH), 256, 0, s>>>(a, it);
+  // few points per head need the exact scan: a handful of blocks per head
+  k_km_fallback<MAXR><<<dim3(16, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm) {
@@ -1437,19 +1540,29 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm
 }
 
 template <int D>
-static void project(const Geom& g, const Work& w, const void* x, const float* F, int R, int rms,
-                    float eps, float* phi, hipStream_t s) {
+static void project(const Geom& g, const Work& w, const void* x, const float* F, int R, int query,
+                    int rms, float eps, float* phi, hipStream_t s) {
   const dim3 grid((g.NV + 63) / 64, g.BH);
   const int RP = (R + 15) / 16 * 16;
   if (R <= 32)
-    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
-                                          w.km_xn, RP);
+    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
+                                          w.km_xlo, w.km_xn, RP);
   else if (R <= 64)
-    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
-                                          w.km_xn, RP);
+    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
+                                          w.km_xlo, w.km_xn, RP);
   else
-    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo,
-                                           w.km_xn, RP);
+    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
+                                           w.km_xlo, w.km_xn, RP);
+}
+
+// The semantic partitions cluster the raw rows: coordinates phi = I^T x.
+__global__ __launch_bounds__(256) void k_identity_basis(float* F, double* gram, float* evals, int D) {
+  const int bh = blockIdx.x;
+  for (int i = threadIdx.x; i < D * D; i += 256) {
+    F[(size_t)bh * D * D + i] = (i / D == i % D) ? 1.f : 0.f;
+    gram[(size_t)bh * D * D + i] = 0.0;
+  }
+  for (int i = threadIdx.x; i < D; i += 256) evals[(size_t)bh * D + i] = 0.f;
 }
 
 template <int D>
@@ -1457,10 +1570,15 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
                    bool warm) {
   const int BH = g.BH;
   k_plan_init<<<BH, 64, 0, s>>>(g, w);
-  // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1)
-  k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
-  k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
-  project<D>(g, w, k, w.fk, g.rk, 0, 0.f, w.phik, s);
+  // Key-response coordinates and the paired K/V partition (Sec. 4.1, App. B.1);
+  // the semantic partition clusters the raw keys instead (Sec. 3.1)
+  if (g.partition == SPARSEPR_PARTITION_SEMANTIC) {
+    k_identity_basis<<<BH, 256, 0, s>>>(w.fk, w.gram_k, w.evals_k, D);
+  } else {
+    k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
+  }
+  project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
@@ -1468,9 +1586,15 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
                                                          w.kbar, 0);
-  k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
-  k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
-  project<D>(g, w, q, w.fq, g.rq, 1, g.eps_q, w.phiq, s);
+  if (g.partition == SPARSEPR_PARTITION_RESPONSE) {
+    k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
+    project<D>(g, w, q, w.fq, g.rq, 1, 1, g.eps_q, w.phiq, s);
+  } else {
+    // semantic query groups: k-means on the raw queries
+    k_identity_basis<<<BH, 256, 0, s>>>(w.fq, w.gram_q, w.evals_q, D);
+    project<D>(g, w, q, w.fq, g.rq, 1, 0, 0.f, w.phiq, s);
+  }
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
             w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
@@ -1494,8 +1618,14 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
   // Probes (App. A.2)
   if (g.M > 0) {
-    k_probe_d2<<<dim3((g.NV + 255) / 256, BH), 256, 0, s>>>(g, w);
-    k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
+    if (g.probe_rule == SPARSEPR_PROBES_STRATIFIED) {
+      k_probe_d2<<<dim3((g.NV + 255) / 256, BH), 256, 0, s>>>(g, w);
+      k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
+    } else if (g.probe_rule == SPARSEPR_PROBES_UNIFORM) {
+      k_probe_uniform<<<BH, 256, 0, s>>>(g, w);
+    } else {
+      k_probe_random<<<BH, 1024, 0, s>>>(g, w);
+    }
   }
   k_plan_stats<<<BH, 256, 0, s>>>(g, w, 1, warm ? g.T_warm : g.T);
 }

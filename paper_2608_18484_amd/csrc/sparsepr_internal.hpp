@@ -36,6 +36,10 @@ struct Geom {
   int T;                  // k-means iterations (cold start; sizes the per-iteration state)
   int T_warm;             // k-means iterations when warm-started (<= T)
   int warm;               // warm start requested
+  int partition;          // SPARSEPR_PARTITION_*
+  int probe_rule;         // SPARSEPR_PROBES_*
+  uint32_t probe_seed;    // seed of the random probe rule
+  int ridge_only;         // fit without the probe-residual subspace (Psi = I)
   int M;                  // probes per head, min(n_probes, NV)
   int r;                  // residual rank
   int bf16;               // 1: bf16 tensors, 0: fp32

@@ -38,7 +38,9 @@ class Params(ctypes.Structure):
                 ("resid_rank", ctypes.c_int32), ("ridge", ctypes.c_float),
                 ("eps_q", ctypes.c_float), ("eps_x", ctypes.c_float),
                 ("n_dense_prefix", ctypes.c_int32), ("warm_start", ctypes.c_int32),
-                ("warm_iters", ctypes.c_int32)]
+                ("warm_iters", ctypes.c_int32), ("partition", ctypes.c_int32),
+                ("probe_rule", ctypes.c_int32), ("probe_seed", ctypes.c_uint32),
+                ("ridge_only", ctypes.c_int32)]
 
 
 class Stats(ctypes.Structure):
@@ -109,6 +111,10 @@ class SparsePRError(RuntimeError):
 def _check(st):
     if st != 0:
         raise SparsePRError(st, lib().sparsepr_last_error().decode())
+
+
+PARTITION_RESPONSE, PARTITION_SEMANTIC, PARTITION_KEY_RESPONSE = 0, 1, 2
+PROBES_STRATIFIED, PROBES_RANDOM, PROBES_UNIFORM = 0, 1, 2
 
 
 def default_params(**kw) -> Params:
@@ -211,7 +217,12 @@ class SparsePR:
         sh, p = self.shape, self.params
         n, d, dv = sh.n_q, sh.d, sh.d_v
         nv = n - p.n_dense_prefix
-        rk, rq, r = min(p.r_k, d), min(p.r_q, d), p.resid_rank
+        rk, rq = min(p.r_k, d), min(p.r_q, d)
+        if p.partition == PARTITION_SEMANTIC:
+            rk = d
+        if p.partition != PARTITION_RESPONSE:
+            rq = d
+        r = dv if p.ridge_only else p.resid_rank
         m = max(self.m, 1)
         return {
             "labels_q": n, "labels_kv": n, "routes": self.cq_t * self.ck_t, "probes": m,
@@ -240,8 +251,13 @@ class SparsePR:
         _check(lib().sparsepr_plan_export(self.handle, ctypes.c_int32(bh), ctypes.byref(ph),
                                           _stream(stream)))
         sh, p = self.shape, self.params
-        d, dv, r = sh.d, sh.d_v, p.resid_rank
+        d, dv = sh.d, sh.d_v
+        r = dv if p.ridge_only else p.resid_rank
         rk, rq = min(p.r_k, d), min(p.r_q, d)
+        if p.partition == PARTITION_SEMANTIC:
+            rk = d
+        if p.partition != PARTITION_RESPONSE:
+            rq = d
         npr = ph.n_probes
         shapes = {"routes": (self.cq_t, self.ck_t), "m_k": (d, d), "m_q": (d, d),
                   "f_k": (d, rk), "f_q": (d, rq), "phi_k": (-1, rk), "phi_q": (-1, rq),

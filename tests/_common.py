@@ -29,7 +29,8 @@ def oracle_kwargs(p):
     return dict(n_text=p.n_dense_prefix, n_sampled=p.n_sampled_queries, r_k=p.r_k, r_q=p.r_q,
                 c_k=p.n_kv_groups, c_q=p.n_q_groups, iters=p.kmeans_iters,
                 density=float(np.float32(p.target_exec_density)), n_probes=p.n_probes,
-                r=p.resid_rank, lam=float(np.float32(p.ridge)))
+                r=p.resid_rank, lam=float(np.float32(p.ridge)), partition=p.partition,
+                probe_rule=p.probe_rule, probe_seed=p.probe_seed, ridge_only=p.ridge_only)
 
 
 def to_device(q, k, v, dtype):

@@ -101,6 +101,11 @@ def test_workspace_size_ok_and_monotone():
     ({}, dict(ridge=-1.0), 1, "ridge"),
     ({}, dict(n_dense_prefix=1024), 1, "n_dense_prefix"),
     ({}, dict(kmeans_iters=0), 1, "kmeans_iters"),
+    ({}, dict(partition=3), 1, "partition"),
+    ({}, dict(probe_rule=-1), 1, "probe_rule"),
+    ({}, dict(ridge_only=2), 1, "ridge_only"),
+    (dict(n_q=4096, n_kv=4096, stride_b=4096 * 64, stride_h=4096 * 64), dict(probe_rule=1, n_probes=2000),
+     2, "random probe rule"),
     (dict(heads=4, stride_b=4 * 65536, heads_kv=3), {}, 1, "heads_kv"),
     (dict(heads=4, stride_b=4 * 65536, heads_kv=-1), {}, 1, "heads_kv"),
     (dict(heads=4, stride_b=4 * 65536, heads_kv=2), {}, 1, "kv_stride"),

@@ -98,7 +98,8 @@ def _replay(orc, r, ex, b, h):
     kw = oracle_kwargs(p)
     ref, fit = orc.attend(r["q"][b, h], r["k"][b, h], r["v"][b, h], ex["labels_q"], ex["labels_kv"],
                           ex["routes"], ex["probes"], ex["probe_weights"].astype(np.float64),
-                          n_text=kw["n_text"], r=kw["r"], lam=kw["lam"], eps=float(np.float32(p.eps_x)))
+                          n_text=kw["n_text"], r=r["q"].shape[-1] if p.ridge_only else kw["r"],
+                          lam=kw["lam"], eps=float(np.float32(p.eps_x)), ridge_only=bool(p.ridge_only))
     return ref, fit
 
 
@@ -362,3 +363,52 @@ def test_gqa_pooled_plan_and_outputs(orc, dtype, d):
     assert st["routed_pairs"] == pairs
     assert st["exec_pairs"] == pairs + st["n_probes"] * n
     assert st["n_probes"] == g * hkv * min(p.n_probes, n)
+
+
+@pytest.mark.parametrize("partition,probe_rule,ridge_only", [
+    (1, 0, 0),   # semantic partition (Sec. 3.1 reference)
+    (2, 0, 0),   # key-response K/V groups, semantic query groups
+    (0, 1, 0),   # random probes
+    (0, 2, 0),   # uniform spatiotemporal probes
+    (0, 0, 1),   # ridge estimator without the probe-residual subspace
+])
+def test_ablation_variants(orc, partition, probe_rule, ridge_only):
+    """Sec. 5.2 ablations: the plan stages bit-exact against the oracle on the
+    GPU's own float inputs, and the output against the oracle's replay."""
+    wl = medium(heads=1)
+    r = _run(wl, partition=partition, probe_rule=probe_rule, probe_seed=7, ridge_only=ridge_only)
+    p, op = r["p"], r["op"]
+    ex = op.export(0)
+    q, k = r["q"][0, 0], r["k"][0, 0]
+    n, d = q.shape
+    ck, cq, iters = p.n_kv_groups, p.n_q_groups, p.kmeans_iters
+    if partition == 1:  # the raw keys are the K/V coordinates
+        assert np.array_equal(ex["phi_k"], k)
+    else:
+        assert rel_l2(ex["m_k"], orc.key_metric(q, p.n_sampled_queries)) < 1e-5
+    lab_k, cent_k, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, iters)
+    assert np.array_equal(ex["labels_kv"], lab_k) and np.array_equal(ex["cent_k"], cent_k)
+    kbar, _ = orc.group_mean(k, lab_k, ck)
+    assert np.array_equal(ex["kbar"], kbar)
+    if partition != 0:  # the raw queries are the query coordinates
+        assert np.array_equal(ex["phi_q"], q)
+    lab_q, cent_q, cnt_q, _ = orc.kmeans(ex["phi_q"], cq, iters)
+    assert np.array_equal(ex["labels_q"], lab_q) and np.array_equal(ex["cent_q"], cent_q)
+    assert np.array_equal(ex["qbar"], orc.group_mean(q, lab_q, cq)[0])
+    m = min(p.n_probes, n)
+    budget = int(np.floor(float(np.float32(p.target_exec_density)) * n * n)) - m * n
+    z, _ = orc.route_select(ex["route_prio"], cnt_q, cnt_k, budget)
+    assert np.array_equal(ex["routes"], z)
+    if probe_rule == 1:
+        probes, w = orc.probe_random(n, p.n_probes, 7)
+    elif probe_rule == 2:
+        probes, w = orc.probe_uniform(n, p.n_probes)
+    else:
+        probes, w = orc.probe_select(ex["phi_q"], lab_q, ex["cent_q"], p.n_probes)
+    assert np.array_equal(ex["probes"], probes)
+    assert np.allclose(ex["probe_weights"], w, rtol=1e-6)
+    ref, fit = _replay(orc, r, ex, 0, 0)
+    if ridge_only:
+        assert ex["fit_rank"] == d
+    err = rel_l2(r["out"][0, 0], ref)
+    assert err < 2e-2, err

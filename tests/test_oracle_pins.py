@@ -695,3 +695,99 @@ def test_gqa_plan_of_duplicated_heads_is_single_head_plan(orc):
     p2 = orc.plan(np.stack([q, q]), k, **kw)
     for key in ("labels_q", "labels_kv", "z", "probes", "w"):
         assert np.array_equal(p1[key], p2[key]), key
+
+
+# --------------------------------------------------------------------------
+# Ablation variants (Sec. 5.2; Tables partition_repair_ablation and
+# probe_estimator_ablation)
+# --------------------------------------------------------------------------
+
+def test_splitmix64_is_a_bijection_on_a_sample():
+    # the mixing function is a composition of invertible steps (xor-shifts and
+    # odd multipliers mod 2^64): distinct inputs give distinct keys; undo the
+    # steps with the modular inverses of the multipliers to recover inputs
+    import oracle as orc_mod
+    m1, m2 = 0xBF58476D1CE4E5B9, 0x94D049BB133111EB
+    inv1, inv2 = pow(m1, -1, 1 << 64), pow(m2, -1, 1 << 64)
+
+    def unxorshift(y, s):
+        x = y
+        for _ in range(64 // s + 1):
+            x = y ^ (x >> s)
+        return x
+
+    for x in [0, 1, 2, 12345, (7 << 32) | 99, (1 << 64) - 1]:
+        z = orc_mod.splitmix64(x)
+        z = unxorshift(z, 31)
+        z = (z * inv2) % (1 << 64)
+        z = unxorshift(z, 27)
+        z = (z * inv1) % (1 << 64)
+        z = unxorshift(z, 30)
+        assert (z - 0x9E3779B97F4A7C15) % (1 << 64) == x
+
+
+def test_random_probes_are_a_uniform_subset(orc):
+    n, m = 500, 40
+    counts = np.zeros(n)
+    for seed in range(200):
+        p, w = orc.probe_random(n, m, seed)
+        assert len(set(p.tolist())) == m and p.min() >= 0 and p.max() < n
+        assert np.allclose(w, n / m)
+        counts[p] += 1
+    # each row is drawn with probability m / n: chi-square over 200 draws
+    exp = 200 * m / n
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    assert chi2 < n + 6 * math.sqrt(2 * n)
+    # different seeds give different subsets; all rows when m >= n
+    assert not np.array_equal(orc.probe_random(n, m, 1)[0], orc.probe_random(n, m, 2)[0])
+    assert sorted(orc.probe_random(30, 50, 3)[0].tolist()) == list(range(30))
+
+
+def test_uniform_probes_are_evenly_spaced(orc):
+    for n, m in [(1000, 64), (97, 10), (64, 64), (10, 32)]:
+        p, w = orc.probe_uniform(n, m)
+        k = min(n, m)
+        assert len(p) == k and np.all(np.diff(p) >= 1)
+        # one probe in each of the k equal slices of the rows
+        assert np.array_equal((p * k) // n, np.arange(k))
+        assert np.allclose(w, n / k)
+
+
+def test_ridge_only_is_the_plain_ridge_fit(orc):
+    # Psi = I: the correction map is the ridge solution of all d_v outputs,
+    # which numpy's least squares on the augmented system also gives
+    rng = np.random.default_rng(41)
+    m, dv, lam = 30, 12, 0.05
+    x = rng.standard_normal((m, dv))
+    od = x + 0.1 * rng.standard_normal((m, dv))
+    w = rng.uniform(0.5, 2.0, m)
+    ft = orc.fit(x, od, w, dv, lam, ridge_only=True)
+    al = w / w.sum()
+    mu_x, res = al @ x, od - x
+    mu_r = al @ res
+    s_x = np.sqrt(al @ (x - mu_x) ** 2 + 1e-6)
+    xb, rb = (x - mu_x) / s_x, res - mu_r
+    wt = m * w / w.sum()
+    a = np.vstack([np.sqrt(wt)[:, None] * xb, math.sqrt(lam) * np.eye(dv)])
+    bb = np.vstack([np.sqrt(wt)[:, None] * rb, np.zeros((dv, dv))])
+    ref = np.linalg.lstsq(a, bb, rcond=None)[0]
+    assert ft["rank"] == dv
+    assert np.max(np.abs(ft["g"] - ref)) < 1e-10 * np.max(np.abs(ref))
+
+
+def test_semantic_partition_clusters_the_raw_rows(orc):
+    q, k, v = tiny_head()
+    kw = {key: TINY[key] for key in ("n_sampled", "r_k", "r_q", "c_k", "c_q", "iters", "density",
+                                     "n_probes")}
+    sem = orc.plan(q, k, partition=1, **kw)
+    # K/V groups: k-means on the keys; query groups: k-means on the queries
+    assert np.array_equal(sem["labels_kv"], orc.kmeans(k, 16, 8)[0])
+    assert np.array_equal(sem["labels_q"], orc.kmeans(q, 16, 8)[0])
+    # the K/V partition of the semantic plan does not look at the queries
+    sem2 = orc.plan(2.0 * q[::-1].copy(), k, partition=1, **kw)
+    assert np.array_equal(sem["labels_kv"], sem2["labels_kv"])
+    # key-response: the response-coupled K/V groups with semantic query groups
+    resp = orc.plan(q, k, **kw)
+    kr = orc.plan(q, k, partition=2, **kw)
+    assert np.array_equal(kr["labels_kv"], resp["labels_kv"])
+    assert np.array_equal(kr["labels_q"], sem["labels_q"])
