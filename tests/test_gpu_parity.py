@@ -227,7 +227,7 @@ def test_independent_plan_agreement(orc):
     r = _run(wl)
     ex = r["op"].export(0, fields=["labels_q", "labels_kv", "routes"])
     pl = orc.plan(r["q"][0, 0], r["k"][0, 0], **{k: v for k, v in oracle_kwargs(r["p"]).items()
-                                                 if k not in ("r", "lam")})
+                                                 if k not in ("r", "lam", "ridge_only")})
     agree_k = np.mean(ex["labels_kv"] == pl["labels_kv"])
     print(f"label agreement kv={agree_k:.4f}")
     assert agree_k > 0.5
