@@ -129,6 +129,9 @@ def main():
                          "semantic query groups")
     ap.add_argument("--probe-rule", default="stratified", choices=["stratified", "random", "uniform"],
                     help="probe-selection ablation (Table probe_estimator_ablation)")
+    ap.add_argument("--routing", default="priority", choices=["priority", "top-p"],
+                    help="routing rule: cost-aware greedy on the cell priorities (the default "
+                         "reading) or per-group top-p with one p fitted to the budget")
     ap.add_argument("--ridge-only", action="store_true",
                     help="estimator ablation: ridge fit without the probe-residual subspace")
     ap.add_argument("--n-probes", type=int, default=-1,
@@ -157,6 +160,7 @@ def main():
     p.partition = {"response": 0, "semantic": 1, "key-response": 2}[args.partition]
     p.probe_rule = {"stratified": 0, "random": 1, "uniform": 2}[args.probe_rule]
     p.ridge_only = int(args.ridge_only)
+    p.routing = {"priority": 0, "top-p": 1}[args.routing]
     if args.n_probes >= 0:
         p.n_probes = args.n_probes
     gqa = args.kv_heads > 0 and args.kv_heads != wl.heads
@@ -256,6 +260,7 @@ def main():
                    "q_groups": wl.groups()[1], "probes": p.n_probes, "resid_rank": wl.resid_rank,
                    "kv_heads": wl.batch * (args.kv_heads if gqa else wl.heads),
                    "partition": args.partition, "probe_rule": args.probe_rule,
+                   "routing": args.routing,
                    "estimator": "ridge only" if args.ridge_only else "ridge + probe-residual subspace",
                    "ridge": wl.ridge, "kmeans_iters": wl.kmeans_iters,
                    "kmeans_start": ("warm: 2 assignments from the previous call's centroids, "

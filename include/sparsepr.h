@@ -111,6 +111,7 @@ typedef struct {
   int32_t ridge_only;          /* 1: ridge estimator without the probe-residual
                                   output subspace (Psi = I, so the correction is
                                   xbar B_lambda); 0 */
+  int32_t routing;             /* SPARSEPR_ROUTING_*; PRIORITY */
 } sparsepr_params;
 
 /* partition: how the K/V and query groups are formed.
@@ -133,6 +134,21 @@ typedef struct {
  *               (tokens are in raster order, so these spread over space and
  *               time).
  * RANDOM and UNIFORM weigh every probe equally, w_p = n_v / M. */
+/* routing: which cells the pair budget buys (Sec. 4.3).  Both keep the best
+ * cell of every nonempty query group (forced) and walk the other cells in a
+ * fixed order, taking the longest prefix whose pair cost fits the budget.
+ *   PRIORITY  order of the centroid estimate of the per-pair log probability
+ *             pi_ab = s_ab - lse_a, descending (the cost-aware greedy);
+ *   TOP_P     per-group top-p with one p for all query groups, the largest
+ *             whose cost fits: a group takes its cells in pi order until their
+ *             estimated attention mass m_ab = |G_b| exp(pi_ab) (which sums to 1
+ *             over b) reaches p.  Cell (a, b) is in the top-p set exactly when
+ *             the mass ranked before it in its group, e_ab, is below p, so the
+ *             walk is in e_ab ascending order (e_ab in double, the group's
+ *             order being pi descending, b ascending).
+ * Ties in the walk go to the lower flat index a * C_k + b. */
+#define SPARSEPR_ROUTING_PRIORITY 0
+#define SPARSEPR_ROUTING_TOP_P 1
 #define SPARSEPR_PROBES_STRATIFIED 0
 #define SPARSEPR_PROBES_RANDOM 1
 #define SPARSEPR_PROBES_UNIFORM 2
@@ -204,6 +220,8 @@ typedef struct {
   float* fit_bpsi;       /* [d_v * r] B_lambda Psi_r (the ridge map times the basis) */
   float* fit_psi;        /* [d_v * r] Psi_r (columns beyond fit_rank are 0) */
   int32_t fit_rank;      /* export: retained residual rank */
+  float* route_key;      /* [C_q * C_k] key of the routing walk (larger first): route_prio
+                            under PRIORITY, -(float)e_ab under TOP_P (0 for empty groups) */
 } sparsepr_plan_host;
 
 typedef struct sparsepr_plan_s* sparsepr_plan_t;

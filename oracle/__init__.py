@@ -245,6 +245,15 @@ def route_select(prio, nq, nk, budget):
                "routed_cells": int(out[2]), "forced_cells": int(out[3])}
 
 
+def route_topp_keys(prio, nq, nk):
+    """Keys of the per-group top-p walk: -(mass ranked before each cell)."""
+    prio = _f32(prio)
+    cq, ck = prio.shape
+    keys = np.zeros((cq, ck), np.float32)
+    lib().or_route_topp_keys(_p(prio), _p(_i32(nq)), cq, _p(_i32(nk)), ck, _p(keys))
+    return keys
+
+
 def probe_select(phi, labels, cent, m):
     phi, cent = _f32(phi), _f32(cent)
     n, r = phi.shape
@@ -282,7 +291,7 @@ def correct_rows(x, ft):
 
 
 def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_probes,
-         partition=0, probe_rule=0, probe_seed=0):
+         partition=0, probe_rule=0, probe_seed=0, routing=0):
     """Whole Response-Coupled Partitioning + routing + probe choice for one
     K/V head.  q is [n, d], or [G, n, d] for the G query heads that share the
     K/V head under grouped-query attention (the plan pools them)."""
@@ -308,7 +317,7 @@ def plan(q, k, *, n_text=0, n_sampled, r_k, r_q, c_k, c_q, iters, density, n_pro
     }
     lib().or_plan(_p(q), nqh, _p(k), n, d, n_text, n_sampled, r_k, r_q, c_k, c_q, iters,
                   ctypes.c_double(density), n_probes, int(partition), int(probe_rule),
-                  ctypes.c_uint32(probe_seed), _p(out["labels_q"]), _p(out["labels_kv"]),
+                  ctypes.c_uint32(probe_seed), int(routing), _p(out["labels_q"]), _p(out["labels_kv"]),
                   _p(out["z"]), _p(out["probes"]), _p(out["w"]), _p(out["fk"]), _p(out["fq"]),
                   _p(out["phik"]), _p(out["phiq"]), _p(out["kbar"]), _p(out["qbar"]),
                   _p(out["cqphi"]), _p(out["prio"]), _p(out["stats"]))
@@ -348,7 +357,7 @@ def run(q, k, v, **params):
               r_k=params["r_k"], r_q=params["r_q"], c_k=params["c_k"], c_q=params["c_q"],
               iters=params["iters"], density=params["density"], n_probes=params["n_probes"],
               partition=params.get("partition", 0), probe_rule=params.get("probe_rule", 0),
-              probe_seed=params.get("probe_seed", 0))
+              probe_seed=params.get("probe_seed", 0), routing=params.get("routing", 0))
     ridge_only = bool(params.get("ridge_only", False))
     dv = np.shape(v)[-1]
     out, ft = attend(q, k, v, pl["labels_q"], pl["labels_kv"], pl["z"], pl["probes"], pl["w"],

@@ -448,6 +448,45 @@ void or_route_select(const float* prio, const int32_t* nq, int cq, const int32_t
   out[3] = forced_cells;
 }
 
+/* Per-group top-p routing with one p for every query group (the alternative
+ * reading of the routing rule, Sec. 4.3).  Row a's estimated attention mass on
+ * cell b is m_ab = nk_b exp(pi_ab); a group takes its cells in (pi descending,
+ * b ascending) order until their mass reaches p.  So cell (a, b) is taken
+ * exactly when the mass ranked before it, e_ab, is below p, and the largest p
+ * that fits the budget takes the longest prefix of the cells ordered by e_ab
+ * ascending: the walk of or_route_select on keys -e_ab (the best cell of each
+ * group has e = 0 and stays the forced one). */
+static const float* topp_prio_row;
+static int topp_cmp(const void* x, const void* y) {
+  const int a = *(const int*)x, b = *(const int*)y;
+  const float pa = topp_prio_row[a], pb = topp_prio_row[b];
+  if (pa > pb) return -1;
+  if (pa < pb) return 1;
+  return (a > b) - (a < b);
+}
+
+void or_route_topp_keys(const float* prio, const int32_t* nq, int cq, const int32_t* nk, int ck,
+                        float* keys) {
+  int* order = (int*)malloc(sizeof(int) * (ck > 0 ? ck : 1));
+  for (int a = 0; a < cq; ++a) {
+    float* out = keys + (size_t)a * ck;
+    for (int b = 0; b < ck; ++b) out[b] = 0.0f;
+    if (nq[a] == 0) continue;
+    int cnt = 0;
+    for (int b = 0; b < ck; ++b)
+      if (nk[b] > 0) order[cnt++] = b;
+    topp_prio_row = prio + (size_t)a * ck;
+    qsort(order, (size_t)cnt, sizeof(int), topp_cmp);
+    double e = 0.0;
+    for (int t = 0; t < cnt; ++t) {
+      const int b = order[t];
+      out[b] = -(float)e;
+      e += (double)nk[b] * exp((double)topp_prio_row[b]);
+    }
+  }
+  free(order);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Probe selection (App. A.2)                                                */
 /* ------------------------------------------------------------------------ */
@@ -832,7 +871,7 @@ void or_group_mean_pooled(const float* x, int nqh, int n, int d, const int32_t* 
 
 int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
             int r_q, int ck, int cq, int iters, double density, int m, int partition,
-            int probe_rule, uint32_t probe_seed, int32_t* labels_q,
+            int probe_rule, uint32_t probe_seed, int routing, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk_out,
             double* fq_out, float* phik_out, float* phiq_out, float* kbar_out, float* qbar_out,
             float* cqphi_out, float* prio_out, int64_t* stats) {
@@ -900,7 +939,14 @@ int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, i
   /* the probe rows' cost against all keys is reserved first */
   const int64_t budget = (int64_t)floor(density * (double)nv * (double)nv) - (int64_t)meff * n;
   int64_t rs[4];
-  or_route_select(prio, cntq, cq, cntk, ck, budget, zv, rs);
+  if (routing == 1) {
+    float* keys = (float*)malloc(sizeof(float) * (size_t)cq * ck);
+    or_route_topp_keys(prio, cntq, cq, cntk, ck, keys);
+    or_route_select(keys, cntq, cq, cntk, ck, budget, zv, rs);
+    free(keys);
+  } else {
+    or_route_select(prio, cntq, cq, cntk, ck, budget, zv, rs);
+  }
 
   /* Probes (App. A.2) */
   int np;

@@ -111,6 +111,14 @@ void or_route_priorities(const float* qbar, const int32_t* nq, int cq, const flo
 void or_route_select(const float* prio, const int32_t* nq, int cq, const int32_t* nk, int ck,
                      int64_t budget, uint8_t* z, int64_t* out);
 
+/* Keys of the per-group top-p routing walk (reading of Sec. 4.3, one p for
+ * every group, the largest that fits the budget): keys[a][b] = -(float)e_ab,
+ * e_ab = sum of nk_b' exp((double)prio[a][b']) over the nonempty b' ranked
+ * before b in (prio descending, b ascending) order, summed in that order.
+ * Routing by top-p is or_route_select on these keys.  0 for empty groups. */
+void or_route_topp_keys(const float* prio, const int32_t* nq, int cq, const int32_t* nk, int ck,
+                        float* keys);
+
 /* Query-group-stratified probe selection (App. A.2, Algorithm "Query-Group-
  * Stratified Exact Probe Selection") and coverage weights (eq. app_probe_weight).
  * Rows of a group are ordered by their squared distance to the group mean in
@@ -178,7 +186,7 @@ void or_correct_rows(const double* x, int n_rows, int dv, const double* mu_x, co
  * 2 = or_probe_uniform. */
 int or_plan(const float* q, int nqh, const float* k, int n, int d, int n_text, int m_s, int r_k,
             int r_q, int ck, int cq, int iters, double density, int m, int partition,
-            int probe_rule, uint32_t probe_seed, int32_t* labels_q,
+            int probe_rule, uint32_t probe_seed, int routing, int32_t* labels_q,
             int32_t* labels_kv, uint8_t* z, int32_t* probes, double* w, double* fk, double* fq,
             float* phik, float* phiq, float* kbar, float* qbar, float* cqphi, float* prio,
             int64_t* stats);

@@ -97,6 +97,7 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->kbar, (size_t)g.CK * d * 4);
   add(&w->qbar, (size_t)g.CQ * d * 4);
   add(&w->prio, (size_t)g.CQ * g.CK * 4);
+  add(&w->skey, g.routing == SPARSEPR_ROUTING_TOP_P ? (size_t)g.CQ * g.CK * 4 : 0);
   add(&w->forced, (size_t)g.CQ * 4);
   add(&w->selhist, (size_t)kSelPasses * kSelBins * 8);
   add(&w->selstate, 8 * 8);
@@ -200,6 +201,10 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "probe_rule must be one of SPARSEPR_PROBES_*");
   if (p->ridge_only != 0 && p->ridge_only != 1)
     return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "ridge_only must be 0 or 1");
+  if (p->routing != SPARSEPR_ROUTING_PRIORITY && p->routing != SPARSEPR_ROUTING_TOP_P)
+    return fail(SPARSEPR_ERR_INVALID_ARGUMENT, "routing must be one of SPARSEPR_ROUTING_*");
+  if (p->routing == SPARSEPR_ROUTING_TOP_P && CK > 4096)
+    return fail(SPARSEPR_ERR_UNSUPPORTED, "top-p routing takes at most 4096 K/V groups");
   if (p->probe_rule == SPARSEPR_PROBES_RANDOM && p->n_probes > 1024 &&
       s->n_q - p->n_dense_prefix > 1024)
     return fail(SPARSEPR_ERR_UNSUPPORTED, "the random probe rule takes at most 1024 probes");
@@ -225,6 +230,7 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   g.probe_rule = p->probe_rule;
   g.probe_seed = p->probe_seed;
   g.ridge_only = p->ridge_only;
+  g.routing = p->routing;
   // the semantic partitions cluster the raw d-dimensional rows
   g.rk = p->partition == SPARSEPR_PARTITION_SEMANTIC ? s->d : std::min(p->r_k, s->d);
   g.rq = p->partition != SPARSEPR_PARTITION_RESPONSE ? s->d : std::min(p->r_q, s->d);
@@ -347,6 +353,7 @@ void sparsepr_params_default(sparsepr_params* p) {
   p->probe_rule = SPARSEPR_PROBES_STRATIFIED;
   p->probe_seed = 0;
   p->ridge_only = 0;
+  p->routing = SPARSEPR_ROUTING_PRIORITY;
 }
 
 sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const sparsepr_params* params,
@@ -550,6 +557,8 @@ sparsepr_status sparsepr_plan_export(sparsepr_plan_t plan, int32_t bh, sparsepr_
       {out->kbar, h.kbar, (size_t)g.CK * d * 4, "kbar"},
       {out->qbar, h.qbar, (size_t)g.CQ * d * 4, "qbar"},
       {out->route_prio, h.prio, (size_t)g.CQ * g.CK * 4, "route_prio"},
+      {out->route_key, g.routing == SPARSEPR_ROUTING_TOP_P ? h.skey : h.prio,
+       (size_t)g.CQ * g.CK * 4, "route_key"},
       {out->o_sparse, h.osp, N * dv * 4, "o_sparse"},
       {out->o_dense_probes, h.odp, (size_t)np * dv * 4, "o_dense_probes"},
       {out->fit_mu_x, h.fitv, dv * 4, "fit_mu_x"},

@@ -971,6 +971,104 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
   }
 }
 
+// Top-p routing keys (SPARSEPR_ROUTING_TOP_P): for query group a, the cells
+// in (pi desc, b asc) order over nonempty K/V groups, and key(a, b) =
+// -(float)e_ab with e_ab the estimated attention mass ranked before b, the
+// sum of |G_b'| exp(pi_ab') in double.  One block per (a, head): the 64-bit
+// order keys are bitonic-sorted in LDS; each thread sums a contiguous run of
+// the sorted masses and a block scan of the run totals gives every prefix.
+// np2 = C_k rounded up to a power of two (dynamic LDS: np2 * 8 bytes).
+__global__ __launch_bounds__(256) void k_route_topp(Geom g, Work w, int np2) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char topp_lds[];
+  uint64_t* key = (uint64_t*)topp_lds;
+  __shared__ double run_tot[256];
+  const int a = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
+  const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
+  const float* pr = w.prio + ((size_t)bh * g.CQ + a) * g.CK;
+  float* out = w.skey + ((size_t)bh * g.CQ + a) * g.CK;
+  if (oq[a + 1] == oq[a]) {
+    for (int b = tid; b < g.CK; b += 256) out[b] = 0.f;
+    return;
+  }
+  // larger key first: priority descending, then b ascending; 0 = no cell
+  for (int i = tid; i < np2; i += 256) {
+    uint64_t k = 0;
+    if (i < g.CK && ok[i + 1] > ok[i])
+      k = ((uint64_t)float_order_bits(pr[i]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+    key[i] = k;
+  }
+  for (int b = tid; b < g.CK; b += 256)
+    if (ok[b + 1] == ok[b]) out[b] = 0.f;
+  __syncthreads();
+  for (int size = 2; size <= np2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < np2; i += 256) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool desc = (i & size) == 0;
+          const uint64_t ki = key[i], kj = key[j];
+          if (desc ? (ki < kj) : (ki > kj)) {
+            key[i] = kj;
+            key[j] = ki;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // thread t owns sorted positions [t * per, (t + 1) * per)
+  const int per = (np2 + 255) / 256;
+  const int i0 = min(tid * per, np2), i1 = min(i0 + per, np2);
+  auto mass_at = [&](int i, int& b) -> double {
+    const uint64_t k = key[i];
+    if (k == 0) {
+      b = -1;
+      return 0.0;
+    }
+    b = (int)(0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFu));
+    return (double)(ok[b + 1] - ok[b]) * exp((double)pr[b]);
+  };
+  double tot = 0.0;
+  for (int i = i0; i < i1; ++i) {
+    int b;
+    tot += mass_at(i, b);
+  }
+  run_tot[tid] = tot;
+  __syncthreads();
+  if (tid < 64) {  // exclusive scan of the 256 run totals by one wave
+    double v[4], t4 = 0.0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      v[u] = run_tot[tid * 4 + u];
+      t4 += v[u];
+    }
+    double incl = t4;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const double y = __shfl_up(incl, o);
+      if (tid >= o) incl += y;
+    }
+    const double before = __shfl_up(incl, 1);
+    double e = tid > 0 ? before : 0.0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const double next = e + v[u];
+      run_tot[tid * 4 + u] = e;
+      e = next;
+    }
+  }
+  __syncthreads();
+  double e = run_tot[tid];
+  for (int i = i0; i < i1; ++i) {
+    int b;
+    const double m = mass_at(i, b);
+    if (b < 0) break;
+    out[b] = -(float)e;
+    e += m;
+  }
+}
+
 // selstate slots.  SS_DONE: 0 searching, 1 every eligible cell fits,
 // 2 boundary key found (cells with larger keys are taken), 3 nothing beyond
 // the forced cells fits.
@@ -1041,7 +1139,7 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
   const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
-  const float* pr = w.prio + (size_t)bh * g.CQ * g.CK;
+  const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
   const int64_t ncell = (int64_t)g.CQ * g.CK;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + tid; idx < ncell; idx += (int64_t)gridDim.x * 256) {
     const int a = (int)(idx / g.CK), b = (int)(idx - (int64_t)a * g.CK);
@@ -1095,7 +1193,7 @@ __global__ __launch_bounds__(256) void k_sel_mark(Geom g, Work w) {
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
   const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
-  const float* pr = w.prio + (size_t)bh * g.CQ * g.CK;
+  const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
   uint8_t* z = w.z + (size_t)bh * g.CQt * g.CKt;
   const int64_t ncell = (int64_t)g.CQt * g.CKt;
   int cnt = 0;
@@ -1604,6 +1702,11 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Routing (Sec. 4.3)
   k_route_prio<D><<<dim3((g.CQ + 63) / 64, BH), 256, 0, s>>>(w.qbar, w.kbar, g, w.offq, w.offk,
                                                              w.prio, w.forced);
+  if (g.routing == SPARSEPR_ROUTING_TOP_P) {
+    int np2 = 1;
+    while (np2 < g.CK) np2 <<= 1;
+    k_route_topp<<<dim3(g.CQ, BH), 256, (size_t)np2 * 8, s>>>(g, w, np2);
+  }
   k_sel_init<<<BH, 256, 0, s>>>(g, w);
   const int64_t ncell = (int64_t)g.CQ * g.CK;
   const int gsel = (int)std::min<int64_t>(std::max<int64_t>((ncell + 4095) / 4096, 1), 512);

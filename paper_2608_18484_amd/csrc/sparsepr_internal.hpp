@@ -40,6 +40,7 @@ struct Geom {
   int probe_rule;         // SPARSEPR_PROBES_*
   uint32_t probe_seed;    // seed of the random probe rule
   int ridge_only;         // fit without the probe-residual subspace (Psi = I)
+  int routing;            // SPARSEPR_ROUTING_*
   int M;                  // probes per head, min(n_probes, NV)
   int r;                  // residual rank
   int bf16;               // 1: bf16 tensors, 0: fp32
@@ -89,6 +90,7 @@ struct Work {
   float* kbar;      // [BH][CK][d]
   float* qbar;      // [BH][CQ][d]
   float* prio;      // [BH][CQ][CK]
+  float* skey;      // [BH][CQ][CK] key of the routing walk (prio itself, or the top-p keys)
   int32_t* forced;  // [BH][CQ]
   uint64_t* selhist;  // [BH][kSelPasses][kSelBins]
   int64_t* selstate;  // [BH][8]

@@ -40,7 +40,7 @@ class Params(ctypes.Structure):
                 ("n_dense_prefix", ctypes.c_int32), ("warm_start", ctypes.c_int32),
                 ("warm_iters", ctypes.c_int32), ("partition", ctypes.c_int32),
                 ("probe_rule", ctypes.c_int32), ("probe_seed", ctypes.c_uint32),
-                ("ridge_only", ctypes.c_int32)]
+                ("ridge_only", ctypes.c_int32), ("routing", ctypes.c_int32)]
 
 
 class Stats(ctypes.Structure):
@@ -69,7 +69,7 @@ HOST_FIELDS = [
     ("phi_k", "f4"), ("phi_q", "f4"), ("cent_k", "f4"), ("cent_q", "f4"), ("kbar", "f4"),
     ("qbar", "f4"), ("route_prio", "f4"), ("o_sparse", "f4"), ("o_dense_probes", "f4"),
     ("fit_mu_x", "f4"), ("fit_s_x", "f4"), ("fit_mu_r", "f4"), ("fit_bpsi", "f4"),
-    ("fit_psi", "f4"), ("fit_rank", None),
+    ("fit_psi", "f4"), ("fit_rank", None), ("route_key", "f4"),
 ]
 
 
@@ -115,6 +115,7 @@ def _check(st):
 
 PARTITION_RESPONSE, PARTITION_SEMANTIC, PARTITION_KEY_RESPONSE = 0, 1, 2
 PROBES_STRATIFIED, PROBES_RANDOM, PROBES_UNIFORM = 0, 1, 2
+ROUTING_PRIORITY, ROUTING_TOP_P = 0, 1
 
 
 def default_params(**kw) -> Params:
@@ -230,7 +231,8 @@ class SparsePR:
             "off_kv": self.ck_t + 1, "m_k": d * d, "m_q": d * d, "f_k": d * rk, "f_q": d * rq,
             "phi_k": nv * rk, "phi_q": nv * rq, "cent_k": self.ck * rk, "cent_q": self.cq * rq,
             "kbar": self.ck * d, "qbar": self.cq * d, "route_prio": self.cq * self.ck,
-            "o_sparse": n * dv, "o_dense_probes": m * dv, "fit_mu_x": dv, "fit_s_x": dv,
+            "route_key": self.cq * self.ck, "o_sparse": n * dv, "o_dense_probes": m * dv,
+            "fit_mu_x": dv, "fit_s_x": dv,
             "fit_mu_r": dv, "fit_bpsi": dv * r, "fit_psi": dv * r,
         }
 
@@ -262,7 +264,8 @@ class SparsePR:
         shapes = {"routes": (self.cq_t, self.ck_t), "m_k": (d, d), "m_q": (d, d),
                   "f_k": (d, rk), "f_q": (d, rq), "phi_k": (-1, rk), "phi_q": (-1, rq),
                   "cent_k": (self.ck, rk), "cent_q": (self.cq, rq), "kbar": (self.ck, d),
-                  "qbar": (self.cq, d), "route_prio": (self.cq, self.ck), "o_sparse": (-1, dv),
+                  "qbar": (self.cq, d), "route_prio": (self.cq, self.ck),
+                  "route_key": (self.cq, self.ck), "o_sparse": (-1, dv),
                   "o_dense_probes": (-1, dv), "fit_bpsi": (dv, r), "fit_psi": (dv, r)}
         out = {}
         for name, arr in bufs.items():

@@ -30,7 +30,8 @@ def oracle_kwargs(p):
                 c_k=p.n_kv_groups, c_q=p.n_q_groups, iters=p.kmeans_iters,
                 density=float(np.float32(p.target_exec_density)), n_probes=p.n_probes,
                 r=p.resid_rank, lam=float(np.float32(p.ridge)), partition=p.partition,
-                probe_rule=p.probe_rule, probe_seed=p.probe_seed, ridge_only=p.ridge_only)
+                probe_rule=p.probe_rule, probe_seed=p.probe_seed, ridge_only=p.ridge_only,
+                routing=p.routing)
 
 
 def to_device(q, k, v, dtype):

@@ -104,6 +104,9 @@ def test_workspace_size_ok_and_monotone():
     ({}, dict(partition=3), 1, "partition"),
     ({}, dict(probe_rule=-1), 1, "probe_rule"),
     ({}, dict(ridge_only=2), 1, "ridge_only"),
+    ({}, dict(routing=2), 1, "routing"),
+    (dict(n_q=8192, n_kv=8192, stride_b=8192 * 64, stride_h=8192 * 64),
+     dict(routing=1, n_kv_groups=5000), 2, "top-p"),
     (dict(n_q=4096, n_kv=4096, stride_b=4096 * 64, stride_h=4096 * 64), dict(probe_rule=1, n_probes=2000),
      2, "random probe rule"),
     (dict(heads=4, stride_b=4 * 65536, heads_kv=3), {}, 1, "heads_kv"),

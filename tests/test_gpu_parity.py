@@ -412,3 +412,40 @@ def test_ablation_variants(orc, partition, probe_rule, ridge_only):
         assert ex["fit_rank"] == d
     err = rel_l2(r["out"][0, 0], ref)
     assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("ntext", [0, 96])
+def test_top_p_routing(orc, ntext):
+    """Per-group top-p routing (the alternative routing reading): the walk keys
+    against the oracle's on the GPU's priorities, the route set bit-exact given
+    the GPU's keys, the budget respected, and the output against the oracle's
+    replay."""
+    from paper_2608_18484_amd import sparsepr as S
+    wl = medium(heads=1)
+    if ntext:
+        wl = wl.with_(n_text=ntext)
+    r = _run(wl, routing=S.ROUTING_TOP_P)
+    p, op = r["p"], r["op"]
+    ex = op.export(0)
+    n = r["q"].shape[2]
+    nt = p.n_dense_prefix
+    ck, cq = p.n_kv_groups, p.n_q_groups
+    cnt_q = np.bincount(ex["labels_q"][nt:], minlength=cq)[:cq]
+    cnt_k = np.bincount(ex["labels_kv"][nt:], minlength=ck)[:ck]
+    keys = orc.route_topp_keys(ex["route_prio"], cnt_q, cnt_k)
+    assert np.max(np.abs(ex["route_key"] - keys)) < 1e-6
+    nv = n - nt
+    m = min(p.n_probes, nv)
+    budget = int(np.floor(float(np.float32(p.target_exec_density)) * nv * nv)) - m * n
+    z, st = orc.route_select(ex["route_key"], cnt_q, cnt_k, budget)
+    assert np.array_equal(ex["routes"][:cq, :ck], z)
+    assert st["routed_pairs"] <= max(budget, st["forced_pairs"])
+    # one threshold for all groups: no untaken cell has a larger key than a
+    # taken one of its group
+    live = np.flatnonzero(cnt_k)
+    for a in np.flatnonzero(cnt_q):
+        kk, tk = ex["route_key"][a, live], z[a, live].astype(bool)
+        assert tk.any() and (tk.all() or kk[tk].min() >= kk[~tk].max())
+    ref, _ = _replay(orc, r, ex, 0, 0)
+    err = rel_l2(r["out"][0, 0], ref)
+    assert err < 2e-2, err

@@ -624,6 +624,79 @@ def test_route_priorities_normalised(orc):
         assert np.array_equal(o1, o2)
 
 
+def _topp_case(orc, seed):
+    rng = np.random.default_rng(seed)
+    cq, ck = 6, 9
+    qbar = (2.0 * rng.standard_normal((cq, 16))).astype(np.float32)
+    kbar = rng.standard_normal((ck, 16)).astype(np.float32)
+    nq = rng.integers(1, 6, cq).astype(np.int32)
+    nk = rng.integers(1, 9, ck).astype(np.int32)
+    nq[2], nk[4] = 0, 0  # an empty query group and an empty K/V group
+    return orc.route_priorities(qbar, nq, kbar, nk), nq, nk
+
+
+def test_topp_keys_are_preceding_mass(orc):
+    # key(a, b) = -(estimated mass of the cells ranked before b in row a's
+    # pi order): 0 for the best cell, decreasing along the order, and the last
+    # cell's key minus its own mass is -1 (the masses of a row sum to 1).
+    prio, nq, nk = _topp_case(orc, 3)
+    keys = orc.route_topp_keys(prio, nq, nk)
+    live = np.flatnonzero(nk)
+    for a in range(len(nq)):
+        if nq[a] == 0:
+            assert np.all(keys[a] == 0)
+            continue
+        order = live[np.lexsort((live, -prio[a, live]))]
+        mass = nk[order] * np.exp(prio[a, order].astype(np.float64))
+        before = np.concatenate([[0.0], np.cumsum(mass)[:-1]])
+        assert np.allclose(-keys[a, order], before, atol=1e-7, rtol=0)
+        assert keys[a, order[0]] == 0
+        assert abs(-float(keys[a, order[-1]]) + mass[-1] - 1.0) < 1e-5
+
+
+def test_topp_routing_is_one_threshold_per_group(orc):
+    # Brute force of the top-p rule: for a threshold p every nonempty row takes
+    # the shortest prefix of its pi order whose mass reaches p.  Spending
+    # exactly that set's pair cost, the budget walk on the top-p keys must
+    # select exactly that set, for every p between consecutive breakpoints.
+    for seed in (3, 4):
+        prio, nq, nk = _topp_case(orc, seed)
+        keys = orc.route_topp_keys(prio, nq, nk)
+        cq, ck = prio.shape
+        live = np.flatnonzero(nk)
+        cum = {}
+        for a in np.flatnonzero(nq):
+            order = live[np.lexsort((live, -prio[a, live]))]
+            mass = nk[order] * np.exp(prio[a, order].astype(np.float64))
+            cum[a] = (order, np.concatenate([[0.0], np.cumsum(mass)]))
+        bps = np.unique(np.concatenate([c[1][:-1] for c in cum.values()]))
+        for p in list((bps[:-1] + bps[1:]) / 2) + [bps[-1] + 1e-3]:
+            want = np.zeros((cq, ck), np.uint8)
+            for a, (order, c) in cum.items():
+                k = int(np.searchsorted(c, p, side="left"))  # first prefix reaching p
+                want[a, order[:max(k, 1)]] = 1
+            budget = int(np.sum(want * np.outer(nq, nk)))
+            z, st = orc.route_select(keys, nq, nk, budget)
+            assert np.array_equal(z, want), p
+            assert st["routed_pairs"] == budget
+
+
+def test_topp_plan_keeps_the_partition(orc):
+    # The routing rule changes only the route set: labels and probes equal
+    # the default plan's, the realised density stays within the target.
+    from paper_2608_18484_amd import workloads as W
+    wl = W.CONFIGS["tiny"]
+    q, k, v, _ = W.make_inputs(wl)
+    kw = dict(n_sampled=64, r_k=48, r_q=64, c_k=16, c_q=16, iters=8, density=0.25, n_probes=32)
+    p0 = orc.plan(q[0, 0], k[0, 0], **kw)
+    p1 = orc.plan(q[0, 0], k[0, 0], routing=1, **kw)
+    assert np.array_equal(p0["labels_q"], p1["labels_q"])
+    assert np.array_equal(p0["labels_kv"], p1["labels_kv"])
+    assert np.array_equal(p0["probes"], p1["probes"])
+    assert p1["rho_exec"] <= 0.25 + 1e-12
+    assert not np.array_equal(p0["z"], p1["z"])
+
+
 # --------------------------------------------------------------------------
 # Grouped-query attention: the plan of a K/V head pools its query heads
 # (Sec. 4.3 shares the K/V partition and routes across them; App. B.1 builds
