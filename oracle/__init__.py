@@ -365,3 +365,38 @@ def run(q, k, v, **params):
                      lam=params["lam"], ridge_only=ridge_only)
     pl["fit"] = ft
     return out, pl
+
+
+# --------------------------------------------------------------------------
+# Diagnostics of Sec. 3.1 (observations O1 and O3)
+# --------------------------------------------------------------------------
+
+def support_sets(q, k, rows, alpha):
+    """|D_i(alpha)| for each listed row and the membership marks of D_i
+    (bool, len(rows) x n_k): the smallest set of highest-weight keys whose
+    dense attention mass reaches alpha."""
+    q, k = _f32(q), _f32(k)
+    n_k, d = k.shape
+    rows = _i32(rows)
+    counts = np.zeros(len(rows), np.int32)
+    member = np.zeros((len(rows), n_k), np.uint8)
+    lib().or_support_sets(_p(q), _p(k), n_k, d, _p(rows), len(rows), ctypes.c_double(alpha),
+                          _p(counts), _p(member))
+    return counts, member.astype(bool)
+
+
+def pooled_support(member):
+    """gamma: size of the union of the rows' supports over n_k."""
+    member = np.asarray(member, bool)
+    return float(np.count_nonzero(member.any(axis=0))) / member.shape[1]
+
+
+def affine_fraction(osp, r):
+    """Affine-explainable fraction ||P_X R||^2 / ||R||^2 with X = [1, O_sp],
+    the affine-orthogonal energy and ||R||^2."""
+    osp, r = _f64(osp), _f64(r)
+    n, dv = osp.shape
+    out = np.zeros(3)
+    rank = lib().or_affine_fraction(_p(osp), _p(r), n, dv, _p(out))
+    return {"fraction": float(out[0]), "orthogonal": float(out[1]), "energy": float(out[2]),
+            "rank": int(rank)}

@@ -1074,3 +1074,102 @@ int or_attend(const float* q, const float* k, const float* v, int n, int d, int 
   free(rows);
   return st;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics of Sec. 3.1 (oracle side only: they need the dense attention) */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  double p;
+  int32_t j;
+} pk_t;
+
+static int pk_cmp(const void* x, const void* y) {
+  const pk_t* a = (const pk_t*)x;
+  const pk_t* b = (const pk_t*)y;
+  if (a->p > b->p) return -1; /* weight descending */
+  if (a->p < b->p) return 1;
+  return (a->j > b->j) - (a->j < b->j); /* then key index ascending */
+}
+
+void or_support_sets(const float* q, const float* k, int n_k, int d, const int32_t* rows,
+                     int nrows, double alpha, int32_t* counts, uint8_t* member) {
+  /* Observation O1: D_i(alpha) is the smallest set of highest-weight keys
+   * whose dense attention mass for query i reaches alpha. */
+  const double scale = 1.0 / sqrt((double)d);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int t = 0; t < nrows; ++t) {
+    const float* qi = q + (size_t)rows[t] * d;
+    pk_t* a = (pk_t*)malloc(sizeof(pk_t) * (size_t)n_k);
+    double mx = -INFINITY;
+    for (int j = 0; j < n_k; ++j) {
+      double s = 0.0;
+      for (int c = 0; c < d; ++c) s += (double)qi[c] * (double)k[(size_t)j * d + c];
+      a[j].p = s * scale;
+      a[j].j = j;
+      if (a[j].p > mx) mx = a[j].p;
+    }
+    double z = 0.0;
+    for (int j = 0; j < n_k; ++j) {
+      a[j].p = exp(a[j].p - mx);
+      z += a[j].p;
+    }
+    for (int j = 0; j < n_k; ++j) a[j].p /= z;
+    qsort(a, (size_t)n_k, sizeof(pk_t), pk_cmp);
+    double cum = 0.0;
+    int cnt = 0;
+    while (cnt < n_k && cum < alpha) {
+      cum += a[cnt].p;
+      if (member) member[(size_t)t * n_k + a[cnt].j] = 1;
+      ++cnt;
+    }
+    counts[t] = cnt;
+    free(a);
+  }
+}
+
+int or_affine_fraction(const double* osp, const double* r, int n, int dv, double* out) {
+  /* Observation O3: with X = [1, O_sp], the residual splits into P_X R (the
+   * best least-squares affine function of the sparse output) and
+   * (I - P_X) R.  ||P_X R||_F^2 = tr(C^T G^+ C) with G = X^T X and
+   * C = X^T R, through the eigenvectors of G (eigenvalues below 1e-12 of the
+   * largest count as zero, so a rank-deficient X is handled). */
+  const int p = dv + 1;
+  double* g = (double*)calloc((size_t)p * p, sizeof(double));
+  double* c = (double*)calloc((size_t)p * dv, sizeof(double));
+  double* x = (double*)malloc(sizeof(double) * p);
+  double rr = 0.0;
+  for (int i = 0; i < n; ++i) {
+    x[0] = 1.0;
+    for (int a = 0; a < dv; ++a) x[a + 1] = osp[(size_t)i * dv + a];
+    const double* ri = r + (size_t)i * dv;
+    for (int a = 0; a < p; ++a) {
+      for (int b = 0; b < p; ++b) g[(size_t)a * p + b] += x[a] * x[b];
+      for (int b = 0; b < dv; ++b) c[(size_t)a * dv + b] += x[a] * ri[b];
+    }
+    for (int b = 0; b < dv; ++b) rr += ri[b] * ri[b];
+  }
+  double* ev = (double*)malloc(sizeof(double) * p);
+  double* u = (double*)malloc(sizeof(double) * (size_t)p * p);
+  or_sym_eig(g, p, ev, u);
+  double e = 0.0;
+  int rank = 0;
+  for (int kk = 0; kk < p; ++kk) {
+    if (!(ev[kk] > 1e-12 * ev[0])) continue;
+    ++rank;
+    for (int b = 0; b < dv; ++b) {
+      double t = 0.0;
+      for (int a = 0; a < p; ++a) t += u[(size_t)a * p + kk] * c[(size_t)a * dv + b];
+      e += t * t / ev[kk];
+    }
+  }
+  out[0] = rr > 0.0 ? e / rr : 0.0; /* affine-explainable fraction */
+  out[1] = rr - e;                  /* affine-orthogonal energy */
+  out[2] = rr;                      /* residual energy */
+  free(u);
+  free(ev);
+  free(x);
+  free(c);
+  free(g);
+  return rank;
+}

@@ -214,6 +214,24 @@ int or_attend(const float* q, const float* k, const float* v, int n, int d, int 
               const uint8_t* z, const int32_t* probes, const double* w, int m, int r,
               int ridge_only, double lambda, double eps, double* out, double* fit_out);
 
+/* Diagnostics of Sec. 3.1 (observations O1 and O3); they need the dense
+ * attention, so they exist on the oracle side only.
+ *
+ * or_support_sets: for each query row rows[t], the dense attention
+ * probabilities over the n_k keys (double, scale 1/sqrt(d)) and D_i(alpha),
+ * the smallest set of highest-weight keys (ties to the lower key index) whose
+ * cumulative mass reaches alpha.  counts[t] = |D_i(alpha)| (tau_i = counts /
+ * n_k); member (nrows x n_k bytes, zeroed by the caller, optional) marks the
+ * keys of D_i, so the pooled support of a set of rows is the size of the
+ * union of their marks. */
+void or_support_sets(const float* q, const float* k, int n_k, int d, const int32_t* rows,
+                     int nrows, double alpha, int32_t* counts, uint8_t* member);
+
+/* or_affine_fraction (eq. projection_decomposition): X = [1, O_sp] (n x (dv+1)),
+ * R the residual (n x dv).  out[0] = ||P_X R||_F^2 / ||R||_F^2, out[1] =
+ * ||(I - P_X) R||_F^2, out[2] = ||R||_F^2.  Returns the rank used for X. */
+int or_affine_fraction(const double* osp, const double* r, int n, int dv, double* out);
+
 #ifdef __cplusplus
 }
 #endif
