@@ -308,20 +308,30 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     return make_int2(lo, hi - lo);
   };
   const int safe_pos = (MODE == MODE_SPARSE) ? (nseg > 0 ? range_at(0).x : 0) : w.k0;
+  // Each of lanes 0-31 of wave 0 walks the ranges for key tid of every tile
+  // with a cursor that only moves forward.  The cursor's range and the one
+  // after it are kept in registers, so a tile costs no dependent LDS read
+  // unless its key crosses two range boundaries; the read of the new next
+  // range is only waited for at the following crossing.
   KeyCursor cur{0, 0};
+  int2 cr = make_int2(0, 0), nx = make_int2(0, 0);
+  if (MODE == MODE_SPARSE && tid < KT && nseg > 0) {
+    cr = range_at(0);
+    nx = nseg > 1 ? range_at(1) : make_int2(0, 0x7fffffff);
+  }
   auto fill_pos = [&](int tt) {  // key positions of tile tt -> ring slot tt % 3
     if (tid < KT) {
       const int f = tt * KT + tid;
       int pos = safe_pos;
       if (f < w.nkeys) {
         if (MODE == MODE_SPARSE) {
-          int2 r = range_at(cur.j);
-          while (f >= cur.cum + r.y && cur.j + 1 < nseg) {
-            cur.cum += r.y;
+          while (f >= cur.cum + cr.y) {  // f < nkeys: the run ends after f
+            cur.cum += cr.y;
             ++cur.j;
-            r = range_at(cur.j);
+            cr = nx;
+            nx = cur.j + 1 < nseg ? range_at(cur.j + 1) : make_int2(0, 0x7fffffff);
           }
-          pos = r.x + (f - cur.cum);
+          pos = cr.x + (f - cur.cum);
         } else {
           pos = w.k0 + f;
         }
