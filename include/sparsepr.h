@@ -245,7 +245,12 @@ sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const spars
  * kv_stride_h given when heads_kv < heads.  UNSUPPORTED: d != d_v, d not in {64, 128}, C_k or C_q
  * above 8191, n_q above 2^24, strides not multiples of 8 elements,
  * n_kv * stride_n * element size of 4 GiB or more (one head's K/V rows are
- * addressed with 32-bit byte offsets). */
+ * addressed with 32-bit byte offsets).
+ * Tuning: the bf16 sparse attention runs in key segments of about 6 MiB of
+ * one head's group-major K+V each (one launch per segment, sized for one
+ * XCD's L2); the environment variable SPARSEPR_SEG_KB, read here, overrides
+ * that size in KiB (at least 64).  The result is the same up to the fp32
+ * rounding of the regrouped tiles. */
 sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr_params* params,
                                      void* workspace, size_t bytes, sparsepr_plan_t* out);
 
