@@ -40,9 +40,9 @@ def to_device(q, k, v, dtype):
     return tuple(torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(tdt) for x in (q, k, v))
 
 
-def medium(grid=(4, 24, 32), heads=2, dtype="bf16", **kw):
+def medium(grid=(4, 24, 32), heads=2, dtype="bf16", d=128, **kw):
     """A workload the oracle finishes in seconds that still spans many tiles."""
     base = dict(length_scale=None, length_range=(2.0, 6.0), n_sampled=256, density=0.25,
                 n_probes=64, resid_rank=16, ridge=0.1)
     base.update(kw)
-    return W.Workload("medium", 1, heads, grid, 128, dtype, **base)
+    return W.Workload("medium", 1, heads, grid, d, dtype, **base)

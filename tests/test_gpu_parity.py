@@ -134,6 +134,20 @@ def test_bf16_medium_stagewise_and_output(orc, heads, ntext):
         assert err < 2e-2, (h, err)
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("f32", 128)])
+def test_medium_other_head_dims(orc, dtype, d):
+    # the bf16 MFMA path at d = 64 and the fp32 path at d = 128: every plan
+    # stage against the oracle and the output against its replay
+    wl = medium(heads=2, dtype=dtype, d=d)
+    r = _run(wl)
+    tol = 2e-2 if dtype == "bf16" else 1e-5
+    for h in range(2):
+        ex = _stagewise(orc, r, 0, h)
+        ref, _ = _replay(orc, r, ex, 0, h)
+        err = rel_l2(r["out"][0, h], ref)
+        assert err < tol, (h, err)
+
+
 def test_stats_accounting(orc):
     wl = medium(heads=2)
     r = _run(wl)
