@@ -124,6 +124,7 @@ void describe(const Geom& g, Work* w, Layout& L) {
   addq(&w->fitscr, (2 * M * dv + M * r + dv * r + M) * 8);
   addq(&w->fitgram, 2 * dv * dv * 8);
   addq(&w->fitvec, (!g.bf16 && dv > 64) ? dv * (dv + 4) * 8 : 0);
+  addq(&w->eigscr, 4 * std::max(d, dv) * std::max(d, dv) * 8);
   add(&w->stats, 16 * 8);
   size_t off = 0;
   for (auto& it : L.items) off += align256((size_t)g.BH * it.per_head * (it.per_query ? g.G : 1));

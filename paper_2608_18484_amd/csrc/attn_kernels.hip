@@ -26,6 +26,7 @@
 #include "device_utils.hpp"
 #include "sparsepr_internal.hpp"
 #include "jacobi_lds.hpp"
+#include "tridiag_eig.hpp"
 
 namespace sparsepr {
 
@@ -827,10 +828,11 @@ __global__ __launch_bounds__(256) void k_fit_gram(Geom g, Work w) {
 }
 
 // Residual subspace and ridge solve, one block of 1024 threads per head:
-// Psi = leading r eigenvectors of H with sigma > 1e-6 sigma_1 (Jacobi in
-// LDS); then (xbar^T W xbar + lambda I) Y = xbar^T W (Rbar Psi) by Cholesky,
-// so Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
-// T is the Jacobi's precision.  Double A and V of a 128 x 128 problem do not
+// Psi = leading r eigenvectors of H with sigma > 1e-6 sigma_1 (tridiagonal
+// solver in LDS, or cyclic Jacobi when its check fails); then
+// (xbar^T W xbar + lambda I) Y = xbar^T W (Rbar Psi) by Cholesky, so
+// Y = B_lambda Psi and the correction of row i is xbar_i Y Psi^T + mu_R.
+// T is the eigensolver's precision.  Double A and V of a 128 x 128 problem do not
 // both fit in LDS; V (VG) then lives in the head's global scratch.
 template <int D, typename T>
 __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
@@ -840,6 +842,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
                    CHOL = (size_t)D * D * sizeof(double);
   __shared__ __attribute__((aligned(16))) unsigned char smem[JAC > CHOL ? JAC : CHOL];
   __shared__ JacobiRot<T> rot[D / 2];
+  __shared__ TriWork<D, T, 1024> tw;
   __shared__ int order[D];
   __shared__ int flag, rank_s, fail;
   const int bq = blockIdx.x, bh = bq % g.BH, tid = threadIdx.x;
@@ -865,31 +868,62 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   } else {
     for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
     __syncthreads();
-    jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
-    if (tid < D) {
-      const T li = Am[tid * LD + tid];
-      int rank = 0;
-      for (int j = 0; j < D; ++j) {
-        const T lj = Am[j * LD + j];
-        rank += (lj > li) || (lj == li && j < tid);
-      }
-      order[rank] = tid;
-    }
-    __syncthreads();
+    tri_reduce<D, T, 1024>(Am, tw);
+    tri_eigvals<D, T, 1024>(tw);
     if (tid == 0) {
-      const double l1 = Am[order[0] * LD + order[0]];
+      // rank: the leading t < r with sigma_t > 1e-6 sigma_1.  In double the
+      // float eigenvalues of the multisection cannot place an eigenvalue
+      // near 1e-12 lambda_1, so a retained range reaching below 1e-5
+      // lambda_1 is left to the Jacobi solve.
+      const double l1 = tw.lamf[0];
       const double s1 = l1 > 0.0 ? sqrt(l1) : 0.0;
       int rk = 0;
+      bool amb = false;
       for (int t = 0; t < r && t < D; ++t) {
-        const double lt = Am[order[t] * LD + order[t]];
+        const double lt = tw.lamf[t];
+        if (sizeof(T) == 8 && !(lt >= 1e-5 * l1)) amb = true;
         const double st = lt > 0.0 ? sqrt(lt) : 0.0;
         if (s1 > 0.0 && st > 1e-6 * s1)
           ++rk;
         else
           break;
       }
-      rank_s = rk;
+      rank_s = amb ? -1 : rk;
       fail = 0;
+    }
+    __syncthreads();
+    if (rank_s >= 0) tri_vectors<D, T, 1024>(tw, Vm, LV, rank_s, w.eigscr + (size_t)bq * 4 * D * D);
+    if (rank_s >= 0 && tw.ok) {
+      tri_back<D, T, 1024>(Am, tw, Vm, LV, rank_s);
+      if (tid < D) order[tid] = tid;
+    } else {
+      for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
+      __syncthreads();
+      jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
+      if (tid < D) {
+        const T li = Am[tid * LD + tid];
+        int rank = 0;
+        for (int j = 0; j < D; ++j) {
+          const T lj = Am[j * LD + j];
+          rank += (lj > li) || (lj == li && j < tid);
+        }
+        order[rank] = tid;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        const double l1 = Am[order[0] * LD + order[0]];
+        const double s1 = l1 > 0.0 ? sqrt(l1) : 0.0;
+        int rk = 0;
+        for (int t = 0; t < r && t < D; ++t) {
+          const double lt = Am[order[t] * LD + order[t]];
+          const double st = lt > 0.0 ? sqrt(lt) : 0.0;
+          if (s1 > 0.0 && st > 1e-6 * s1)
+            ++rk;
+          else
+            break;
+        }
+        rank_s = rk;
+      }
     }
     __syncthreads();
   }
@@ -933,20 +967,51 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
     }
     __syncthreads();
   }
-  // L L^T Y = rhs, one right-hand side per thread
-  if (tid < rk && !fail) {
-    const int t = tid;
-    for (int i = 0; i < D; ++i) {
-      double acc = f.rhs[(size_t)i * r + t];
-      for (int k = 0; k < i; ++k) acc -= S[i * D + k] * f.rhs[(size_t)k * r + t];
-      f.rhs[(size_t)i * r + t] = acc / S[i * D + i];
+  // L L^T Y = rhs: wave t solves right-hand side t, lane l holding rows
+  // l, l + 64, ... in registers.  L y = b row by row (each row's dot product
+  // a wave sum over the solved rows), then L^T x = y from the last row up
+  // (each solved x_i subtracted from the rows above it), both reading rows
+  // of L.
+  {
+    constexpr int U = (D + 63) / 64;
+    static_assert(U <= 2, "rows per lane");
+    const int lane = tid & 63;
+    for (int wv = tid >> 6; wv < rk && !fail; wv += 1024 / 64) {
+      double y[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = lane + 64 * u;
+        y[u] = i < D ? f.rhs[(size_t)i * r + wv] : 0.0;
+      }
+      for (int i = 0; i < D; ++i) {
+        double part = 0.0;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = lane + 64 * u;
+          if (k < i) part += S[i * D + k] * y[u];
+        }
+        const double dot = tri_wave_sum(part);
+        const double bi = tri_readlane(U > 1 && i >= 64 ? y[U - 1] : y[0], i & 63);
+        const double yi = (bi - dot) / S[i * D + i];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (lane + 64 * u == i) y[u] = yi;
+      }
+      for (int i = D - 1; i >= 0; --i) {
+        const double xi = tri_readlane(U > 1 && i >= 64 ? y[U - 1] : y[0], i & 63) / S[i * D + i];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int k = lane + 64 * u;
+          if (k < i) y[u] -= S[i * D + k] * xi;
+          if (k == i) y[u] = xi;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = lane + 64 * u;
+        if (i < D) Y[i * r + wv] = (float)y[u];
+      }
     }
-    for (int i = D - 1; i >= 0; --i) {
-      double acc = f.rhs[(size_t)i * r + t];
-      for (int k = i + 1; k < D; ++k) acc -= S[k * D + i] * f.rhs[(size_t)k * r + t];
-      f.rhs[(size_t)i * r + t] = acc / S[i * D + i];
-    }
-    for (int i = 0; i < D; ++i) Y[i * r + t] = (float)f.rhs[(size_t)i * r + t];
   }
   if (tid == 0) {
     int64_t* st = w.stats + (size_t)bh * 16;

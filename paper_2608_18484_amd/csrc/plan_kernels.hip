@@ -18,6 +18,7 @@
 #include "device_utils.hpp"
 #include "sparsepr_internal.hpp"
 #include "jacobi_lds.hpp"
+#include "tridiag_eig.hpp"
 
 namespace sparsepr {
 
@@ -98,33 +99,58 @@ __device__ void eig_order(const T* A, int* order) {
 
 // Eigen-scaled response basis (Sec. 4.1; App. B.1, B.2): the leading r
 // eigendirections, each scaled by sqrt(lambda / mean of the r retained
-// lambdas); eigenvalues below tau * lambda_1 are clamped to 0 first.
+// lambdas); eigenvalues below tau * lambda_1 are clamped to 0 first.  The
+// tridiagonal solver gives the eigenvalues and the vectors of the retained
+// ones; when its check fails (a numerically repeated retained eigenvalue)
+// the block reloads the matrix and solves it by cyclic Jacobi instead.
 template <int D>
 __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, float tau, float* F,
-                                                    float* evals) {
+                                                    float* evals, double* scr) {
   using T = typename std::conditional<D <= 64, double, float>::type;
   constexpr int LD = D + 1;
   constexpr int LV = jacobi_vt_ld<D>();
   __shared__ T A[D * LD];
   __shared__ __attribute__((aligned(16))) T VT[D * LV];
   __shared__ JacobiRot<T> rot[D / 2];
+  __shared__ TriWork<D, T, 1024> tw;
   __shared__ int order[D];
   __shared__ double lam[D];
-  __shared__ int flag;
+  __shared__ int flag, nvec;
   __shared__ double meanv;
   const int bh = blockIdx.x, tid = threadIdx.x;
   const double* G = gram + (size_t)bh * D * D;
   for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
   __syncthreads();
-  // In float the basis reaches its rounding floor at a relative off-diagonal
-  // norm of about 1e-4 (measured on the long-video key metric: the weighted
-  // projector then differs from a double solve by 2.7e-5).
-  jacobi_eig_lds<D, T, 1024>(A, VT, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
-  eig_order<D, T>(A, order);
-  const double l1 = A[order[0] * LD + order[0]];
-  if (tid < D) {
-    const double l = A[order[tid] * LD + order[tid]];
-    lam[tid] = (l1 > 0.0 && l >= (double)tau * l1) ? l : 0.0;
+  tri_reduce<D, T, 1024>(A, tw);
+  tri_eigvals<D, T, 1024>(tw);
+  if (tid == 0) {
+    const float l1 = tw.lamf[0];
+    int n = 0;
+    while (n < r && n < D && l1 > 0.f && tw.lamf[n] >= tau * l1) ++n;
+    nvec = n;
+  }
+  __syncthreads();
+  tri_vectors<D, T, 1024>(tw, VT, LV, nvec, scr + (size_t)bh * 4 * D * D);
+  if (tw.ok) {
+    tri_back<D, T, 1024>(A, tw, VT, LV, nvec);
+    if (tid < D) {
+      order[tid] = tid;
+      lam[tid] = tid < nvec ? tw.lamv[tid]
+                            : ((tw.lamf[0] > 0.f && tw.lamf[tid] >= tau * tw.lamf[0]) ? (double)tw.lamf[tid] : 0.0);
+    }
+  } else {
+    for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
+    __syncthreads();
+    // In float the basis reaches its rounding floor at a relative off-diagonal
+    // norm of about 1e-4 (measured on the long-video key metric: the weighted
+    // projector then differs from a double solve by 2.7e-5).
+    jacobi_eig_lds<D, T, 1024>(A, VT, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
+    eig_order<D, T>(A, order);
+    const double l1 = A[order[0] * LD + order[0]];
+    if (tid < D) {
+      const double l = A[order[tid] * LD + order[tid]];
+      lam[tid] = (l1 > 0.0 && l >= (double)tau * l1) ? l : 0.0;
+    }
   }
   __syncthreads();
   if (tid == 0) {
@@ -136,8 +162,8 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
   float* Fo = F + (size_t)bh * D * r;
   for (int i = tid; i < D * r; i += blockDim.x) {
     const int row = i / r, t = i % r;
-    const double wgt = meanv > 0.0 ? sqrt(lam[t] / meanv) : 0.0;
-    Fo[i] = (float)((double)VT[order[t] * LV + row] * wgt);
+    const double wgt = (meanv > 0.0 && lam[t] > 0.0) ? sqrt(lam[t] / meanv) : 0.0;
+    Fo[i] = wgt > 0.0 ? (float)((double)VT[order[t] * LV + row] * wgt) : 0.f;
   }
   if (tid < D) evals[(size_t)bh * D + tid] = (float)lam[tid];
 }
@@ -806,49 +832,86 @@ template <int D>
 __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const int32_t* offk,
                                                       Geom g, double* gram) {
   // block (x, bh) computes output rows [8x, 8x + 8); every entry is summed
-  // over the groups in ascending order
+  // over the groups in ascending order.  Group means are staged in LDS 32
+  // groups at a time; the next chunk's loads are issued into registers
+  // before the current chunk is used.
   constexpr int RB = 8, GB = 32;
   constexpr int TPR = 256 / RB;       // threads per output row
   constexpr int ENT = D / TPR;        // entries per thread
+  constexpr int P = 256 / D;          // threads per column of the mean
+  constexpr int LPT = GB * D / 4 / 256;  // float4 loads per thread per chunk
+  static_assert(LPT >= 1 && 256 % D == 0, "thread mapping");
   __shared__ double mu[D];
+  __shared__ double part[P][D];
   __shared__ double ks[GB][D + 1];
-  __shared__ int cplus;
+  __shared__ int fl[GB];
+  __shared__ int cplus_part[P], cplus;
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int C = g.CK;
   const int32_t* o = offk + (size_t)bh * (g.CKt + 1);
   const float* kb = kbar + (size_t)bh * C * D;
-  if (tid < D) {
-    double s = 0.0;
+  {
+    // uniform mean over the nonempty groups: column c, groups b = q, q+P, ...
+    const int c = tid % D, q = tid / D;
+    double sacc = 0.0;
     int cp = 0;
 #pragma unroll 8
-    for (int b = 0; b < C; ++b)
-      if (o[b + 1] > o[b]) {
-        s += (double)kb[(size_t)b * D + tid];
-        ++cp;
-      }
-    mu[tid] = cp ? s / cp : 0.0;
-    if (tid == 0) cplus = cp;
+    for (int bb = q; bb < C; bb += P) {
+      const bool ne = o[bb + 1] > o[bb];
+      const float x = kb[(size_t)bb * D + c];
+      sacc += ne ? (double)x : 0.0;
+      cp += ne;
+    }
+    part[q][c] = sacc;
+    if (c == 0) cplus_part[q] = cp;
   }
   __syncthreads();
+  if (tid < D) {
+    double sacc = 0.0;
+    int cp = 0;
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      sacc += part[q][tid];
+      cp += cplus_part[q];
+    }
+    mu[tid] = cp ? sacc / cp : 0.0;
+    if (tid == 0) cplus = cp;
+  }
   const int ra = blockIdx.x * RB + tid / TPR, cb = (tid % TPR) * ENT;
   double acc[ENT];
 #pragma unroll
   for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
-  for (int b0 = 0; b0 < C; b0 += GB) {
-    for (int t = tid; t < GB * D; t += 256) {
-      const int b = b0 + t / D, c = t % D;
-      double v = 0.0;
-      if (b < C && o[b + 1] > o[b]) v = (double)kb[(size_t)b * D + c] - mu[c];
-      ks[t / D][c] = v;
+  float4 pre[LPT];
+  int pfl = 0;
+  auto load_chunk = [&](int b0) {
+#pragma unroll
+    for (int l = 0; l < LPT; ++l) {
+      const int e4 = tid + 256 * l, bb = b0 + e4 / (D / 4);
+      pre[l] = bb < C ? ((const float4*)(kb + (size_t)bb * D))[e4 % (D / 4)] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    if (tid < GB) pfl = (b0 + tid < C) && (o[b0 + tid + 1] > o[b0 + tid]);
+  };
+  load_chunk(0);
+  for (int b0 = 0; b0 < C; b0 += GB) {
+    if (tid < GB) fl[tid] = pfl;
+    __syncthreads();  // flags and mu visible; the previous chunk is consumed
+#pragma unroll
+    for (int l = 0; l < LPT; ++l) {
+      const int e4 = tid + 256 * l, i = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
+      const bool ne = fl[i] != 0;
+      ks[i][c + 0] = ne ? (double)pre[l].x - mu[c + 0] : 0.0;
+      ks[i][c + 1] = ne ? (double)pre[l].y - mu[c + 1] : 0.0;
+      ks[i][c + 2] = ne ? (double)pre[l].z - mu[c + 2] : 0.0;
+      ks[i][c + 3] = ne ? (double)pre[l].w - mu[c + 3] : 0.0;
+    }
+    if (b0 + GB < C) load_chunk(b0 + GB);
     __syncthreads();
     const int cnt = min(GB, C - b0);
     for (int i = 0; i < cnt; ++i) {
-      const double a = ks[i][ra];
+      const double av = ks[i][ra];
 #pragma unroll
-      for (int e = 0; e < ENT; ++e) acc[e] += a * ks[i][cb + e];
+      for (int e = 0; e < ENT; ++e) acc[e] += av * ks[i][cb + e];
     }
-    __syncthreads();
   }
   const double den = (double)max(cplus, 1) * (double)D;
   double* out = gram + (size_t)bh * D * D + (size_t)ra * D + cb;
@@ -1674,7 +1737,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
     k_identity_basis<<<BH, 256, 0, s>>>(w.fk, w.gram_k, w.evals_k, D);
   } else {
     k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
-    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k, w.eigscr);
   }
   project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
@@ -1686,7 +1749,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
                                                          w.kbar, 0);
   if (g.partition == SPARSEPR_PARTITION_RESPONSE) {
     k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
-    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q, w.eigscr);
     project<D>(g, w, q, w.fq, g.rq, 1, 1, g.eps_q, w.phiq, s);
   } else {
     // semantic query groups: k-means on the raw queries

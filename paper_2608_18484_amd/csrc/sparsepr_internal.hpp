@@ -117,6 +117,7 @@ struct Work {
   double* fitscr;     // [BH][2*M*dv + M*r + dv*r + M] fit scratch
   double* fitgram;    // [BH][2][dv][dv] Rbar^T W Rbar and xbar^T W xbar + lambda I
   double* fitvec;     // [BH][dv][dv+4] eigenvectors (transposed) of a double fit solve kept out of LDS
+  double* eigscr;     // [G][BH][4][D][D] pivots and ratios of the tridiagonal eigensolver's twisted factorisations (D = max(d, dv))
   int64_t* stats;     // [BH][16]
 };
 
