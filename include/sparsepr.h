@@ -180,6 +180,11 @@ typedef struct {
 #define SPARSEPR_FLAG_FIT_NOT_PD 2      /* ridge normal matrix not positive definite; correction
                                            reduced to the mean residual */
 #define SPARSEPR_FLAG_BUDGET_BELOW_FORCED 4 /* forced cells alone exceed the pair budget */
+#define SPARSEPR_FLAG_EIG_JACOBI 8 /* an eigenproblem (response basis, residual basis) was
+                                      solved by cyclic Jacobi instead of the tridiagonal
+                                      solver: a numerically repeated retained eigenvalue, or
+                                      (double fit) retained eigenvalues below 1e-5 of the
+                                      largest.  A cost diagnostic: both give the same basis */
 
 /* Host-side view of one head's plan, for export (diagnostics, oracle replay)
  * and import (running attend on a plan made elsewhere).  All arrays are HOST

@@ -897,6 +897,8 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
       tri_back<D, T, 1024>(Am, tw, Vm, LV, rank_s);
       if (tid < D) order[tid] = tid;
     } else {
+      if (tid == 0)
+        atomicOr((unsigned long long*)&w.stats[(size_t)bh * 16 + ST_FLAGS], (unsigned long long)SPARSEPR_FLAG_EIG_JACOBI);
       for (int e = tid; e < D * D; e += 1024) Am[(e / D) * LD + (e % D)] = (T)H[e];
       __syncthreads();
       jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
@@ -1016,7 +1018,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
   if (tid == 0) {
     int64_t* st = w.stats + (size_t)bh * 16;
     st[ST_FIT_RANK] = rk;
-    if (fail) st[ST_FLAGS] |= SPARSEPR_FLAG_FIT_NOT_PD;
+    if (fail) atomicOr((unsigned long long*)&st[ST_FLAGS], (unsigned long long)SPARSEPR_FLAG_FIT_NOT_PD);
   }
 }
 

@@ -105,7 +105,7 @@ __device__ void eig_order(const T* A, int* order) {
 // the block reloads the matrix and solves it by cyclic Jacobi instead.
 template <int D>
 __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, float tau, float* F,
-                                                    float* evals, double* scr) {
+                                                    float* evals, double* scr, int64_t* stats) {
   using T = typename std::conditional<D <= 64, double, float>::type;
   constexpr int LD = D + 1;
   constexpr int LV = jacobi_vt_ld<D>();
@@ -139,6 +139,8 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
                             : ((tw.lamf[0] > 0.f && tw.lamf[tid] >= tau * tw.lamf[0]) ? (double)tw.lamf[tid] : 0.0);
     }
   } else {
+    if (tid == 0)
+      atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS], (unsigned long long)SPARSEPR_FLAG_EIG_JACOBI);
     for (int i = tid; i < D * D; i += blockDim.x) A[(i / D) * LD + (i % D)] = (T)G[i];
     __syncthreads();
     // In float the basis reaches its rounding floor at a relative off-diagonal
@@ -178,18 +180,47 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 // head; G = 1 is the single-head case).
 // ---------------------------------------------------------------------------
 
-template <int D, int MAXR>
+constexpr int PROJ_CHUNKS = 4;
+
+template <int D, int MAXR, bool MF>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
                                                  int query, int rms, float eps, float* phi,
                                                  int64_t* stats, uint16_t* xhi, uint16_t* xlo,
                                                  float* xn, int RP) {
+  // MF (bf16 inputs): the products run on MFMA.  F is split into three bf16
+  // parts (hi + mid + lo reproduce its float value), each bf16 input times a
+  // part is exact in float, so the accumulation is the only rounding, as in
+  // the float loop.  Each wave takes 32 x 32 output tiles (A = 32 input
+  // rows read straight from memory, B = 32 columns of the split F in LDS);
+  // the tiles go through LDS to the same thread mapping as the float loop.
   constexpr int ROWS = 64, CPT = MAXR / 16;
-  __shared__ float xs[ROWS][D + 1];
-  __shared__ __attribute__((aligned(16))) float fs[D * MAXR];
+  constexpr int FLD = D + 8;  // bf16 pitch of the split F rows
+  constexpr int NCT = MAXR / 32, KS = D / 16;
+  constexpr size_t XS_BYTES = MF ? 4 : (size_t)ROWS * (D + 1) * 4;
+  constexpr size_t FS_BYTES = MF ? (size_t)3 * MAXR * FLD * 2 : (size_t)D * MAXR * 4;
+  constexpr size_t OT_BYTES = MF ? (size_t)ROWS * (MAXR + 1) * 4 : 4;
+  __shared__ __attribute__((aligned(16))) unsigned char xs_raw[XS_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char fs_raw[FS_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char ot_raw[OT_BYTES];
+  float(*xs)[D + 1] = (float(*)[D + 1])xs_raw;
+  float* fs = (float*)fs_raw;
+  uint16_t* fsp = (uint16_t*)fs_raw;  // [3][MAXR][FLD]
+  float(*ot)[MAXR + 1] = (float(*)[MAXR + 1])ot_raw;
   const int bh = blockIdx.y, tid = threadIdx.x;
-  const int r0 = blockIdx.x * ROWS;
   const float* Fh = F + (size_t)bh * D * R;
-  if (R == MAXR) {
+  if constexpr (MF) {
+    for (int i = tid; i < D * MAXR; i += 256) {
+      const int k = i / MAXR, c = i % MAXR;
+      const float f = c < R ? Fh[k * R + c] : 0.f;
+      const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f);
+      const float r1 = f - bf16_bits_to_f32(hi);
+      const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
+      const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
+      fsp[(0 * MAXR + c) * FLD + k] = hi;
+      fsp[(1 * MAXR + c) * FLD + k] = mid;
+      fsp[(2 * MAXR + c) * FLD + k] = lo;
+    }
+  } else if (R == MAXR) {
     for (int i = tid; i < D * MAXR / 4; i += 256) ((float4*)fs)[i] = ((const float4*)Fh)[i];
   } else {
     for (int i = tid; i < D * MAXR; i += 256) {
@@ -199,107 +230,151 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
   }
   const int ty = tid >> 4, tx = tid & 15;
   const int nsrc = query ? g.G : 1;
-  float pooled[4][CPT];
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) pooled[u][c] = 0.f;
-  for (int j = 0; j < nsrc; ++j) {
-    const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
-    if (j > 0) __syncthreads();
-    for (int i = tid; i < ROWS * D / 8; i += 256) {
-      const int rr = i / (D / 8), c8 = i % (D / 8);
-      const int row = r0 + rr;
-      float v[8];
-      if (row < g.NV) {
-        const int64_t off = base + (int64_t)(g.ntext + row) * g.sn + c8 * 8;
-        if (g.bf16) {
-          const uint4 u = *(const uint4*)((const uint16_t*)x + off);
-          const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            v[2 * e] = __uint_as_float(wds[e] << 16);
-            v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
-          }
-        } else {
-          const float4 u0 = *(const float4*)((const float*)x + off);
-          const float4 u1 = *(const float4*)((const float*)x + off + 4);
-          v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
-          v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
-    }
-    __syncthreads();
-    float acc[4][CPT];
+  bool bad = false;
+  // PROJ_CHUNKS chunks of 64 rows per block share the staged F
+  for (int chunk = 0; chunk < PROJ_CHUNKS; ++chunk) {
+    const int r0 = (blockIdx.x * PROJ_CHUNKS + chunk) * ROWS;
+    if (r0 >= g.NV) break;
+    if (chunk > 0) __syncthreads();
+    float pooled[4][CPT];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) acc[u][c] = 0.f;
-    for (int k = 0; k < D; ++k) {
-      float xv[4], fv[CPT];
+      for (int c = 0; c < CPT; ++c) pooled[u][c] = 0.f;
+    for (int j = 0; j < nsrc; ++j) {
+      const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
+      float acc[4][CPT];
+      if constexpr (MF) {
+        __syncthreads();  // split F ready; the previous head's tile consumed
+        const int wv = tid >> 6, lane = tid & 63, n = lane & 31, h = lane >> 5;
+        for (int tile = wv; tile < 2 * NCT; tile += 4) {
+          const int rt = tile & 1, ct = tile >> 1;
+          const int row = r0 + rt * 32 + n;
+          bf16x8 av[KS];
+          if (row < g.NV) {
+            const uint16_t* xr = (const uint16_t*)x + base + (int64_t)(g.ntext + row) * g.sn;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) xv[u] = xs[ty + 16 * u][k];
+            for (int ks = 0; ks < KS; ++ks) av[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xr + ks * 16 + h * 8));
+          } else {
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) fv[c] = fs[k * MAXR + tx * CPT + c];
+            for (int ks = 0; ks < KS; ++ks) av[ks] = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+          }
+          f32x16 S;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+          for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) acc[u][c] = fmaf(xv[u], fv[c], acc[u][c]);
+          for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+            for (int part = 0; part < 3; ++part) {
+              const bf16x8 bv = __builtin_bit_cast(
+                  bf16x8, *(const uint4*)(fsp + (size_t)(part * MAXR + ct * 32 + n) * FLD + ks * 16 + h * 8));
+              S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[ks], bv, S, 0, 0, 0);
+            }
+          }
+          // register i holds input row rt*32 + (i/4)*8 + h*4 + i%4, column ct*32 + n
+#pragma unroll
+          for (int i = 0; i < 16; ++i) ot[rt * 32 + (i / 4) * 8 + h * 4 + (i % 4)][ct * 32 + n] = S[i];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) acc[u][c] = ot[ty + 16 * u][tx * CPT + c];
+      } else {
+        if (j > 0) __syncthreads();
+        for (int i = tid; i < ROWS * D / 8; i += 256) {
+          const int rr = i / (D / 8), c8 = i % (D / 8);
+          const int row = r0 + rr;
+          float v[8];
+          if (row < g.NV) {
+            const int64_t off = base + (int64_t)(g.ntext + row) * g.sn + c8 * 8;
+            if (g.bf16) {
+              const uint4 u = *(const uint4*)((const uint16_t*)x + off);
+              const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                v[2 * e] = __uint_as_float(wds[e] << 16);
+                v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+              }
+            } else {
+              const float4 u0 = *(const float4*)((const float*)x + off);
+              const float4 u1 = *(const float4*)((const float*)x + off + 4);
+              v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
+              v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = 0.f;
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) xs[rr][c8 * 8 + e] = v[e];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) acc[u][c] = 0.f;
+        for (int k = 0; k < D; ++k) {
+          float xv[4], fv[CPT];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) xv[u] = xs[ty + 16 * u][k];
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) fv[c] = fs[k * MAXR + tx * CPT + c];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) acc[u][c] = fmaf(xv[u], fv[c], acc[u][c]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float den = 1.f;
+        if (rms) {
+          float ss = 0.f;
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) ss = fmaf(acc[u][c], acc[u][c], ss);
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
+          den = fmaxf(sqrtf(ss / (float)R), eps);
+        }
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) pooled[u][c] += acc[u][c] / den;
+      }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      float den = 1.f;
-      if (rms) {
-        float ss = 0.f;
+      const int row = r0 + ty + 16 * u;
+      // the k-means operands of the same coordinates: bf16 hi + lo halves
+      // (zero-padded to RP) and the row norm (its error-bound input)
+      float ssq = 0.f;
+      float vv[CPT];
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) ss = fmaf(acc[u][c], acc[u][c], ss);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
-        den = fmaxf(sqrtf(ss / (float)R), eps);
+      for (int c = 0; c < CPT; ++c) {
+        const int col = tx * CPT + c;
+        vv[c] = col < R ? (nsrc == 1 ? pooled[u][c] : pooled[u][c] / (float)nsrc) : 0.f;
+        ssq = fmaf(vv[c], vv[c], ssq);
       }
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) pooled[u][c] += acc[u][c] / den;
-    }
-  }
-  bool bad = false;
+      for (int o = 1; o < 16; o <<= 1) ssq += __shfl_xor(ssq, o);
+      if (row >= g.NV) continue;
+      float* out = phi + ((size_t)bh * g.NV + row) * R;
+      uint16_t* oh = xhi + ((size_t)bh * g.NV + row) * RP;
+      uint16_t* ol = xlo + ((size_t)bh * g.NV + row) * RP;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int row = r0 + ty + 16 * u;
-    // the k-means operands of the same coordinates: bf16 hi + lo halves
-    // (zero-padded to RP) and the row norm (its error-bound input)
-    float ssq = 0.f;
-    float vv[CPT];
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int col = tx * CPT + c;
-      vv[c] = col < R ? (nsrc == 1 ? pooled[u][c] : pooled[u][c] / (float)nsrc) : 0.f;
-      ssq = fmaf(vv[c], vv[c], ssq);
-    }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) ssq += __shfl_xor(ssq, o);
-    if (row >= g.NV) continue;
-    float* out = phi + ((size_t)bh * g.NV + row) * R;
-    uint16_t* oh = xhi + ((size_t)bh * g.NV + row) * RP;
-    uint16_t* ol = xlo + ((size_t)bh * g.NV + row) * RP;
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int col = tx * CPT + c;
-      if (col < R) {
-        bad |= !isfinite(vv[c]);
-        out[col] = vv[c];
+      for (int c = 0; c < CPT; ++c) {
+        const int col = tx * CPT + c;
+        if (col < R) {
+          bad |= !isfinite(vv[c]);
+          out[col] = vv[c];
+        }
+        if (col < RP) {
+          const uint16_t hb = __builtin_bit_cast(uint16_t, (__bf16)vv[c]);
+          oh[col] = hb;
+          ol[col] = __builtin_bit_cast(uint16_t, (__bf16)(vv[c] - bf16_bits_to_f32(hb)));
+        }
       }
-      if (col < RP) {
-        const uint16_t hb = __builtin_bit_cast(uint16_t, (__bf16)vv[c]);
-        oh[col] = hb;
-        ol[col] = __builtin_bit_cast(uint16_t, (__bf16)(vv[c] - bf16_bits_to_f32(hb)));
-      }
+      if (tx == 0) xn[(size_t)bh * g.NV + row] = sqrtf(ssq) * 1.000001f;
     }
-    if (tx == 0) xn[(size_t)bh * g.NV + row] = sqrtf(ssq) * 1.000001f;
   }
   if (bad)
     atomicOr((unsigned long long*)&stats[(size_t)bh * 16 + ST_FLAGS],
@@ -321,7 +396,7 @@ struct KmArgs {
   int32_t* changed;   // [BH][2][T+1]
   int n;              // rows taking part (sorted rows are row0 .. row0+n-1)
   int row0, N;
-  int R, C;           // coordinate rank, groups
+  int R, C;           // coordinate rank (at most the head dimension, 128), groups
   int offstride, nblk, cmax, sel, T;
   // MFMA screening of the assignment
   uint16_t* xhi;      // [BH][n][RP]
@@ -668,11 +743,19 @@ __global__ __launch_bounds__(1024) void k_sort_scan(KmArgs a, int it) {
   if (km_skip(a, bh, it)) return;
   int32_t* hist = a.blkhist + (size_t)bh * a.nblk * a.cmax;
   for (int b = tid; b < a.C; b += 1024) {
+    // the block counts are read 16 at a time ahead of their running sums
     int run = 0;
-    for (int k = 0; k < a.nblk; ++k) {
-      const int v = hist[(size_t)k * a.cmax + b];
-      hist[(size_t)k * a.cmax + b] = run;
-      run += v;
+    for (int k0 = 0; k0 < a.nblk; k0 += 16) {
+      int v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = k0 + u < a.nblk ? hist[(size_t)(k0 + u) * a.cmax + b] : 0;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        if (k0 + u < a.nblk) {
+          hist[(size_t)(k0 + u) * a.cmax + b] = run;
+          run += v[u];
+        }
+      }
     }
     cnt[b] = run;
   }
@@ -684,8 +767,9 @@ __global__ __launch_bounds__(1024) void k_sort_scan(KmArgs a, int it) {
 }
 
 // Counting sort, pass 3: stable scatter.  One wave per block of rows walks its
-// rows in order; rows with equal labels inside a 64-row slice get their
-// stable rank from a ballot over the lanes holding that label.
+// rows in order, 64 at a time: each lane reads its label's next slot, its
+// stable rank among the lanes holding the same label comes from a ballot per
+// distinct label, and the last such lane advances the slot.
 __global__ __launch_bounds__(64) void k_sort_scatter(KmArgs a, int it) {
   extern __shared__ int pos[];
   const int bh = blockIdx.y, blk = blockIdx.x, lane = threadIdx.x;
@@ -697,31 +781,39 @@ __global__ __launch_bounds__(64) void k_sort_scatter(KmArgs a, int it) {
   const int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   int32_t* perm = a.perm + (size_t)bh * a.N;
   const int j0 = blk * kSortBlock, j1 = min(a.n, j0 + kSortBlock);
+  const uint64_t below = (1ull << lane) - 1ull;
   for (int s = j0; s < j1; s += 64) {
     const int j = s + lane;
     const bool valid = j < j1;
     const int L = valid ? lab[j] : -1;
+    // the block is one wave: its LDS accesses complete in program order, so
+    // this read sees the previous slice's updates without a barrier
+    const int base = valid ? pos[L] : 0;
     uint64_t active = __ballot(valid);
+    int rank = 0, cnt = 0;
     while (active) {
       const int first = __ffsll((unsigned long long)active) - 1;
-      const int Lf = __shfl(L, first);
+      const int Lf = __builtin_amdgcn_readlane(L, first);
       const uint64_t m = __ballot(L == Lf) & active;
       if (L == Lf) {
-        const uint64_t below = m & ((1ull << lane) - 1ull);
-        perm[pos[Lf] + __popcll(below)] = a.row0 + j;
+        rank = __popcll(m & below);
+        cnt = __popcll(m);
       }
-      // the block is one wave: its LDS accesses complete in program order,
-      // so the update below is seen by the next reads without a barrier
-      // (a barrier would also wait for the permutation stores)
-      if (lane == first) pos[Lf] += __popcll(m);
       active &= ~m;
+    }
+    if (valid) {
+      perm[base + rank] = a.row0 + j;
+      if (rank == cnt - 1) pos[L] = base + cnt;
     }
   }
 }
 
 // Centroid update: per group, double sums of the members' coordinates in
 // ascending row order (the stable permutation order) / count, rounded to
-// float; an empty group keeps its centroid.  One wave per group.
+// float; an empty group keeps its centroid.  One wave per group: the
+// members' rows are fetched 64 at a time (lane i holds member m0 + i) and
+// exchanged by readlane; lane l owns coordinates l and l + 64, whose values
+// are loaded eight members at a time and added in ascending member order.
 __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (km_changed(a, bh)[it] == 0) return;
@@ -729,24 +821,49 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   if (b >= a.C) return;
   const int32_t* off = a.off + (size_t)bh * a.offstride;
   const int32_t* perm = a.perm + (size_t)bh * a.N;
-  const int s0 = off[b], s1 = off[b + 1];
+  const int s0 = __builtin_amdgcn_readfirstlane(off[b]), s1 = __builtin_amdgcn_readfirstlane(off[b + 1]);
   if (s1 == s0) return;
   const float* pts = a.pts + (size_t)bh * a.n * a.R;
   const int R = a.R;
-  for (int k = lane; k < R; k += 64) {
-    // members loaded eight at a time, added in ascending order
-    double sum = 0.0;
-    int m = s0;
-    for (; m + 8 <= s1; m += 8) {
-      float v[8];
+  // loads are unconditional (columns clamped into the row); lanes past R
+  // drop their sums
+  const int k0 = min(lane, R - 1), k1 = min(lane + 64, R - 1);
+  double sum0 = 0.0, sum1 = 0.0;
+  auto members = [&](auto two) {
+    constexpr bool TWO = decltype(two)::value;
+    for (int m0 = s0; m0 < s1; m0 += 64) {
+      const int cnt = min(64, s1 - m0);
+      const int myrow = lane < cnt ? perm[m0 + lane] - a.row0 : 0;
+      int u = 0;
+      for (; u + 8 <= cnt; u += 8) {
+        float v0[8], v1[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = pts[(size_t)(perm[m + u] - a.row0) * R + k];
+        for (int e = 0; e < 8; ++e) {
+          const float* pr = pts + (size_t)__builtin_amdgcn_readlane(myrow, u + e) * R;
+          v0[e] = pr[k0];
+          if constexpr (TWO) v1[e] = pr[k1];
+        }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) sum += (double)v[u];
+        for (int e = 0; e < 8; ++e) {
+          sum0 += (double)v0[e];
+          if constexpr (TWO) sum1 += (double)v1[e];
+        }
+      }
+      for (; u < cnt; ++u) {
+        const float* pr = pts + (size_t)__builtin_amdgcn_readlane(myrow, u) * R;
+        sum0 += (double)pr[k0];
+        if constexpr (TWO) sum1 += (double)pr[k1];
+      }
     }
-    for (; m < s1; ++m) sum += (double)pts[(size_t)(perm[m] - a.row0) * R + k];
-    a.cent[((size_t)bh * a.C + b) * R + k] = (float)(sum / (double)(s1 - s0));
-  }
+  };
+  if (R > 64)
+    members(std::true_type{});
+  else
+    members(std::false_type{});
+  const double inv = (double)(s1 - s0);
+  float* c = a.cent + ((size_t)bh * a.C + b) * R;
+  if (lane < R) c[lane] = (float)(sum0 / inv);
+  if (lane + 64 < R) c[lane + 64] = (float)(sum1 / inv);
 }
 
 // The dense-prefix rows (before row0) form the extra last group: label C and
@@ -1703,17 +1820,24 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm
 template <int D>
 static void project(const Geom& g, const Work& w, const void* x, const float* F, int R, int query,
                     int rms, float eps, float* phi, hipStream_t s) {
-  const dim3 grid((g.NV + 63) / 64, g.BH);
+  const dim3 grid((g.NV + 64 * PROJ_CHUNKS - 1) / (64 * PROJ_CHUNKS), g.BH);
   const int RP = (R + 15) / 16 * 16;
-  if (R <= 32)
-    k_project<D, 32><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
-                                          w.km_xlo, w.km_xn, RP);
-  else if (R <= 64)
-    k_project<D, 64><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
-                                          w.km_xlo, w.km_xn, RP);
+  auto run = [&](auto maxr, auto mf) {
+    k_project<D, decltype(maxr)::value, decltype(mf)::value><<<grid, 256, 0, s>>>(
+        x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi, w.km_xlo, w.km_xn, RP);
+  };
+  auto by_rank = [&](auto mf) {
+    if (R <= 32)
+      run(std::integral_constant<int, 32>{}, mf);
+    else if (R <= 64)
+      run(std::integral_constant<int, 64>{}, mf);
+    else
+      run(std::integral_constant<int, 128>{}, mf);
+  };
+  if (g.bf16)
+    by_rank(std::true_type{});
   else
-    k_project<D, 128><<<grid, 256, 0, s>>>(x, g, F, R, query, rms, eps, phi, w.stats, w.km_xhi,
-                                           w.km_xlo, w.km_xn, RP);
+    by_rank(std::false_type{});
 }
 
 // The semantic partitions cluster the raw rows: coordinates phi = I^T x.
@@ -1737,7 +1861,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
     k_identity_basis<<<BH, 256, 0, s>>>(w.fk, w.gram_k, w.evals_k, D);
   } else {
     k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
-    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k, w.eigscr);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k, w.eigscr, w.stats);
   }
   project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
@@ -1749,7 +1873,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
                                                          w.kbar, 0);
   if (g.partition == SPARSEPR_PARTITION_RESPONSE) {
     k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
-    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q, w.eigscr);
+    k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q, w.eigscr, w.stats);
     project<D>(g, w, q, w.fq, g.rq, 1, 1, g.eps_q, w.phiq, s);
   } else {
     // semantic query groups: k-means on the raw queries

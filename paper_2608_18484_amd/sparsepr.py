@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsparsepr.so")
 
 F32, BF16 = 0, 1
-FLAG_NONFINITE_INPUT, FLAG_FIT_NOT_PD, FLAG_BUDGET_BELOW_FORCED = 1, 2, 4
+FLAG_NONFINITE_INPUT, FLAG_FIT_NOT_PD, FLAG_BUDGET_BELOW_FORCED, FLAG_EIG_JACOBI = 1, 2, 4, 8
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP",
           5: "NUMERICAL"}
 

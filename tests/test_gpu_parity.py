@@ -16,9 +16,9 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-def _run(wl, **over):
+def _run(wl, inputs=None, **over):
     from paper_2608_18484_amd import sparsepr as S
-    q, k, v, _ = W.make_inputs(wl)
+    q, k, v = inputs if inputs is not None else W.make_inputs(wl)[:3]
     tq, tk, tv = to_device(q, k, v, wl.dtype)
     p = params_for(wl, **over)
     op = S.SparsePR(S.shape_of(tq), p)
@@ -124,6 +124,9 @@ def test_bf16_medium_stagewise_and_output(orc, heads, ntext):
     if ntext:
         wl = wl.with_(n_text=ntext)
     r = _run(wl)
+    # the tridiagonal eigensolver (not its Jacobi fallback) made every basis
+    from paper_2608_18484_amd import sparsepr as S
+    assert not r["op"].stats()["status_flags"] & S.FLAG_EIG_JACOBI
     for h in range(heads):
         ex = _stagewise(orc, r, 0, h)
         osp = orc.sparse_rows(r["q"][0, h], r["k"][0, h], r["v"][0, h], ex["labels_q"],
@@ -490,6 +493,35 @@ def test_degenerate_plans(orc, case):
     ref, _ = _replay(orc, r, ex, 0, 0)
     err = rel_l2(r["out"][0, 0], ref)
     assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_repeated_retained_eigenvalue(orc, dtype, d):
+    """Sampled query rows alternating between 2 e_0 and 2 e_1 make the key
+    metric exactly diag(2, 2, 0, ...): two retained eigenvalues that are
+    equal, whose twisted vectors coincide, so the tridiagonal solver's check
+    rejects them and the block solves the metric by Jacobi instead (float at
+    d = 128, double at d = 64).  Every plan stage against the oracle and the
+    output against its replay."""
+    wl = medium(heads=1, dtype=dtype, d=d)
+    q, k, v, _ = W.make_inputs(wl)
+    p = params_for(wl)
+    n, nt = q.shape[2], p.n_dense_prefix
+    nv = n - nt
+    m = min(p.n_sampled_queries, nv)
+    for i in range(m):
+        row = nt + (i * nv) // m
+        q[0, 0, row] = 0.0
+        q[0, 0, row, i % 2] = 2.0
+    r = _run(wl, inputs=(q, k, v))
+    ex = _stagewise(orc, r, 0, 0)
+    assert np.count_nonzero(ex["m_k"]) == 2 and ex["m_k"][0, 0] == ex["m_k"][1, 1] == 2.0
+    from paper_2608_18484_amd import sparsepr as S
+    assert r["op"].stats()["status_flags"] & S.FLAG_EIG_JACOBI
+    assert np.count_nonzero(np.abs(ex["f_k"]).sum(axis=0)) == 2
+    ref, _ = _replay(orc, r, ex, 0, 0)
+    err = rel_l2(r["out"][0, 0], ref)
+    assert err < (2e-2 if dtype == "bf16" else 1e-5), err
 
 
 def test_imported_plan_with_many_ranges(orc):
