@@ -1026,108 +1026,126 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
 // final_reconstructed_output): out_i = x_i + mu_R + ((x_i - mu_x)/s_x) Y Psi^T
 // for the video rows; dense-prefix rows keep their (exact) sparse output.
 // Probe rows are overwritten afterwards by k_probe_scatter.
+constexpr int CORR_CHUNKS = 4;
+
 template <int D>
 __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
-  // 64 rows per block.  Thread (row = tid / 4, quarter = tid % 4) owns the
-  // columns [quarter * D/4, quarter * D/4 + D/4) of its row: it standardises
-  // them once into LDS, computes a quarter of the rank directions of
-  // t = xbar Y (Y = B_lambda Psi), and after the exchange forms its columns of
-  // x + mu_R + t Psi^T.  The rank is processed in slices of 16 directions.
-  constexpr int ROWS = 64, CW = D / 4, RS = 16;
-  __shared__ float xb[ROWS][D + 1];
-  __shared__ float ts[ROWS][RS + 1];
+  // CORR_CHUNKS chunks of 64 rows per block.  Thread (row = tid / 4,
+  // quarter = tid % 4) owns the columns [quarter * D/4, quarter * D/4 + D/4)
+  // of its row, held in registers; its partial of t = xbar Y
+  // (Y = B_lambda Psi) over those columns is summed with the other quarters'
+  // by lane exchange within the quad, and it forms its columns of
+  // x + mu_R + t Psi^T.  The rank is processed in slices of 16 directions,
+  // staged in LDS once per block when the rank fits one slice.
+  constexpr int CW = D / 4, RS = 16;
   __shared__ __attribute__((aligned(16))) float fy[D][RS];
   __shared__ __attribute__((aligned(16))) float fp[D][RS];
+  __shared__ __attribute__((aligned(16))) float fvs[3][D];  // mu_x, s_x, mu_R
   const int bq = blockIdx.y, bh = bq % g.BH, tid = threadIdx.x;
-  const int r0 = blockIdx.x * ROWS;
   const int r = g.r;
   const int rw = tid >> 2, qtr = tid & 3;
-  const int row = r0 + rw;
-  const bool valid = row < g.N;
-  const bool text = row < g.ntext;
   const float* fv = w.fitv + (size_t)bq * 3 * D;
   const float* Y = w.fity + (size_t)bq * D * r;
   const float* Psi = w.fitpsi + (size_t)bq * D * r;
-  const float* src = w.osp + ((size_t)bq * g.N + (valid ? row : 0)) * D + qtr * CW;
-  float x[CW], acc[CW];
-#pragma unroll
-  for (int c4 = 0; c4 < CW / 4; ++c4) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (valid) v = *(const float4*)(src + 4 * c4);
-    x[4 * c4] = v.x;
-    x[4 * c4 + 1] = v.y;
-    x[4 * c4 + 2] = v.z;
-    x[4 * c4 + 3] = v.w;
-  }
-#pragma unroll
-  for (int c = 0; c < CW; ++c) {
-    const int col = qtr * CW + c;
-    xb[rw][col] = (x[c] - fv[col]) / fv[D + col];
-    acc[c] = 0.f;
-  }
-  for (int t0 = 0; t0 < r; t0 += RS) {
+  const bool one_slice = r <= RS;
+  auto stage = [&](int t0) {
     const int tn = min(RS, r - t0);
-    __syncthreads();
     for (int i = tid; i < D * RS; i += 256) {
       const int c = i / RS, t = i % RS;
-      fy[c][t] = t < tn ? Y[c * r + t0 + t] : 0.f;
-      fp[c][t] = t < tn ? Psi[c * r + t0 + t] : 0.f;
+      // 16-byte slot t/4 is XOR-swizzled by the column's quarter, so the
+      // four quarters of a quad read different banks
+      const int sl = (((t >> 2) ^ (c / CW)) & 3) * 4 + (t & 3);
+      fy[c][sl] = t < tn ? Y[c * r + t0 + t] : 0.f;
+      fp[c][sl] = t < tn ? Psi[c * r + t0 + t] : 0.f;
     }
-    __syncthreads();
-    // t[rw][qtr*4 .. qtr*4+4): dims in index order
-    float tq[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < D; ++c) {
-      const float xv = xb[rw][c];
-      const float4 y4 = *(const float4*)&fy[c][qtr * 4];
-      tq[0] = fmaf(xv, y4.x, tq[0]);
-      tq[1] = fmaf(xv, y4.y, tq[1]);
-      tq[2] = fmaf(xv, y4.z, tq[2]);
-      tq[3] = fmaf(xv, y4.w, tq[3]);
+  };
+  for (int i = tid; i < 3 * D; i += 256) fvs[i / D][i % D] = fv[i];
+  if (one_slice) stage(0);
+  __syncthreads();
+  for (int chunk = 0; chunk < CORR_CHUNKS; ++chunk) {
+    const int row = (blockIdx.x * CORR_CHUNKS + chunk) * 64 + rw;
+    if ((blockIdx.x * CORR_CHUNKS + chunk) * 64 >= g.N) break;  // uniform over the block
+    const bool valid = row < g.N;
+    const bool text = row < g.ntext;
+    const float* src = w.osp + ((size_t)bq * g.N + (valid ? row : 0)) * D + qtr * CW;
+    float x[CW], acc[CW];
+#pragma unroll
+    for (int c4 = 0; c4 < CW / 4; ++c4) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (valid) v = *(const float4*)(src + 4 * c4);
+      x[4 * c4] = v.x;
+      x[4 * c4 + 1] = v.y;
+      x[4 * c4 + 2] = v.z;
+      x[4 * c4 + 3] = v.w;
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) ts[rw][qtr * 4 + e] = tq[e];
-    __syncthreads();
-    float tr[RS];
-#pragma unroll
-    for (int t = 0; t < RS; ++t) tr[t] = ts[rw][t];
-#pragma unroll
-    for (int c = 0; c < CW; ++c) {
-      const int col = qtr * CW + c;
-      float a = acc[c];
-#pragma unroll
-      for (int t4 = 0; t4 < RS / 4; ++t4) {
-        const float4 p4 = *(const float4*)&fp[col][t4 * 4];
-        a = fmaf(tr[4 * t4], p4.x, a);
-        a = fmaf(tr[4 * t4 + 1], p4.y, a);
-        a = fmaf(tr[4 * t4 + 2], p4.z, a);
-        a = fmaf(tr[4 * t4 + 3], p4.w, a);
+    for (int c = 0; c < CW; ++c) acc[c] = 0.f;
+    for (int t0 = 0; t0 < r; t0 += RS) {
+      if (!one_slice) {
+        __syncthreads();
+        stage(t0);
+        __syncthreads();
       }
-      acc[c] = a;
-    }
-  }
-  if (!valid) return;
-  const int64_t dst = q_base(g, bh, bq / g.BH) + (int64_t)row * g.sn + qtr * CW;
-  float o[CW];
+      float tp[RS];
 #pragma unroll
-  for (int c = 0; c < CW; ++c) o[c] = text ? x[c] : x[c] + fv[2 * D + qtr * CW + c] + acc[c];
-  if (g.bf16) {
-    uint16_t* op = (uint16_t*)out + dst;
+      for (int t = 0; t < RS; ++t) tp[t] = 0.f;
 #pragma unroll
-    for (int c8 = 0; c8 < CW / 8; ++c8) {
-      uint32_t wd[4];
+      for (int c = 0; c < CW; ++c) {
+        const int col = qtr * CW + c;
+        const float xb = (x[c] - fvs[0][col]) / fvs[1][col];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e]);
-        const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e + 1]);
-        wd[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+        for (int t4 = 0; t4 < RS / 4; ++t4) {
+          const float4 y4 = *(const float4*)&fy[col][(t4 ^ qtr) * 4];
+          tp[4 * t4] = fmaf(xb, y4.x, tp[4 * t4]);
+          tp[4 * t4 + 1] = fmaf(xb, y4.y, tp[4 * t4 + 1]);
+          tp[4 * t4 + 2] = fmaf(xb, y4.z, tp[4 * t4 + 2]);
+          tp[4 * t4 + 3] = fmaf(xb, y4.w, tp[4 * t4 + 3]);
+        }
       }
-      *(uint4*)(op + c8 * 8) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
-    }
-  } else {
-    float* op = (float*)out + dst;
 #pragma unroll
-    for (int c4 = 0; c4 < CW / 4; ++c4)
-      *(float4*)(op + 4 * c4) = make_float4(o[4 * c4], o[4 * c4 + 1], o[4 * c4 + 2], o[4 * c4 + 3]);
+      for (int t = 0; t < RS; ++t) {
+        tp[t] += tri_dpp<kDppXor1>(tp[t]);
+        tp[t] += tri_dpp<kDppXor2>(tp[t]);
+      }
+#pragma unroll
+      for (int c = 0; c < CW; ++c) {
+        const int col = qtr * CW + c;
+        float a = acc[c];
+#pragma unroll
+        for (int t4 = 0; t4 < RS / 4; ++t4) {
+          const float4 p4 = *(const float4*)&fp[col][(t4 ^ qtr) * 4];
+          a = fmaf(tp[4 * t4], p4.x, a);
+          a = fmaf(tp[4 * t4 + 1], p4.y, a);
+          a = fmaf(tp[4 * t4 + 2], p4.z, a);
+          a = fmaf(tp[4 * t4 + 3], p4.w, a);
+        }
+        acc[c] = a;
+      }
+    }
+    if (!valid) continue;
+    const int64_t dst = q_base(g, bh, bq / g.BH) + (int64_t)row * g.sn + qtr * CW;
+    float o[CW];
+#pragma unroll
+    for (int c = 0; c < CW; ++c) o[c] = text ? x[c] : x[c] + fvs[2][qtr * CW + c] + acc[c];
+    if (g.bf16) {
+      uint16_t* op = (uint16_t*)out + dst;
+#pragma unroll
+      for (int c8 = 0; c8 < CW / 8; ++c8) {
+        uint32_t wd[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e]);
+          const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)o[c8 * 8 + 2 * e + 1]);
+          wd[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+        }
+        *(uint4*)(op + c8 * 8) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+      }
+    } else {
+      float* op = (float*)out + dst;
+#pragma unroll
+      for (int c4 = 0; c4 < CW / 4; ++c4)
+        *(float4*)(op + 4 * c4) = make_float4(o[4 * c4], o[4 * c4 + 1], o[4 * c4 + 2], o[4 * c4 + 3]);
+    }
   }
 }
 
@@ -1236,7 +1254,7 @@ static void attend_d(const Geom& g, const Work* wq, const void* q, const void* k
   else
     k_fit_solve<D, float><<<BQ, 1024, 0, s>>>(g, wq[0]);
   if (ev) (void)hipEventRecord(ev[3], s);
-  k_correct<D><<<dim3((g.N + 63) / 64, BQ), 256, 0, s>>>(g, wq[0], out);
+  k_correct<D><<<dim3((g.N + 64 * CORR_CHUNKS - 1) / (64 * CORR_CHUNKS), BQ), 256, 0, s>>>(g, wq[0], out);
   if (g.M > 0) k_probe_scatter<<<dim3(g.M, BQ), 128, 0, s>>>(g, wq[0], out);
   if (ev) (void)hipEventRecord(ev[4], s);
 }

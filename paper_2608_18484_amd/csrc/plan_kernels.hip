@@ -1083,6 +1083,7 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
     for (int u = 0; u < 4; ++u)
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc[u][v] = 0.f;
+#pragma unroll 4
     for (int c = 0; c < D; ++c) {
       float qv[4], kv[4];
 #pragma unroll
@@ -1104,6 +1105,9 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
       }
   }
   __syncthreads();
+  // Phase 2 reads each row's scores and the K/V group sizes 8 per lane at a
+  // time (cells b = b0 + lane + 64u), so each batch waits once.
+  constexpr int NB = 8;
   const int wv = tid >> 6, lane = tid & 63;
   for (int rr = wv; rr < TR; rr += 4) {
     const int a = a0 + rr;
@@ -1115,28 +1119,63 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
       continue;
     }
     float mx = -INFINITY;
-    for (int b = lane; b < CK; b += 64)
-      if (ok[b + 1] > ok[b]) mx = fmaxf(mx, pr[b]);
+    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+      float sv[NB];
+      int nb[NB];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int b = b0 + lane + 64 * u;
+        sv[u] = b < CK ? pr[b] : 0.f;
+        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        if (nb[u] > 0) mx = fmaxf(mx, sv[u]);
+    }
     mx = wave_max(mx);
+    // terms exp(s - max) <= 1 in float (about 1 ulp each), summed in double
     double z = 0.0;
-    for (int b = lane; b < CK; b += 64) {
-      const int nb = ok[b + 1] - ok[b];
-      if (nb > 0) z += (double)nb * exp((double)pr[b] - (double)mx);
+    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+      float sv[NB];
+      int nb[NB];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int b = b0 + lane + 64 * u;
+        sv[u] = b < CK ? pr[b] : 0.f;
+        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        if (nb[u] > 0) z += (double)nb[u] * (double)expf(sv[u] - mx);
     }
     z = wave_sum_d(z);
     const float lse = (float)((double)mx + log(z));
     float bestv = -INFINITY;
     int besti = 0x7fffffff;
-    for (int b = lane; b < CK; b += 64) {
-      float pv = 0.f;
-      if (ok[b + 1] > ok[b]) {
-        pv = pr[b] - lse;
-        if (besti == 0x7fffffff || pv > bestv) {  // b ascending within the lane
-          bestv = pv;
-          besti = b;
+    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+      float sv[NB];
+      int nb[NB];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int b = b0 + lane + 64 * u;
+        sv[u] = b < CK ? pr[b] : 0.f;
+        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int b = b0 + lane + 64 * u;
+        if (b < CK) {
+          float pv = 0.f;
+          if (nb[u] > 0) {
+            pv = sv[u] - lse;
+            if (besti == 0x7fffffff || pv > bestv) {  // b ascending within the lane
+              bestv = pv;
+              besti = b;
+            }
+          }
+          pr[b] = pv;
         }
       }
-      pr[b] = pv;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -1409,38 +1448,67 @@ __global__ __launch_bounds__(256) void k_sel_mark(Geom g, Work w) {
 }
 
 // Per query group, the routed K/V groups as maximal contiguous ranges of the
-// group-major K/V order, and their total length.
-__global__ __launch_bounds__(64) void k_ranges(Geom g, Work w) {
-  const int bh = blockIdx.y;
-  const int a = blockIdx.x * 64 + threadIdx.x;
+// group-major K/V order, and their total length.  One wave per query group
+// walks the K/V groups 64 at a time.  Among the nonempty groups, a range
+// starts where routing switches on and ends where it switches off (empty
+// groups hold no keys, so they neither break nor extend a range): each lane
+// at a switch-off emits the range from the previous switch's key (a ballot
+// finds that lane, or the carry from earlier chunks) to its own start key,
+// at the index given by the switch-offs before it.
+__global__ __launch_bounds__(256) void k_ranges(Geom g, Work w) {
+  const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int a = blockIdx.x * 4 + wv;
   if (a >= g.CQt) return;
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
   const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
   const uint8_t* z = w.z + ((size_t)bh * g.CQt + a) * g.CKt;
   int2* rg = w.rng + ((size_t)bh * g.CQt + a) * g.CKt;
   const int na = oq[a + 1] - oq[a];
-  int cnt = 0, tot = 0, cs = -1, ce = -1;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int cnt = 0, tot = 0;
   if (na > 0) {
-    for (int b = 0; b < g.CKt; ++b) {
-      if (!z[b]) continue;
-      const int s = ok[b], e = ok[b + 1];
-      if (e == s) continue;
-      if (s == ce) {
-        ce = e;
-      } else {
-        if (cs >= 0) rg[cnt++] = make_int2(cs, ce - cs);
-        cs = s;
-        ce = e;
+    int prev_rt = 0;    // routing of the last nonempty group so far
+    int start_key = 0;  // key of the last switch so far (a range start when prev_rt)
+    for (int b0 = 0; b0 < g.CKt; b0 += 64) {
+      const int b = b0 + lane;
+      const bool in = b < g.CKt;
+      const int ks = in ? ok[b] : 0, ke = in ? ok[b + 1] : 0;
+      const bool ne = in && ke > ks;
+      const bool rt = ne && z[b] != 0;
+      const uint64_t NE = __ballot(ne), RT = __ballot(rt);
+      const uint64_t nb = NE & below;
+      const int pr = nb ? (int)((RT >> (63 - __clzll((long long)nb))) & 1ull) : prev_rt;
+      const bool sw = ne && ((int)rt != pr);
+      const uint64_t SW = __ballot(sw);
+      const uint64_t sb = SW & below;
+      const int pkey = __shfl(ks, sb ? 63 - __clzll((long long)sb) : lane);
+      const bool off = sw && !rt;
+      const uint64_t OFF = __ballot(off);
+      if (off) {
+        const int sk = sb ? pkey : start_key;
+        rg[cnt + __popcll(OFF & below)] = make_int2(sk, ks - sk);
+        tot += ks - sk;
       }
-      tot += e - s;
+      cnt += __popcll(OFF);
+      if (SW) start_key = __shfl(ks, 63 - __clzll((long long)SW));
+      if (NE) prev_rt = (int)((RT >> (63 - __clzll((long long)NE))) & 1ull);
     }
-    if (cs >= 0) rg[cnt++] = make_int2(cs, ce - cs);
+    tot = wave_sum_i(tot);
+    if (prev_rt) {
+      // the last nonempty group is routed: its range runs to the end
+      const int endk = ok[g.CKt];
+      if (lane == 0) rg[cnt] = make_int2(start_key, endk - start_key);
+      tot += endk - start_key;
+      ++cnt;
+    }
   }
-  w.rng_cnt[(size_t)bh * g.CQt + a] = cnt;
-  w.keytot[(size_t)bh * g.CQt + a] = tot;
-  if (na > 0)
-    atomicAdd((unsigned long long*)&w.stats[(size_t)bh * 16 + ST_ROUTED_PAIRS],
-              (unsigned long long)((long long)na * tot));
+  if (lane == 0) {
+    w.rng_cnt[(size_t)bh * g.CQt + a] = cnt;
+    w.keytot[(size_t)bh * g.CQt + a] = tot;
+    if (na > 0)
+      atomicAdd((unsigned long long*)&w.stats[(size_t)bh * 16 + ST_ROUTED_PAIRS],
+                (unsigned long long)((long long)na * tot));
+  }
 }
 
 // Attention work items: each query group split into tiles of kQTile rows.
@@ -1904,7 +1972,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   const int64_t ncell_t = (int64_t)g.CQt * g.CKt;
   const int gmark = (int)std::min<int64_t>(std::max<int64_t>((ncell_t + 4095) / 4096, 1), 512);
   k_sel_mark<<<dim3(gmark, BH), 256, 0, s>>>(g, w);
-  k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);
+  k_ranges<<<dim3((g.CQt + 3) / 4, BH), 256, 0, s>>>(g, w);
   k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
   // Probes (App. A.2)
   if (g.M > 0) {
@@ -1940,7 +2008,7 @@ void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s) {
             nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0};
   run_sort(aq, BH, -1, s);
   k_zero_routed<<<BH, 64, 0, s>>>(g, w);
-  k_ranges<<<dim3((g.CQt + 63) / 64, BH), 64, 0, s>>>(g, w);
+  k_ranges<<<dim3((g.CQt + 3) / 4, BH), 256, 0, s>>>(g, w);
   k_chunks<<<BH, 1024, (g.CQt + 1 + 17) * sizeof(int), s>>>(g, w);
   if (g.M > 0) k_probe_weights<<<BH, 256, 0, s>>>(g, w);
   k_plan_stats<<<BH, 256, 0, s>>>(g, w, 0, g.T);
