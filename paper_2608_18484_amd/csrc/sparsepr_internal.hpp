@@ -151,6 +151,9 @@ void launch_rebuild(const Geom& g, const Work& w, int bh, hipStream_t s);
 // head; each phase runs for the G query heads in turn.
 void launch_attend(const Geom& g, const Work* wq, const void* q, const void* k, const void* v,
                    void* out, hipStream_t s, hipEvent_t* ev = nullptr);
+// Fit, correction and restore after the sparse and probe attention
+// (records ev[3] after the solve and ev[4] at the end when ev is set).
+void launch_fit_correct(const Geom& g, const Work& w0, void* out, hipStream_t s, hipEvent_t* ev);
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
                   float* part, hipStream_t s);
 
