@@ -455,28 +455,40 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
 // written by k_project together with the coordinates.
 
 // Centroids: hi/lo split and exact squared norms (+inf for the padding rows).
-__global__ __launch_bounds__(64) void k_km_prep_cent(KmArgs a, int it) {
-  const int bh = blockIdx.y;
+__global__ __launch_bounds__(256) void k_km_prep_cent(KmArgs a, int it) {
+  // 64 centroids per block, staged in LDS by coalesced loads; thread t < 64
+  // forms the squared norm of centroid b0 + t as one fmaf chain in index
+  // order, and the hi/lo operand rows go out as one contiguous block.
+  __shared__ float cs[64][129];
+  const int bh = blockIdx.y, tid = threadIdx.x;
   if (km_skip_assign(a, bh, it)) return;
-  const int b = blockIdx.x * 64 + threadIdx.x;
-  if (b >= a.CP) return;
-  uint16_t* hi = a.chi + ((size_t)bh * a.CP + b) * a.RP;
-  uint16_t* lo = a.clo + ((size_t)bh * a.CP + b) * a.RP;
-  float u = INFINITY;
-  if (b < a.C) {
-    const float* c = a.cent + ((size_t)bh * a.C + b) * a.R;
-    u = 0.f;
-    for (int k = 0; k < a.R; ++k) u = fmaf(c[k], c[k], u);
-    for (int k = 0; k < a.RP; ++k) {
-      const float v = k < a.R ? c[k] : 0.f;
-      const uint16_t h = bf16_rne_bits(v);
-      hi[k] = h;
-      lo[k] = bf16_rne_bits(v - bf16_bits_to_f32(h));
-    }
-  } else {
-    for (int k = 0; k < a.RP; ++k) hi[k] = lo[k] = 0;
+  const int b0 = blockIdx.x * 64;
+  if (b0 >= a.CP) return;
+  const int R = a.R, RP = a.RP;
+  const float* cb = a.cent + (size_t)bh * a.C * R;
+  for (int e = tid; e < 64 * R; e += 256) {
+    const int r = e / R, k = e - r * R;
+    cs[r][k] = b0 + r < a.C ? cb[(size_t)(b0 + r) * R + k] : 0.f;
   }
-  a.cu[(size_t)bh * a.CP + b] = u;
+  __syncthreads();
+  if (tid < 64 && b0 + tid < a.CP) {
+    float u = INFINITY;
+    if (b0 + tid < a.C) {
+      u = 0.f;
+      for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
+    }
+    a.cu[(size_t)bh * a.CP + b0 + tid] = u;
+  }
+  uint16_t* hi = a.chi + ((size_t)bh * a.CP + b0) * RP;
+  uint16_t* lo = a.clo + ((size_t)bh * a.CP + b0) * RP;
+  const int rows = min(64, a.CP - b0);
+  for (int e = tid; e < rows * RP; e += 256) {
+    const int r = e / RP, k = e - r * RP;
+    const float v = (b0 + r < a.C && k < R) ? cs[r][k] : 0.f;
+    const uint16_t h = bf16_rne_bits(v);
+    hi[e] = h;
+    lo[e] = bf16_rne_bits(v - bf16_bits_to_f32(h));
+  }
 }
 
 // Screening: a block of 4 waves takes 256 points, 64 per wave as two sets
@@ -1535,18 +1547,34 @@ __global__ __launch_bounds__(1024) void k_chunks(Geom g, Work w) {
 // ---------------------------------------------------------------------------
 
 // Radial key of every video row: squared distance to its group mean in phi_Q
-// space (ordering by it is ordering by the distance).
-__global__ void k_probe_d2(Geom g, Work w) {
-  const int bh = blockIdx.y;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= g.NV) return;
+// space (ordering by it is ordering by the distance), one fmaf chain in
+// coordinate order per row.  When the rank is a multiple of 4, a block stages
+// the coordinates of its 128 rows in LDS (16-byte pitch) with coalesced loads
+// and reads them and the gathered centroid four at a time.
+__global__ __launch_bounds__(128) void k_probe_d2(Geom g, Work w) {
+  extern __shared__ __attribute__((aligned(16))) float ps[];  // 128 * (rq + 4) floats when rq % 4 == 0
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int i0 = blockIdx.x * 128;
+  const int R = g.rq;
+  const int rows = min(128, g.NV - i0);
+  const float* phb = w.phiq + ((size_t)bh * g.NV + i0) * R;
+  const bool vec = (R & 3) == 0;
+  const int LDP = R + 4;
+  if (vec) {
+    for (int e = tid; e < rows * (R / 4); e += 128) {
+      const int r = e / (R / 4), k4 = e - r * (R / 4);
+      *(float4*)&ps[r * LDP + 4 * k4] = ((const float4*)phb)[e];
+    }
+  }
+  __syncthreads();
+  if (tid >= rows) return;
+  const int i = i0 + tid;
   const int a = w.labq[(size_t)bh * g.N + g.ntext + i];
-  const float* ph = w.phiq + ((size_t)bh * g.NV + i) * g.rq;
-  const float* c = w.centq + ((size_t)bh * g.CQ + a) * g.rq;
+  const float* c = w.centq + ((size_t)bh * g.CQ + a) * R;
   float acc = 0.f;
-  int k = 0;
-  if ((g.rq & 3) == 0) {
-    for (; k < g.rq; k += 4) {
+  if (vec) {
+    const float* ph = ps + tid * LDP;
+    for (int k = 0; k < R; k += 4) {
       const float4 p4 = *(const float4*)(ph + k), c4 = *(const float4*)(c + k);
       float diff = p4.x - c4.x;
       acc = fmaf(diff, diff, acc);
@@ -1557,10 +1585,12 @@ __global__ void k_probe_d2(Geom g, Work w) {
       diff = p4.w - c4.w;
       acc = fmaf(diff, diff, acc);
     }
-  }
-  for (; k < g.rq; ++k) {
-    const float diff = ph[k] - c[k];
-    acc = fmaf(diff, diff, acc);
+  } else {
+    const float* ph = phb + (size_t)tid * R;
+    for (int k = 0; k < R; ++k) {
+      const float diff = ph[k] - c[k];
+      acc = fmaf(diff, diff, acc);
+    }
   }
   w.d2[(size_t)bh * g.NV + i] = acc;
 }
@@ -1842,7 +1872,7 @@ static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
 template <int MAXR>
 static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   const int BH = g.BH;
-  k_km_prep_cent<<<dim3(a.CP / 64 + 1, BH), 64, 0, s>>>(a, it);
+  k_km_prep_cent<<<dim3((a.CP + 63) / 64, BH), 256, 0, s>>>(a, it);
   const dim3 grid((a.n + 255) / 256, BH);
   if (a.RP == 16)
     k_km_assign_mfma<16><<<grid, 256, 0, s>>>(a, it);
@@ -1977,7 +2007,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   // Probes (App. A.2)
   if (g.M > 0) {
     if (g.probe_rule == SPARSEPR_PROBES_STRATIFIED) {
-      k_probe_d2<<<dim3((g.NV + 255) / 256, BH), 256, 0, s>>>(g, w);
+      k_probe_d2<<<dim3((g.NV + 127) / 128, BH), 128, (g.rq % 4 == 0) ? (size_t)128 * (g.rq + 4) * 4 : 0, s>>>(g, w);
       k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
     } else if (g.probe_rule == SPARSEPR_PROBES_UNIFORM) {
       k_probe_uniform<<<BH, 256, 0, s>>>(g, w);
