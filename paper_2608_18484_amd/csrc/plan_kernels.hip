@@ -1063,12 +1063,16 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
                                                     const int32_t* offq, const int32_t* offk,
                                                     float* prio, int32_t* forced) {
   // Block (x, bh) owns query groups [64x, 64x + 64).  Phase 1: s_ab for every
-  // K/V group in 64 x 64 tiles staged in LDS, 4 x 4 cells per thread, each
-  // the fmaf chain over the dims in index order.  Phase 2: one wave per query
-  // group computes lse_a in double, pi_ab and the forced (best) cell.
-  constexpr int TR = 64;
-  __shared__ float qs[TR][D + 1];
-  __shared__ float ks[TR][D + 1];
+  // K/V group on MFMA.  Both group means are split into three bf16 parts
+  // (hi + mid + lo reproduce the float value) and the six products whose
+  // terms reach 2^-16 of the leading one (hh; hm, mh; hl, lh, mm) are
+  // accumulated, the five small ones apart from hh, so s_ab keeps float
+  // accuracy.  Wave w holds the parts of query rows 32*(w&1) .. +32 in
+  // registers and takes key columns 32*(w>>1) .. +32 of each 64-group chunk,
+  // staged in LDS.  Phase 2: one wave per query group computes lse_a (double
+  // sum), pi_ab and the forced (best) cell.
+  constexpr int TR = 64, KS = D / 16, FLD = D + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t ks3[3][TR][FLD];
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int a0 = blockIdx.x * TR;
   const int CK = g.CK, CQ = g.CQ;
@@ -1078,49 +1082,88 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
   const float* qb = qbar + (size_t)bh * CQ * D;
   const float* kb = kbar + (size_t)bh * CK * D;
   float* prh = prio + (size_t)bh * CQ * CK;
-  for (int i = tid; i < TR * D; i += 256) {
-    const int r = i / D, c = i % D;
-    qs[r][c] = (a0 + r < CQ) ? qb[(size_t)(a0 + r) * D + c] : 0.f;
-  }
-  const int ty = tid >> 4, tx = tid & 15;
-  for (int b0 = 0; b0 < CK; b0 += TR) {
-    __syncthreads();
-    for (int i = tid; i < TR * D; i += 256) {
-      const int r = i / D, c = i % D;
-      ks[r][c] = (b0 + r < CK) ? kb[(size_t)(b0 + r) * D + c] : 0.f;
-    }
-    __syncthreads();
-    float acc[4][4];
+  {
+    const int wv = tid >> 6, lane = tid & 63, n = lane & 31, h = lane >> 5;
+    const int rt = wv & 1, ct = wv >> 1;
+    const int qa = a0 + rt * 32 + n;  // this lane's A row
+    bf16x8 qp[3][KS];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int ks = 0; ks < KS; ++ks) {
+      float v[8];
+      if (qa < CQ) {
+        const float4 u0 = *(const float4*)(qb + (size_t)qa * D + ks * 16 + h * 8);
+        const float4 u1 = *(const float4*)(qb + (size_t)qa * D + ks * 16 + h * 8 + 4);
+        v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
+        v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
+      } else {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = 0.f;
-#pragma unroll 4
-    for (int c = 0; c < D; ++c) {
-      float qv[4], kv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        qv[u] = qs[ty + 16 * u][c];
-        kv[u] = ks[tx + 16 * u][c];
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(qv[u], kv[v], acc[u][v]);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int a = a0 + ty + 16 * u, b = b0 + tx + 16 * v;
-        if (a < CQ && b < CK) prh[(size_t)a * CK + b] = acc[u][v] * scale;
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 hi = (__bf16)v[e];
+        const float r1 = v[e] - (float)hi;
+        const __bf16 mid = (__bf16)r1;
+        qp[0][ks][e] = hi;
+        qp[1][ks][e] = mid;
+        qp[2][ks][e] = (__bf16)(r1 - (float)mid);
       }
+    }
+    for (int b0 = 0; b0 < CK; b0 += TR) {
+      __syncthreads();  // the previous chunk is consumed
+#pragma unroll 8
+      for (int i = tid; i < TR * D; i += 256) {
+        const int r = i / D, c = i % D;
+        const float f = b0 + r < CK ? kb[(size_t)(b0 + r) * D + c] : 0.f;
+        const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f);
+        const float r1 = f - bf16_bits_to_f32(hi);
+        const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
+        ks3[0][r][c] = hi;
+        ks3[1][r][c] = mid;
+        ks3[2][r][c] = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
+      }
+      __syncthreads();
+      f32x16 Sb, Ss;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) Sb[i] = Ss[i] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int col = ct * 32 + n;
+        const bf16x8 kh = __builtin_bit_cast(bf16x8, *(const uint4*)&ks3[0][col][ks * 16 + h * 8]);
+        const bf16x8 km = __builtin_bit_cast(bf16x8, *(const uint4*)&ks3[1][col][ks * 16 + h * 8]);
+        const bf16x8 kl = __builtin_bit_cast(bf16x8, *(const uint4*)&ks3[2][col][ks * 16 + h * 8]);
+        Sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[0][ks], kh, Sb, 0, 0, 0);
+        Ss = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[0][ks], km, Ss, 0, 0, 0);
+        Ss = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[1][ks], kh, Ss, 0, 0, 0);
+        Ss = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[0][ks], kl, Ss, 0, 0, 0);
+        Ss = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[2][ks], kh, Ss, 0, 0, 0);
+        Ss = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qp[1][ks], km, Ss, 0, 0, 0);
+      }
+      // register i holds query row rt*32 + (i/4)*8 + h*4 + i%4, key column ct*32 + n
+      const int b = b0 + ct * 32 + n;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int a = a0 + rt * 32 + (i / 4) * 8 + h * 4 + (i % 4);
+        if (a < CQ && b < CK) prh[(size_t)a * CK + b] = (Sb[i] + Ss[i]) * scale;
+      }
+    }
   }
   __syncthreads();
-  // Phase 2 reads each row's scores and the K/V group sizes 8 per lane at a
-  // time (cells b = b0 + lane + 64u), so each batch waits once.
-  constexpr int NB = 8;
+  // Phase 2, one wave per query group.  When a row fits in NR cells per lane
+  // (cells b = lane + 64u) its scores stay in registers for the max, the
+  // normaliser and the output, and the K/V group sizes are read once per
+  // wave; longer rows go through global memory 8 cells per lane at a time.
+  constexpr int NR = 24, NB = 8;
   const int wv = tid >> 6, lane = tid & 63;
+  const bool inreg = CK <= 64 * NR;
+  int nbr[NR];
+  if (inreg) {
+#pragma unroll
+    for (int u = 0; u < NR; ++u) {
+      const int b = lane + 64 * u;
+      nbr[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+    }
+  }
   for (int rr = wv; rr < TR; rr += 4) {
     const int a = a0 + rr;
     if (a >= CQ) break;
@@ -1130,55 +1173,33 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
       if (lane == 0) forced[(size_t)bh * CQ + a] = -1;
       continue;
     }
-    float mx = -INFINITY;
-    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
-      float sv[NB];
-      int nb[NB];
-#pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const int b = b0 + lane + 64 * u;
-        sv[u] = b < CK ? pr[b] : 0.f;
-        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
-      }
-#pragma unroll
-      for (int u = 0; u < NB; ++u)
-        if (nb[u] > 0) mx = fmaxf(mx, sv[u]);
-    }
-    mx = wave_max(mx);
-    // terms exp(s - max) <= 1 in float (about 1 ulp each), summed in double
-    double z = 0.0;
-    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
-      float sv[NB];
-      int nb[NB];
-#pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const int b = b0 + lane + 64 * u;
-        sv[u] = b < CK ? pr[b] : 0.f;
-        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
-      }
-#pragma unroll
-      for (int u = 0; u < NB; ++u)
-        if (nb[u] > 0) z += (double)nb[u] * (double)expf(sv[u] - mx);
-    }
-    z = wave_sum_d(z);
-    const float lse = (float)((double)mx + log(z));
     float bestv = -INFINITY;
     int besti = 0x7fffffff;
-    for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
-      float sv[NB];
-      int nb[NB];
+    if (inreg) {
+      float sv[NR];
 #pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const int b = b0 + lane + 64 * u;
+      for (int u = 0; u < NR; ++u) {
+        const int b = lane + 64 * u;
         sv[u] = b < CK ? pr[b] : 0.f;
-        nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
       }
+      float mx = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < NB; ++u) {
-        const int b = b0 + lane + 64 * u;
+      for (int u = 0; u < NR; ++u)
+        if (nbr[u] > 0) mx = fmaxf(mx, sv[u]);
+      mx = wave_max(mx);
+      // terms exp(s - max) <= 1 in float (about 1 ulp each), summed in double
+      double z = 0.0;
+#pragma unroll
+      for (int u = 0; u < NR; ++u)
+        if (nbr[u] > 0) z += (double)nbr[u] * (double)expf(sv[u] - mx);
+      z = wave_sum_d(z);
+      const float lse = (float)((double)mx + log(z));
+#pragma unroll
+      for (int u = 0; u < NR; ++u) {
+        const int b = lane + 64 * u;
         if (b < CK) {
           float pv = 0.f;
-          if (nb[u] > 0) {
+          if (nbr[u] > 0) {
             pv = sv[u] - lse;
             if (besti == 0x7fffffff || pv > bestv) {  // b ascending within the lane
               bestv = pv;
@@ -1186,6 +1207,63 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
             }
           }
           pr[b] = pv;
+        }
+      }
+    } else {
+      float mx = -INFINITY;
+      for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+        float sv[NB];
+        int nb[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+          const int b = b0 + lane + 64 * u;
+          sv[u] = b < CK ? pr[b] : 0.f;
+          nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u)
+          if (nb[u] > 0) mx = fmaxf(mx, sv[u]);
+      }
+      mx = wave_max(mx);
+      double z = 0.0;
+      for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+        float sv[NB];
+        int nb[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+          const int b = b0 + lane + 64 * u;
+          sv[u] = b < CK ? pr[b] : 0.f;
+          nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u)
+          if (nb[u] > 0) z += (double)nb[u] * (double)expf(sv[u] - mx);
+      }
+      z = wave_sum_d(z);
+      const float lse = (float)((double)mx + log(z));
+      for (int b0 = 0; b0 < CK; b0 += 64 * NB) {
+        float sv[NB];
+        int nb[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+          const int b = b0 + lane + 64 * u;
+          sv[u] = b < CK ? pr[b] : 0.f;
+          nb[u] = b < CK ? ok[b + 1] - ok[b] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+          const int b = b0 + lane + 64 * u;
+          if (b < CK) {
+            float pv = 0.f;
+            if (nb[u] > 0) {
+              pv = sv[u] - lse;
+              if (besti == 0x7fffffff || pv > bestv) {  // b ascending within the lane
+                bestv = pv;
+                besti = b;
+              }
+            }
+            pr[b] = pv;
+          }
         }
       }
     }
@@ -1371,14 +1449,20 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
   const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
   const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
-  const int64_t ncell = (int64_t)g.CQ * g.CK;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + tid; idx < ncell; idx += (int64_t)gridDim.x * 256) {
-    const int a = (int)(idx / g.CK), b = (int)(idx - (int64_t)a * g.CK);
-    const int na = oq[a + 1] - oq[a], nb = ok[b + 1] - ok[b];
-    if (na == 0 || nb == 0 || fo[a] == b) continue;
-    const uint64_t key = cell_key(pr[idx], idx);
-    if (p > 0 && (key >> (shift + 8)) != (prefix >> (shift + 8))) continue;
-    atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb);
+  // rows a of the route matrix per block, columns b per thread: the row's
+  // size and forced cell are block-uniform and its scores are contiguous
+  for (int a = blockIdx.x; a < g.CQ; a += gridDim.x) {
+    const int na = oq[a + 1] - oq[a];
+    if (na == 0) continue;
+    const int fa = fo[a];
+    const int64_t row = (int64_t)a * g.CK;
+    for (int b = tid; b < g.CK; b += 256) {
+      const int nb = ok[b + 1] - ok[b];
+      if (nb == 0 || fa == b) continue;
+      const uint64_t key = cell_key(pr[row + b], row + b);
+      if (p > 0 && (key >> (shift + 8)) != (prefix >> (shift + 8))) continue;
+      atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb);
+    }
   }
   __syncthreads();
   uint64_t* gh = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
@@ -1994,7 +2078,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   }
   k_sel_init<<<BH, 256, 0, s>>>(g, w);
   const int64_t ncell = (int64_t)g.CQ * g.CK;
-  const int gsel = (int)std::min<int64_t>(std::max<int64_t>((ncell + 4095) / 4096, 1), 512);
+  const int gsel = std::max(1, std::min(g.CQ, 512));
   for (int p = 0; p < kSelPasses; ++p) {
     k_sel_hist<<<dim3(gsel, BH), 256, 0, s>>>(g, w, p);
     k_sel_choose<<<BH, 64, 0, s>>>(g, w, p);
