@@ -270,33 +270,46 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
     for (int p = 0; p < np; ++p) acc += f.wt[p] * f.xb[(size_t)p * D + c] * f.rp[(size_t)p * r + t];
     f.rhs[(size_t)c * r + t] = acc;
   }
-  // Cholesky S = L L^T in LDS (double)
+  // Cholesky S = L L^T in LDS (double), right-looking: at step j every
+  // thread takes sqrt(S_jj) itself, scales its part of column j, and after
+  // one barrier updates the lower triangle of the trailing block by column
+  // (k = tid % D) and rows (i = j + 1 + tid / D + NT/D * u, i >= k).
   double* S = (double*)smem;
   __syncthreads();
   for (int e = tid; e < D * D; e += 1024) S[e] = Sg[e];
   __syncthreads();
-  for (int j = 0; j < D; ++j) {
-    if (tid == 0) {
+  {
+    constexpr int RS = 1024 / D;  // row strips
+    const int kc = tid % D, i0 = tid / D;
+    for (int j = 0; j < D; ++j) {
       const double dj = S[j * D + j];
-      if (!(dj > 0.0)) fail = 1;
-      S[j * D + j] = dj > 0.0 ? sqrt(dj) : 1.0;
+      const double ljj = dj > 0.0 ? sqrt(dj) : 1.0;
+      for (int i = j + 1 + tid; i < D; i += 1024) S[i * D + j] /= ljj;
+      __syncthreads();
+      if (tid == 0) {
+        if (!(dj > 0.0)) fail = 1;
+        S[j * D + j] = ljj;
+      }
+      if (kc > j) {
+        const double lk = S[kc * D + j];
+        for (int i = j + 1 + i0; i < D; i += RS)
+          if (i >= kc) S[i * D + kc] -= S[i * D + j] * lk;
+      }
+      __syncthreads();
     }
-    __syncthreads();
-    const double ljj = S[j * D + j];
-    for (int i = j + 1 + tid; i < D; i += 1024) S[i * D + j] /= ljj;
-    __syncthreads();
-    const int rem = D - j - 1;
-    for (int e = tid; e < rem * rem; e += 1024) {
-      const int i = j + 1 + e / rem, k = j + 1 + e % rem;
-      if (k <= i) S[i * D + k] -= S[i * D + j] * S[k * D + j];
-    }
-    __syncthreads();
   }
+  // L^T into the strict upper triangle (S[i][k] = L[k][i], k > i), so that
+  // both triangular solves below read rows
+  for (int e = tid; e < D * D; e += 1024) {
+    const int i = e / D, k = e % D;
+    if (k > i) S[i * D + k] = S[k * D + i];
+  }
+  __syncthreads();
   // L L^T Y = rhs: wave t solves right-hand side t, lane l holding rows
-  // l, l + 64, ... in registers.  L y = b row by row (each row's dot product
-  // a wave sum over the solved rows), then L^T x = y from the last row up
-  // (each solved x_i subtracted from the rows above it), both reading rows
-  // of L.
+  // l, l + 64, ... in registers.  Both solves subtract each solved unknown
+  // from the rows still open: L y = b from the first row down (row i of the
+  // upper copy holds column i of L), then L^T x = y from the last row up
+  // (row i of L).
   {
     constexpr int U = (D + 63) / 64;
     static_assert(U <= 2, "rows per lane");
@@ -309,18 +322,13 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
         y[u] = i < D ? f.rhs[(size_t)i * r + wv] : 0.0;
       }
       for (int i = 0; i < D; ++i) {
-        double part = 0.0;
+        const double yi = tri_readlane(U > 1 && i >= 64 ? y[U - 1] : y[0], i & 63) / S[i * D + i];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const int k = lane + 64 * u;
-          if (k < i) part += S[i * D + k] * y[u];
+          if (k > i && k < D) y[u] -= S[i * D + k] * yi;
+          if (k == i) y[u] = yi;
         }
-        const double dot = tri_wave_sum(part);
-        const double bi = tri_readlane(U > 1 && i >= 64 ? y[U - 1] : y[0], i & 63);
-        const double yi = (bi - dot) / S[i * D + i];
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (lane + 64 * u == i) y[u] = yi;
       }
       for (int i = D - 1; i >= 0; --i) {
         const double xi = tri_readlane(U > 1 && i >= 64 ? y[U - 1] : y[0], i & 63) / S[i * D + i];
