@@ -264,10 +264,25 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
     f.rp[(size_t)p * r + t] = acc;
   }
   __syncthreads();
+  // rhs = xbar^T W (Rbar Psi): the probe weights and Rbar Psi are staged in
+  // the LDS (free again here) when they fit; each sum runs over the probes in
+  // order either way
+  double* rps = (double*)smem;  // [np][rk], then [np] weights
+  const bool staged = (size_t)np * (rk + 1) * sizeof(double) <= sizeof(smem);
+  if (staged) {
+    for (int i = tid; i < np * rk; i += 1024) rps[i] = f.rp[(size_t)(i / rk) * r + i % rk];
+    for (int p = tid; p < np; p += 1024) rps[np * rk + p] = f.wt[p];
+  }
+  __syncthreads();
   for (int i = tid; i < D * rk; i += 1024) {
     const int c = i / rk, t = i % rk;
     double acc = 0.0;
-    for (int p = 0; p < np; ++p) acc += f.wt[p] * f.xb[(size_t)p * D + c] * f.rp[(size_t)p * r + t];
+    if (staged) {
+#pragma unroll 8
+      for (int p = 0; p < np; ++p) acc += rps[np * rk + p] * f.xb[(size_t)p * D + c] * rps[p * rk + t];
+    } else {
+      for (int p = 0; p < np; ++p) acc += f.wt[p] * f.xb[(size_t)p * D + c] * f.rp[(size_t)p * r + t];
+    }
     f.rhs[(size_t)c * r + t] = acc;
   }
   // Cholesky S = L L^T in LDS (double), right-looking: at step j every
