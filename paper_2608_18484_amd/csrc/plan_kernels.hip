@@ -546,6 +546,11 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   uint4 nh[TPT], nl[TPT];
   float nu = 0.f;
   auto fetch = [&](int c0) {
+    // padding centroids get a huge finite norm: their scores stay finite
+    // (an index packed into +inf would make a NaN) and never win.  The norm
+    // is loaded first: the wait the compiler places before overwriting `nu`
+    // then covers only loads that have already landed, not the tile's.
+    if (tid < 32) nu = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
 #pragma unroll
     for (int u = 0; u < TPT; ++u) {
       const int i = tid + 256 * u;
@@ -555,9 +560,6 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
         nl[u] = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
       }
     }
-    // padding centroids get a huge finite norm: their scores stay finite
-    // (an index packed into +inf would make a NaN) and never win
-    if (tid < 32) nu = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
   };
   fetch(0);
   for (int c0 = 0; c0 < a.CP; c0 += 32) {
