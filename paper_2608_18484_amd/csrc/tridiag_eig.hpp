@@ -8,11 +8,13 @@
 //  2. tri_eigvals: every eigenvalue of T by multisection of its Sturm counts
 //     in float (NT / D threads per eigenvalue, each counting at one point of
 //     the current bracket), sorted descending.
-//  3. tri_vectors: for the leading nvec eigenvalues, one thread per vector
-//     forms the twisted factorisation of T - lambda I in double (stationary
-//     and progressive pivots, twist index at the smallest |gamma|), corrects
-//     lambda once by the Rayleigh quotient gamma / |z|^2, refactors and takes
-//     the twisted vector.  The vectors' tridiagonal residuals and mutual
+//  3. tri_vectors: for the leading nvec eigenvalues, the twisted
+//     factorisation of T - lambda I in double (stationary and progressive
+//     pivot chains, each vector's two chains in different waves; twist index
+//     at the smallest |gamma|, found by a group of 8 lanes per vector), one
+//     Rayleigh-quotient correction lambda += gamma / |z|^2, a second
+//     factorisation and the twisted vector (its two sides swept by two lanes
+//     of the group).  The vectors' tridiagonal residuals and mutual
 //     orthogonality are then checked; ok = 0 reports a numerically repeated
 //     eigenvalue (whose twisted vectors coincide) so that the caller can use
 //     its Jacobi solver instead.
