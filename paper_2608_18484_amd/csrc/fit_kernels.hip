@@ -372,7 +372,7 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
 // final_reconstructed_output): out_i = x_i + mu_R + ((x_i - mu_x)/s_x) Y Psi^T
 // for the video rows; dense-prefix rows keep their (exact) sparse output.
 // Probe rows are overwritten afterwards by k_probe_scatter.
-constexpr int CORR_CHUNKS = 4;
+constexpr int CORR_CHUNKS = 8;
 
 template <int D>
 __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(1024) void k_eig_basis(const double* gram, int r, f
 // head; G = 1 is the single-head case).
 // ---------------------------------------------------------------------------
 
-constexpr int PROJ_CHUNKS = 4;
+constexpr int PROJ_CHUNKS = 8;
 
 template <int D, int MAXR, bool MF>
 __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const float* F, int R,
