@@ -524,6 +524,22 @@ def test_repeated_retained_eigenvalue(orc, dtype, d):
     assert err < (2e-2 if dtype == "bf16" else 1e-5), err
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_residual_rank_over_one_slice(orc, dtype):
+    """Residual rank 24: the correction stages Y and Psi in two slices of 16
+    directions and the fit solves 24 right-hand sides (more than one per
+    wave of its block).  Every plan stage against the oracle, the fit rank and
+    the output against the oracle's replay."""
+    wl = medium(heads=1, dtype=dtype, resid_rank=24)
+    r = _run(wl)
+    ex = _stagewise(orc, r, 0, 0)
+    assert int(ex["fit_rank"]) == 24
+    ref, fit = _replay(orc, r, ex, 0, 0)
+    assert r["op"].stats()["status_flags"] & 2 == 0  # fit normal matrix positive definite
+    err = rel_l2(r["out"][0, 0], ref)
+    assert err < (2e-2 if dtype == "bf16" else 1e-5), err
+
+
 def test_imported_plan_with_many_ranges(orc):
     """Every token its own K/V group and every other group routed: 1024
     disjoint single-row ranges per query group, more than the attention
