@@ -273,6 +273,15 @@ sparsepr_status validate(const sparsepr_shape* s, const sparsepr_params* p, Geom
   }
   g.nsort_blk = (NV + kSortBlock - 1) / kSortBlock;
   g.nsort_blk_full = (N + kSortBlock - 1) / kSortBlock;
+  {
+    // The route-selection histograms add a bucket's pair cost (at most NV^2)
+    // and, above it, its cell count (at most CQ * CK) in one 64-bit word when
+    // both fit; the count lets the selection stop at a one-cell bucket.
+    auto bits = [](unsigned long long x) { int b = 0; while (x) { ++b; x >>= 1; } return b; };
+    const int wb = bits((unsigned long long)NV * (unsigned long long)NV);
+    const int cb = bits((unsigned long long)g.CQ * (unsigned long long)g.CK);
+    g.sel_cshift = (wb + cb <= 64 && wb < 64) ? wb : 0;
+  }
   g.cmax = std::max(g.CKt, g.CQt);
   g.rpad = (std::max(g.rk, g.rq) + 15) / 16 * 16;
   g.cpad = (std::max(g.CK, g.CQ) + 31) / 32 * 32;

@@ -1380,6 +1380,12 @@ __global__ __launch_bounds__(256) void k_route_topp(Geom g, Work w, int np2) {
   }
 }
 
+// The selection histograms hold, per bucket, the pair cost of its cells and,
+// from bit g.sel_cshift up (when it is nonzero), their count.
+__device__ __forceinline__ unsigned long long sel_count_unit(const Geom& g) {
+  return g.sel_cshift ? (1ull << g.sel_cshift) : 0ull;
+}
+
 // selstate slots.  SS_DONE: 0 searching, 1 every eligible cell fits,
 // 2 boundary key found (cells with larger keys are taken), 3 nothing beyond
 // the forced cells fits.
@@ -1451,6 +1457,7 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
   const int32_t* ok = w.offk + (size_t)bh * (g.CKt + 1);
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
   const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
+  const unsigned long long cunit = sel_count_unit(g);
   // rows a of the route matrix per block, columns b per thread: the row's
   // size and forced cell are block-uniform and its scores are contiguous
   for (int a = blockIdx.x; a < g.CQ; a += gridDim.x) {
@@ -1463,7 +1470,7 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
       if (nb == 0 || fa == b) continue;
       const uint64_t key = cell_key(pr[row + b], row + b);
       if (p > 0 && (key >> (shift + 8)) != (prefix >> (shift + 8))) continue;
-      atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb);
+      atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb + cunit);
     }
   }
   __syncthreads();
@@ -1483,13 +1490,20 @@ __global__ void k_sel_choose(Geom g, Work w, int p) {
   const long long rem = st[SS_REM];
   long long run = st[SS_ABOVE];
   for (int dg = kSelBins - 1; dg >= 0; --dg) {
-    const long long h = (long long)gh[dg];
+    const unsigned long long cunit = sel_count_unit(g);
+    const long long h = (long long)(cunit ? (gh[dg] & (cunit - 1ull)) : gh[dg]);
     if (run + h > rem) {
       const uint64_t prefix = (uint64_t)st[SS_PREFIX] | ((uint64_t)dg << shift);
       st[SS_PREFIX] = (int64_t)prefix;
       st[SS_ABOVE] = run;
       if (shift == 0) {
         st[SS_BOUND] = (int64_t)prefix;
+        st[SS_DONE] = 2;
+      } else if (cunit && (gh[dg] >> g.sel_cshift) == 1) {
+        // the boundary cell is the only one with this prefix: every cell of
+        // a higher bucket is taken and it is not, which is what comparing
+        // keys with the largest key of the prefix selects
+        st[SS_BOUND] = (int64_t)(prefix | ((1ull << shift) - 1ull));
         st[SS_DONE] = 2;
       }
       return;

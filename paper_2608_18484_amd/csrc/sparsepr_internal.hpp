@@ -41,6 +41,7 @@ struct Geom {
   uint32_t probe_seed;    // seed of the random probe rule
   int ridge_only;         // fit without the probe-residual subspace (Psi = I)
   int routing;            // SPARSEPR_ROUTING_*
+  int sel_cshift;         // bit where the selection histograms count cells (0: not counted)
   int M;                  // probes per head, min(n_probes, NV)
   int r;                  // residual rank
   int bf16;               // 1: bf16 tensors, 0: fp32
