@@ -44,17 +44,20 @@ __global__ void k_plan_init(Geom g, Work w) {
 
 template <int D>
 __global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, double* gram) {
-  constexpr int ENT = D * D / 256;
+  // block (x, bh) forms output rows [RB x, RB x + RB)
+  constexpr int RB = 16;
+  constexpr int ENT = RB * D / 256;
   constexpr int SB = 32;
   __shared__ float qs[SB][D];
-  const int bh = blockIdx.x, tid = threadIdx.x;
-  const int e0 = tid * ENT, ra = e0 / D, cb = e0 % D;
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int e0 = tid * ENT, ra = blockIdx.x * RB + e0 / D, cb = e0 % D;
   double acc[ENT];
 #pragma unroll
   for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
   for (int j = 0; j < g.G; ++j) {
     const int64_t base = q_base(g, bh, j);
     for (int s0 = 0; s0 < g.Ms; s0 += SB) {
+#pragma unroll 8
       for (int t = tid; t < SB * D; t += 256) {
         const int i = s0 + t / D, c = t % D;
         float v = 0.f;
@@ -74,9 +77,9 @@ __global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, doubl
       __syncthreads();
     }
   }
-  double* out = gram + (size_t)bh * D * D;
+  double* out = gram + (size_t)bh * D * D + (size_t)ra * D + cb;
 #pragma unroll
-  for (int e = 0; e < ENT; ++e) out[e0 + e] = acc[e] / ((double)g.Ms * (double)g.G);
+  for (int e = 0; e < ENT; ++e) out[e] = acc[e] / ((double)g.Ms * (double)g.G);
 }
 
 // Sort the eigenvalues on A's diagonal in descending order (ties by index):
@@ -2058,7 +2061,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   if (g.partition == SPARSEPR_PARTITION_SEMANTIC) {
     k_identity_basis<<<BH, 256, 0, s>>>(w.fk, w.gram_k, w.evals_k, D);
   } else {
-    k_key_metric<D><<<BH, 256, 0, s>>>(q, g, w.gram_k);
+    k_key_metric<D><<<dim3(D / 16, BH), 256, 0, s>>>(q, g, w.gram_k);
     k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_k, g.rk, 1e-6f, w.fk, w.evals_k, w.eigscr, w.stats);
   }
   project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
