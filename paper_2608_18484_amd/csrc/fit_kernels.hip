@@ -74,16 +74,19 @@ __global__ __launch_bounds__(256) void k_fit_prep(Geom g, Work w) {
   const float* pwt = w.pw + (size_t)bh * g.M;
   const float* osp = w.osp + (size_t)bq * g.N * D;
   const float* odp = w.odp + (size_t)bq * g.M * D;
-  if (tid == 0) {
+  if (tid < 64) {
+    // fixed order: lane-strided partial sums, then the wave sum
     double s = 0.0;
-    for (int p = 0; p < np; ++p) s += (double)pwt[p];
-    swsh = s;
+    for (int p = tid; p < np; p += 64) s += (double)pwt[p];
+    s = wave_sum_d(s);
+    if (tid == 0) swsh = s;
   }
   __syncthreads();
   const double sw = swsh;
   for (int p = tid; p < np; p += 256) f.wt[p] = (double)np * (double)pwt[p] / sw;
   for (int c = tid; c < D; c += 256) {
     double mx = 0.0, mr = 0.0;
+#pragma unroll 8
     for (int p = 0; p < np; ++p) {
       const double al = (double)pwt[p] / sw;
       const double x = osp[(size_t)pr[p] * D + c];
@@ -91,12 +94,14 @@ __global__ __launch_bounds__(256) void k_fit_prep(Geom g, Work w) {
       mr += al * ((double)odp[(size_t)p * D + c] - x);
     }
     double vx = 0.0;
+#pragma unroll 8
     for (int p = 0; p < np; ++p) {
       const double al = (double)pwt[p] / sw;
       const double t = (double)osp[(size_t)pr[p] * D + c] - mx;
       vx += al * t * t;
     }
     const double sx = sqrt(vx + (double)g.eps_x);
+#pragma unroll 8
     for (int p = 0; p < np; ++p) {
       const double x = osp[(size_t)pr[p] * D + c];
       f.xb[(size_t)p * D + c] = (x - mx) / sx;
