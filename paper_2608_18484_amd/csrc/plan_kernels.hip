@@ -914,44 +914,54 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
   const int nsrc = query ? g.G : 1;
   const int32_t* o = off + (size_t)bh * offstride;
   const int32_t* p = perm + (size_t)bh * g.N;
-  const int s0 = o[b], s1 = o[b + 1];
+  const int s0 = __builtin_amdgcn_readfirstlane(o[b]), s1 = __builtin_amdgcn_readfirstlane(o[b + 1]);
   // d <= 128: every channel pair has a lane; all lanes run the member loop
   // (the row indices are exchanged with readlane), idle lanes only skip the adds
   const int c = 2 * lane;
   const bool cin = c < g.d;
   double s0d = 0.0, s1d = 0.0;
-  auto ld2 = [&](int64_t base, int row) -> float2 {
-    if (!cin) return make_float2(0.f, 0.f);
-    const int64_t idx = base + (int64_t)row * g.sn + c;
-    if (g.bf16) {
-      const uint32_t u = *(const uint32_t*)((const uint16_t*)x + idx);
-      return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
-    }
-    return *(const float2*)((const float*)x + idx);
-  };
-  for (int j = 0; j < nsrc; ++j) {
-    const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
-    for (int m0 = s0; m0 < s1; m0 += 64) {
-      const int cm = min(64, s1 - m0);
-      const int pv = lane < cm ? p[m0 + lane] : 0;
-      int i = 0;
-      for (; i + 8 <= cm; i += 8) {
-        float2 v[8];
+  // loads are unconditional (lanes past d read channel 0 and drop their
+  // sums) and the dtype is decided outside the member loop
+  const int cl = cin ? c : 0;
+  auto members = [&](auto bfv) {
+    constexpr bool BF = decltype(bfv)::value;
+    auto ld2 = [&](int64_t base, int row) -> float2 {
+      const int64_t idx = base + (int64_t)row * g.sn + cl;
+      if constexpr (BF) {
+        const uint32_t u = *(const uint32_t*)((const uint16_t*)x + idx);
+        return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+      } else {
+        return *(const float2*)((const float*)x + idx);
+      }
+    };
+    for (int j = 0; j < nsrc; ++j) {
+      const int64_t base = query ? q_base(g, bh, j) : kv_base(g, bh);
+      for (int m0 = s0; m0 < s1; m0 += 64) {
+        const int cm = min(64, s1 - m0);
+        const int pv = lane < cm ? p[m0 + lane] : 0;
+        int i = 0;
+        for (; i + 8 <= cm; i += 8) {
+          float2 v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = ld2(base, __builtin_amdgcn_readlane(pv, i + u));
+          for (int u = 0; u < 8; ++u) v[u] = ld2(base, __builtin_amdgcn_readlane(pv, i + u));
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          s0d += (double)v[u].x;
-          s1d += (double)v[u].y;
+          for (int u = 0; u < 8; ++u) {
+            s0d += (double)v[u].x;
+            s1d += (double)v[u].y;
+          }
+        }
+        for (; i < cm; ++i) {
+          const float2 v = ld2(base, __builtin_amdgcn_readlane(pv, i));
+          s0d += (double)v.x;
+          s1d += (double)v.y;
         }
       }
-      for (; i < cm; ++i) {
-        const float2 v = ld2(base, __builtin_amdgcn_readlane(pv, i));
-        s0d += (double)v.x;
-        s1d += (double)v.y;
-      }
     }
-  }
+  };
+  if (g.bf16)
+    members(std::true_type{});
+  else
+    members(std::false_type{});
   if (!cin) return;
   const double n = (double)(s1 - s0) * (double)nsrc;
   float* dst = mean + ((size_t)bh * C + b) * g.d + c;
