@@ -1494,12 +1494,17 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
 
 // Pick the digit bucket where the cumulative cost (from the largest keys
 // down) first exceeds the remaining budget.
-__global__ void k_sel_choose(Geom g, Work w, int p) {
+__global__ __launch_bounds__(256) void k_sel_choose(Geom g, Work w, int p) {
+  __shared__ uint64_t gh[kSelBins];
   const int bh = blockIdx.x;
   int64_t* st = w.selstate + (size_t)bh * 8;
-  if (threadIdx.x != 0 || st[SS_DONE] != 0) return;
+  if (st[SS_DONE] != 0) return;  // uniform over the block
+  // the bins are read by all threads at once; thread 0 then walks them
+  const uint64_t* ghg = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
+  for (int i = threadIdx.x; i < kSelBins; i += blockDim.x) gh[i] = ghg[i];
+  __syncthreads();
+  if (threadIdx.x != 0) return;
   const int shift = 56 - 8 * p;
-  const uint64_t* gh = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
   const long long rem = st[SS_REM];
   long long run = st[SS_ABOVE];
   for (int dg = kSelBins - 1; dg >= 0; --dg) {
@@ -2110,7 +2115,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   const int gsel = std::max(1, std::min(g.CQ, 512));
   for (int p = 0; p < kSelPasses; ++p) {
     k_sel_hist<<<dim3(gsel, BH), 256, 0, s>>>(g, w, p);
-    k_sel_choose<<<BH, 64, 0, s>>>(g, w, p);
+    k_sel_choose<<<BH, 256, 0, s>>>(g, w, p);
   }
   const int64_t ncell_t = (int64_t)g.CQt * g.CKt;
   const int gmark = (int)std::min<int64_t>(std::max<int64_t>((ncell_t + 4095) / 4096, 1), 512);
