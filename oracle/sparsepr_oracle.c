@@ -169,8 +169,9 @@ void or_response_basis(const double* m, int d, int r, double tau, double* f, dou
   for (int i = 0; i < d; ++i)
     if (!(ev[i] >= tau * l1) || l1 <= 0.0) ev[i] = 0.0;
   if (r > d) r = d;
-  /* "scaled by the square root of their eigenvalues after the retained
-   * eigenvalues are normalized to unit mean" */
+  /* App. B.1 eq. app_key_response_coordinate (Sec. 3.2): divide the r kept
+   * eigenvalues by their mean, then weight each kept eigenvector by the
+   * square root of its normalised eigenvalue. */
   double mean = 0.0;
   for (int i = 0; i < r; ++i) mean += ev[i];
   mean /= (double)r;

@@ -149,6 +149,50 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def check_tensors(shape: Shape, q=None, k=None, v=None, out=None, device_type="cuda"):
+    """Check tensors against the geometry a plan was created with, before any
+    launch: the C side sees only pointers, so a tensor with another dtype,
+    fewer heads or rows, or other strides would make the kernels read or write
+    past its end.  Q and the output are [batch, heads, n, d] with the shape's
+    strides; K and V are [batch, heads_kv, n, d] with the K/V strides (the Q
+    strides when heads_kv is 0).  Raises ValueError on any mismatch."""
+    import torch
+    want_dtype = torch.bfloat16 if shape.dtype == BF16 else torch.float32
+    hkv = shape.heads_kv or shape.heads
+    kvsb = shape.kv_stride_b or shape.stride_b
+    kvsh = shape.kv_stride_h or shape.stride_h
+    geo = {
+        "q": ((shape.batch, shape.heads, shape.n_q, shape.d),
+              (shape.stride_b, shape.stride_h, shape.stride_n, 1)),
+        "out": ((shape.batch, shape.heads, shape.n_q, shape.d_v),
+                (shape.stride_b, shape.stride_h, shape.stride_n, 1)),
+        "k": ((shape.batch, hkv, shape.n_kv, shape.d), (kvsb, kvsh, shape.stride_n, 1)),
+        "v": ((shape.batch, hkv, shape.n_kv, shape.d_v), (kvsb, kvsh, shape.stride_n, 1)),
+    }
+    device = None
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out)):
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+        if t.device.type != device_type:
+            raise ValueError(f"{name}: tensor on {t.device}, expected a {device_type} tensor")
+        if device is None:
+            device = t.device
+        elif t.device != device:
+            raise ValueError(f"{name}: tensor on {t.device}, the others on {device}")
+        if t.dtype != want_dtype:
+            raise ValueError(f"{name}: dtype {t.dtype}, the plan was made for {want_dtype}")
+        dims, strides = geo[name]
+        if tuple(t.shape) != dims:
+            raise ValueError(f"{name}: shape {tuple(t.shape)}, the plan was made for {dims}")
+        # a dimension of extent 1 is never stepped over, so its stride is free
+        for ax, (got, exp) in enumerate(zip(t.stride(), strides)):
+            if dims[ax] > 1 and got != exp:
+                raise ValueError(f"{name}: strides {tuple(t.stride())}, the plan was made for "
+                                 f"{strides}")
+
+
 def _stream(stream):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
@@ -186,9 +230,11 @@ class SparsePR:
             self.handle = None
 
     def plan(self, q, k, stream=None):
+        check_tensors(self.shape, q=q, k=k)
         _check(lib().sparsepr_plan(self.handle, _ptr(q), _ptr(k), _stream(stream)))
 
     def attend(self, q, k, v, out, stream=None):
+        check_tensors(self.shape, q=q, k=k, v=v, out=out)
         _check(lib().sparsepr_attend(self.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                      _stream(stream)))
 
@@ -302,6 +348,7 @@ def dense_attention(q, k, v, out=None, stream=None):
     if out is None:
         out = torch.empty_like(q)
     sh = shape_of(q, kv=k if k.shape[1] != q.shape[1] else None)
+    check_tensors(sh, q=q, k=k, v=v, out=out)
     _check(lib().sparsepr_dense_attend(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                        None, ctypes.c_size_t(0), _stream(stream)))
     return out

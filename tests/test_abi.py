@@ -142,3 +142,76 @@ def test_null_arguments_rejected():
     assert lib.sparsepr_plan_create(ctypes.byref(sh), ctypes.byref(p), ctypes.c_void_p(1 << 20), 256,
                                     ctypes.byref(h)) == 3
     assert "needs" in lib.sparsepr_last_error().decode()
+
+
+# --- the binding checks tensors against the plan's geometry before any launch
+
+def _t(shape, dtype="float32", stride=None):
+    import torch
+    dt = getattr(torch, dtype)
+    t = torch.zeros(shape, dtype=dt)
+    if stride is not None:
+        t = torch.empty_strided(shape, stride, dtype=dt)
+    return t
+
+
+def _plan_shape(**kw):
+    base = dict(batch=1, heads=4, n_q=96, n_kv=96, d=64, d_v=64, stride_b=4 * 96 * 64,
+                stride_h=96 * 64, stride_n=64, dtype=S.F32)
+    base.update(kw)
+    return S.Shape(**base)
+
+
+def test_check_tensors_accepts_matching_tensors():
+    sh = _plan_shape()
+    x = _t((1, 4, 96, 64))
+    S.check_tensors(sh, q=x, k=x, v=x, out=x.clone(), device_type="cpu")
+    # grouped-query attention: K/V with their own head count and strides
+    g = _plan_shape(heads_kv=2, kv_stride_b=2 * 96 * 64, kv_stride_h=96 * 64)
+    kv = _t((1, 2, 96, 64))
+    S.check_tensors(g, q=x, k=kv, v=kv, out=x, device_type="cpu")
+
+
+@pytest.mark.parametrize("name,bad,needle", [
+    ("q", dict(dtype="bfloat16"), "dtype"),
+    ("out", dict(dtype="bfloat16"), "dtype"),
+    ("k", dict(shape=(1, 3, 96, 64)), "shape"),
+    ("v", dict(shape=(1, 4, 95, 64)), "shape"),
+    ("out", dict(shape=(1, 4, 96, 32)), "shape"),
+    ("q", dict(shape=(2, 4, 96, 64)), "shape"),
+    ("v", dict(stride=(4 * 96 * 128, 96 * 128, 128, 1)), "strides"),
+    ("out", dict(stride=(4 * 96 * 64, 64, 4 * 64, 1)), "strides"),
+])
+def test_check_tensors_rejects_mismatch(name, bad, needle):
+    sh = _plan_shape()
+    tens = {n: _t((1, 4, 96, 64)) for n in ("q", "k", "v", "out")}
+    tens[name] = _t(bad.get("shape", (1, 4, 96, 64)), bad.get("dtype", "float32"), bad.get("stride"))
+    with pytest.raises(ValueError, match=needle):
+        S.check_tensors(sh, device_type="cpu", **tens)
+
+
+def test_check_tensors_rejects_host_tensor_and_wrong_kv_heads():
+    sh = _plan_shape()
+    x = _t((1, 4, 96, 64))
+    with pytest.raises(ValueError, match="expected a cuda tensor"):
+        S.check_tensors(sh, q=x)
+    g = _plan_shape(heads_kv=2, kv_stride_b=2 * 96 * 64, kv_stride_h=96 * 64)
+    with pytest.raises(ValueError, match="shape"):
+        S.check_tensors(g, q=x, k=x, device_type="cpu")
+    with pytest.raises(ValueError, match="torch.Tensor"):
+        S.check_tensors(sh, q=x.numpy(), device_type="cpu")
+
+
+def test_op_methods_check_before_launch():
+    # an op whose handle was never created: a launch would fail in the library,
+    # so a ValueError proves the check runs first
+    op = object.__new__(S.SparsePR)
+    op.shape = _plan_shape()
+    op.handle = ctypes.c_void_p()
+    x = _t((1, 4, 96, 64))
+    with pytest.raises(ValueError):
+        op.plan(x, x)
+    with pytest.raises(ValueError):
+        op.attend(x, x, x, x)
+    with pytest.raises(ValueError, match="expected a cuda tensor"):
+        S.dense_attention(x, x, x, x)
