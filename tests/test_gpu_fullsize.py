@@ -3,8 +3,8 @@ configuration bench.py times (every head of the layer in one plan + attend).
 
 The oracle cannot replay a whole full-size call in test time, so for two
 heads of each workload it checks, on the GPU's own float inputs to each
-decision: the K/V k-means labels (bit-exact), the route set (bit-exact), the
-probe set (bit-exact); then, on sampled rows, the hard-drop output, the exact
+decision: the K/V and query k-means labels and final centroids (bit-exact),
+the route set (bit-exact), the probe set (bit-exact); then, on sampled rows, the hard-drop output, the exact
 probe rows and the corrected output (the oracle's fit on its own sparse and
 dense probe rows, applied to the sampled rows).
 """
@@ -50,9 +50,14 @@ def test_full_size_sampled_parity(orc, name):
         ex = op.export(bh)
         qh, kh, vh = q[b, h], k[b, h], v[b, h]
         n = qh.shape[0]
-        # K/V k-means on the GPU's coordinates: bit-exact labels
-        lab_k, _, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, p.kmeans_iters)
+        # K/V and query k-means on the GPU's coordinates: bit-exact labels and
+        # final centroids (the query centroids are the probe-selection means)
+        lab_k, cent_k, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, p.kmeans_iters)
         assert np.array_equal(ex["labels_kv"][nt:], lab_k)
+        assert np.array_equal(ex["cent_k"], cent_k)
+        lab_q, cent_q, _, _ = orc.kmeans(ex["phi_q"], cq, p.kmeans_iters)
+        assert np.array_equal(ex["labels_q"][nt:], lab_q)
+        assert np.array_equal(ex["cent_q"], cent_q)
         # routes given the GPU's priorities, bit-exact
         _, cnt_q = orc.group_mean(qh[nt:], ex["labels_q"][nt:], cq)
         nv = n - nt
