@@ -122,10 +122,19 @@ __device__ __forceinline__ int key_row(const Geom& g, const AttnArgs& A, int bh,
 }
 
 // Bank swizzle of the 16-byte chunks of a K/V tile row in LDS: chunk c of
-// key r sits at position c ^ swz(r) (low three bits), so 8 consecutive keys
-// reading one chunk (the K operand) and 4 consecutive keys reading two
-// neighbouring chunks (the transposed V reads) hit distinct banks.
-__device__ __forceinline__ int kv_swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// key r sits at position c ^ swz(r).  A 16-lane phase of a 128-bit read (the
+// K operand) takes one chunk of 16 consecutive keys, and one of a transposing
+// read takes two neighbouring chunks of 4 consecutive keys (two phases: four
+// chunks).  With 256-byte rows (D = 128) a row spans the 64 banks once, so
+// swz is a bijection of 16 consecutive keys onto the 16 chunk positions whose
+// bits 2-3 differ within every aligned group of 4 keys: both reads hit
+// distinct banks.  With 128-byte rows (D = 64) two keys share a bank row and
+// the 3-bit form is used.
+template <int D>
+__device__ __forceinline__ int kv_swz(int r) {
+  if (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  return ((r & 3) << 1) | ((r >> 2) & 1);
+}
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -351,7 +360,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       const int inst = wv * LPT + u;
       const int s = inst * 64 + lane;
       const int key = s / CH, p = s % CH;
-      const int c8 = p ^ kv_swz(key);
+      const int c8 = p ^ kv_swz<D>(key);
       voff[u] = (uint32_t)spos[tt % 3][key] * row_bytes + (uint32_t)(c8 * 16);
     }
 #pragma unroll
@@ -420,7 +429,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       bf16x8 kf[NKS];
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        const int c8 = (2 * ks + h) ^ kv_swz(n);
+        const int c8 = (2 * ks + h) ^ kv_swz<D>(n);
         kf[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
       }
       const int grp = lane >> 4, gl = lane & 15;
@@ -432,8 +441,8 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int c = 0; c < 2; ++c) {
           const int key0 = 16 * c + 4 * h + (gl >> 2);
           const int key1 = key0 + 8;
-          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz(key0))) * 8 + (dv & 7));
-          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz(key1))) * 8 + (dv & 7));
+          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz<D>(key0))) * 8 + (dv & 7));
+          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz<D>(key1))) * 8 + (dv & 7));
           vf[db][c] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
       }
