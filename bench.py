@@ -7,7 +7,8 @@ Prints ONE JSON line: ms per call, effective TFLOP/s on executed pairs
 (4 d per executed query-key pair), the output's error against dense attention,
 the roofline of the dominant kernel (block-sparse attention, bf16 MFMA) timed
 with HIP events on the stream it runs on, and the CPU oracle timed on one head
-of the same workload on this host's cores.
+of the same workload on this host's cores (whole call extrapolated), plus an
+fp64 dense cross-check of the dense reference on strided rows.
 """
 from __future__ import annotations
 
@@ -87,24 +88,61 @@ def generate(wl, torch):
     return q, k, v, host
 
 
-def cpu_baseline(wl, host, density):
-    """The oracle, as it is, on head (0, 0) of the same inputs: plan + attend."""
+def head_inputs(wl, b, h):
+    """Host copies of one head's inputs, exactly as placed in HBM."""
+    qh, kh, vh, _, _ = W.make_head(wl, b, h)
+    if wl.dtype == "bf16":
+        qh, kh, vh = W.bf16_round(qh), W.bf16_round(kh), W.bf16_round(vh)
+    return qh, kh, vh
+
+
+def cpu_baseline(wl, host, density, n_heads=1):
+    """The oracle, as it is, on the first `n_heads` heads of the same inputs:
+    plan + attend, timed per head and summed; the whole call (all B*H heads)
+    is extrapolated from the mean per head when fewer heads are timed."""
     import oracle
     oracle.build(force=False)
     ck, cq = wl.groups()
-    t0 = time.perf_counter()
-    out, pl = oracle.run(host["q"], host["k"], host["v"], n_text=wl.n_text,
-                         n_sampled=wl.n_sampled, r_k=wl.r_k, r_q=wl.r_q, c_k=ck, c_q=cq,
-                         iters=wl.kmeans_iters, density=float(np.float32(density)),
-                         n_probes=wl.n_probes, r=wl.resid_rank, lam=float(np.float32(wl.ridge)))
-    dt = time.perf_counter() - t0
     n = wl.n
-    exec_pairs = int(pl["stats"][0]) + len(pl["probes"]) * n
+    total = wl.batch * wl.heads
+    n_heads = max(1, min(n_heads, total))
+    dt = 0.0
+    exec_pairs = 0
+    for bh in range(n_heads):
+        b, h = divmod(bh, wl.heads)
+        qh, kh, vh = (host["q"], host["k"], host["v"]) if bh == 0 else head_inputs(wl, b, h)
+        t0 = time.perf_counter()
+        out, pl = oracle.run(qh, kh, vh, n_text=wl.n_text,
+                             n_sampled=wl.n_sampled, r_k=wl.r_k, r_q=wl.r_q, c_k=ck, c_q=cq,
+                             iters=wl.kmeans_iters, density=float(np.float32(density)),
+                             n_probes=wl.n_probes, r=wl.resid_rank, lam=float(np.float32(wl.ridge)))
+        dt += time.perf_counter() - t0
+        exec_pairs += int(pl["stats"][0]) + len(pl["probes"]) * n
     flops = 4.0 * wl.d * exec_pairs
+    per_call = dt / n_heads * total
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle", "seconds": dt,
-            "sample": f"1 of {wl.batch * wl.heads} heads (b=0, h=0) at full size N={n}: "
-                      f"plan + attend, {exec_pairs} executed pairs"}
+            "sample": f"{n_heads} of {total} heads (from b=0, h=0) at full size N={n}: "
+                      f"plan + attend, {exec_pairs} executed pairs",
+            "ms_per_call": round(per_call * 1e3, 1),
+            "ms_per_call_kind": "measured (all heads)" if n_heads == total else
+                                f"extrapolated: mean of {n_heads} head(s) x {total} heads"}
+
+
+def dense_crosscheck(wl, host, dense_gpu, out_gpu, rows=1024):
+    """fp64 dense attention of the oracle on `rows` strided rows of head (0, 0),
+    against the GPU's dense reference (the MFMA kernel the error readout uses)
+    and against the SparsePR output, on the same rows."""
+    import oracle
+    oracle.build(force=False)
+    idx = W.strided_rows(wl.n, rows)
+    ref = oracle.dense_rows(host["q"], host["k"], host["v"], idx)
+    dg = dense_gpu[0, 0, idx].float().cpu().numpy().astype(np.float64)
+    og = out_gpu[0, 0, idx].float().cpu().numpy().astype(np.float64)
+    nrm = np.linalg.norm(ref)
+    return {"rows": int(len(idx)), "head": [0, 0],
+            "rel_l2_gpu_dense_vs_fp64": round(float(np.linalg.norm(dg - ref) / nrm), 8),
+            "rel_l2_sparsepr_vs_fp64": round(float(np.linalg.norm(og - ref) / nrm), 6)}
 
 
 def main():
@@ -116,6 +154,9 @@ def main():
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention error check")
+    ap.add_argument("--cpu-heads", type=int, default=1,
+                    help="heads the CPU oracle baseline runs (the whole call is extrapolated "
+                         "from their mean when fewer than all)")
     ap.add_argument("--warm-start", action="store_true",
                     help="steady state of consecutive calls: both k-means start from the previous "
                          "call's centroids and run 2 assignments; calls alternate between the "
@@ -279,6 +320,7 @@ def main():
                      "unit_of_work": f"one call's sparse-attention launches ({nseg} key segments)"},
     }
 
+    dense = None
     if not args.no_dense:
         ql, kl, vl = inputs[(ncall[0] - 1) % len(inputs)]  # the inputs of the last call
         dense = S.dense_attention(ql, kl, vl)
@@ -293,12 +335,26 @@ def main():
         result["row_err_mean"] = round(row.mean().item(), 6)
         result["row_err_p99"] = round(torch.quantile(row[:: max(1, row.numel() // 1000000)], 0.99).item(), 6)
         log(f"rel-L2 vs dense {rel:.5f}")
-        del dense, o, dn, diff, ref, row
+        # the same plan with the repair off: the hard-drop output of every row
+        # (probe rows included), read back head by head from the workspace
+        num = den = 0.0
+        for bh in range(wl.batch * wl.heads):
+            b, h = divmod(bh, wl.heads)
+            osp = torch.from_numpy(op.export(bh, fields=["o_sparse"])["o_sparse"]).to(q.device)
+            dh = dn[b, h]
+            num += (osp - dh).double().pow(2).sum().item()
+            den += dh.double().pow(2).sum().item()
+        result["rel_l2_hard_drop"] = round((num / den) ** 0.5, 6)
+        log(f"rel-L2 vs dense of the hard-drop output (repair off) {result['rel_l2_hard_drop']:.5f}")
+        del o, dn, diff, ref, row
 
     if not args.no_cpu_baseline:
-        log("CPU oracle on one head ...")
-        result["cpu_baseline"] = cpu_baseline(wl, host, args.density)
+        log(f"CPU oracle on {args.cpu_heads} head(s) ...")
+        result["cpu_baseline"] = cpu_baseline(wl, host, args.density, args.cpu_heads)
         log(f"CPU oracle: {result['cpu_baseline']['seconds']:.1f}s")
+        if dense is not None and not args.warm_start and not gqa:
+            result["dense_crosscheck"] = dense_crosscheck(wl, host, dense, out)
+            log(f"dense cross-check: {result['dense_crosscheck']}")
 
     print(json.dumps(result), flush=True)
 

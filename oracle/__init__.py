@@ -16,6 +16,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sparsepr_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "libsparsepr_oracle.so")
+# AddressSanitizer + UndefinedBehaviorSanitizer build of the same source, used
+# when SPARSEPR_ORACLE_SANITIZE=1 (the process must preload the gcc runtimes,
+# see sanitize_env())
+_SAN_PATH = os.path.join(_HERE, "libsparsepr_oracle_san.so")
 _lib = None
 
 # Portable x86-64-v3 code (the library travels to other hosts); no
@@ -24,21 +28,47 @@ CFLAGS = ["-O3", "-march=x86-64-v3", "-fopenmp", "-ffp-contract=off", "-fno-fast
           "-shared", "-fPIC", "-std=c11", "-Wall"]
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc into oracle/libsparsepr_oracle.so."""
-    if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp"
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined"]
+
+
+def _sanitized() -> bool:
+    return os.environ.get("SPARSEPR_ORACLE_SANITIZE", "") == "1"
+
+
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc into oracle/libsparsepr_oracle.so, or with
+    sanitize=True into oracle/libsparsepr_oracle_san.so (ASan + UBSan)."""
+    sanitize = sanitize or _sanitized()
+    path = _SAN_PATH if sanitize else _LIB_PATH
+    if force or not os.path.exists(path):
+        tmp = path + ".tmp"
+        flags = CFLAGS + (SAN_FLAGS if sanitize else [])
+        subprocess.check_call(["gcc", *flags, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, path)
+    return path
+
+
+def sanitize_env() -> dict:
+    """Environment for a process that loads the sanitizer builds: the gcc
+    ASan/UBSan runtimes preloaded (the interpreter itself is not
+    instrumented), leak checking off (the interpreter's own allocations)."""
+    rt = [subprocess.check_output(["gcc", f"-print-file-name={n}"], text=True).strip()
+          for n in ("libasan.so", "libubsan.so")]
+    env = dict(os.environ)
+    env.update({"LD_PRELOAD": " ".join(rt), "ASAN_OPTIONS": "detect_leaks=0:abort_on_error=1",
+                "UBSAN_OPTIONS": "print_stacktrace=1:halt_on_error=1",
+                "SPARSEPR_ORACLE_SANITIZE": "1"})
+    return env
 
 
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
-            build()
-        _lib = ctypes.CDLL(_LIB_PATH)
+        path = _SAN_PATH if _sanitized() else _LIB_PATH
+        if not os.path.exists(path):
+            build(sanitize=_sanitized())
+        _lib = ctypes.CDLL(path)
     return _lib
 
 

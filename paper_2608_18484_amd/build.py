@@ -51,5 +51,30 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-side sanitizer build: api.cpp (argument validation, workspace layout,
+# export/import, timing) holds no device code, so g++ compiles it with
+# AddressSanitizer and UndefinedBehaviorSanitizer and it is linked with the
+# regular kernel objects into libsparsepr_san.so.  The binding loads it when
+# SPARSEPR_LIB points there; the process must preload the gcc runtimes.
+SAN_LIB = os.path.join(HERE, "libsparsepr_san.so")
+HOST_SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=undefined"]
+
+
+def build_sanitized() -> str:
+    build()
+    api = os.path.join(BUILD, "api_san.o")
+    host_cc = ["g++", "-std=c++17", "-fPIC", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
+    subprocess.check_call([*host_cc, *HOST_SAN_FLAGS, "-c", os.path.join(CSRC, "api.cpp"), "-o", api])
+    objs = [os.path.join(BUILD, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "api.cpp"]
+    link = ["g++", "-shared", *HOST_SAN_FLAGS, "-o", SAN_LIB, api, *objs,
+            "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"]
+    subprocess.check_call(link)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if len(sys.argv) > 1 and sys.argv[1] == "--sanitize":
+        print(build_sanitized())
+    else:
+        print(build(verbose=True))

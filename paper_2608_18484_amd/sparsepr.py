@@ -13,7 +13,9 @@ from typing import Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libsparsepr.so")
+# SPARSEPR_LIB selects another build of the same library (the host-side
+# sanitizer build of build.py --sanitize); the default is the in-tree build
+LIB_PATH = os.environ.get("SPARSEPR_LIB") or os.path.join(HERE, "libsparsepr.so")
 
 F32, BF16 = 0, 1
 FLAG_NONFINITE_INPUT, FLAG_FIT_NOT_PD, FLAG_BUDGET_BELOW_FORCED, FLAG_EIG_JACOBI = 1, 2, 4, 8
