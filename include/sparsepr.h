@@ -42,7 +42,8 @@
  *    output and the workspace alive until that work has completed.  Only
  *    sparsepr_get_stats and sparsepr_plan_export synchronise the stream.
  *  - The caller owns all memory.  The library never allocates device memory:
- *    everything it needs lives in the caller's workspace.
+ *    everything it needs lives in the caller's workspace (or, for a plan made
+ *    by sparsepr_plan_create_static, in the library's static device array).
  *  - Every entry point returns a status; no C++ exception crosses the ABI.
  *    Arguments are validated on the host before anything is enqueued, and a
  *    call that fails validation has no side effects.  sparsepr_last_error()
@@ -258,6 +259,24 @@ sparsepr_status sparsepr_workspace_size(const sparsepr_shape* shape, const spars
  * rounding of the regrouped tiles. */
 sparsepr_status sparsepr_plan_create(const sparsepr_shape* shape, const sparsepr_params* params,
                                      void* workspace, size_t bytes, sparsepr_plan_t* out);
+
+/* For callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same as
+ * sparsepr_plan_create, but the plan is bound to a file-scope device array of
+ * the library (64 MiB; each device the library runs on holds one copy until
+ * the process ends) instead of a caller workspace.  Nothing is allocated: no
+ * hipMalloc, hipFree or allocating library routine.  The array's address on
+ * the current device is looked up on the first call on that device.
+ * Shapes whose workspace (sparsepr_workspace_size) exceeds 64 MiB are
+ * rejected with WORKSPACE_TOO_SMALL.  One device has one array: while a plan
+ * made by this entry point is alive (until sparsepr_plan_destroy), another
+ * call on the same device fails with INVALID_ARGUMENT; work enqueued for it
+ * on several streams at once races like any plan used concurrently.  The
+ * array keeps what the last plan left; the plan clears what it must start
+ * from.  The returned plan is used with sparsepr_plan, sparsepr_attend and the
+ * other calls exactly like one from sparsepr_plan_create. */
+sparsepr_status sparsepr_plan_create_static(const sparsepr_shape* shape,
+                                            const sparsepr_params* params, sparsepr_plan_t* out);
 
 /* Response-Coupled Partitioning, routing and probe choice for every head
  * (Sec. 4.1, Sec. 4.3, App. A.2, App. B).  Reads Q and K only (values never

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsparsepr.so")
-SOURCES = ["plan_kernels.hip", "attn_kernels.hip", "fit_kernels.hip", "api.cpp"]
+SOURCES = ["plan_kernels.hip", "attn_kernels.hip", "fit_kernels.hip", "noalloc.hip", "api.cpp"]
 ARCH = os.environ.get("SPARSEPR_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -307,7 +307,13 @@ struct sparsepr_plan_s {
   hipEvent_t ev_att[kRing][5] = {};
   int n_plan = 0, n_att = 0;  // pending (recorded, not yet harvested) calls
   sparsepr_timings acc{};
+  int static_dev = -1;  // device whose static scratch array this plan holds (-1: none)
 };
+
+namespace sparsepr {
+sparsepr_status set_error(sparsepr_status st, const std::string& msg) { return fail(st, msg); }
+void mark_static_plan(sparsepr_plan_t plan, int dev) { plan->static_dev = dev; }
+}  // namespace sparsepr
 
 namespace {
 
@@ -713,6 +719,7 @@ sparsepr_status sparsepr_get_timings(sparsepr_plan_t plan, sparsepr_timings* out
 void sparsepr_plan_destroy(sparsepr_plan_t plan) {
   if (!plan) return;
   destroy_events(plan);
+  if (plan->static_dev >= 0) release_static_scratch(plan->static_dev);
   delete plan;
 }
 

@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "../../include/sparsepr.h"
 
 namespace sparsepr {
@@ -157,5 +159,15 @@ void launch_attend(const Geom& g, const Work* wq, const void* q, const void* k, 
 void launch_fit_correct(const Geom& g, const Work& w0, void* out, hipStream_t s, hipEvent_t* ev);
 void launch_dense(const Geom& g, const void* q, const void* k, const void* v, void* out,
                   float* part, hipStream_t s);
+
+// ---- plans on the static scratch array (noalloc.hip) ---------------------
+// Size of the file-scope device array behind sparsepr_plan_create_static.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+// Record the calling thread's error message and return `st` (api.cpp).
+sparsepr_status set_error(sparsepr_status st, const std::string& msg);
+// Mark a plan as holding device `dev`'s static array; destroying it releases
+// the array (api.cpp / noalloc.hip).
+void mark_static_plan(sparsepr_plan_t plan, int dev);
+void release_static_scratch(int dev);
 
 }  // namespace sparsepr

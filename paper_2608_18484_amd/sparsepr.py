@@ -83,7 +83,7 @@ EXPORTED = ["sparsepr_params_default", "sparsepr_workspace_size", "sparsepr_plan
             "sparsepr_plan", "sparsepr_attend", "sparsepr_dense_workspace_size",
             "sparsepr_dense_attend", "sparsepr_get_stats", "sparsepr_plan_export",
             "sparsepr_plan_import", "sparsepr_set_profiling", "sparsepr_get_timings",
-            "sparsepr_plan_destroy", "sparsepr_last_error"]
+            "sparsepr_plan_destroy", "sparsepr_last_error", "sparsepr_plan_create_static"]
 
 _lib = None
 
@@ -204,18 +204,27 @@ def _stream(stream):
 class SparsePR:
     """One SparsePR operator instance bound to a shape, parameters and a workspace."""
 
-    def __init__(self, shape: Shape, params: Params, device="cuda"):
+    def __init__(self, shape: Shape, params: Params, device="cuda", static=False):
+        """static=True binds the plan to the library's static scratch array of
+        the current device (sparsepr_plan_create_static: nothing is
+        allocated; one such plan per device at a time, small shapes only)."""
         import torch
         self.shape, self.params = shape, params
         nbytes = ctypes.c_size_t(0)
         _check(lib().sparsepr_workspace_size(ctypes.byref(shape), ctypes.byref(params),
                                              ctypes.byref(nbytes)))
         self.workspace_bytes = nbytes.value
-        self.workspace = torch.empty(max(nbytes.value, 256), dtype=torch.uint8, device=device)
         self.handle = ctypes.c_void_p()
-        _check(lib().sparsepr_plan_create(ctypes.byref(shape), ctypes.byref(params),
-                                          _ptr(self.workspace), ctypes.c_size_t(self.workspace.numel()),
-                                          ctypes.byref(self.handle)))
+        if static:
+            self.workspace = None
+            _check(lib().sparsepr_plan_create_static(ctypes.byref(shape), ctypes.byref(params),
+                                                     ctypes.byref(self.handle)))
+        else:
+            self.workspace = torch.empty(max(nbytes.value, 256), dtype=torch.uint8, device=device)
+            _check(lib().sparsepr_plan_create(ctypes.byref(shape), ctypes.byref(params),
+                                              _ptr(self.workspace),
+                                              ctypes.c_size_t(self.workspace.numel()),
+                                              ctypes.byref(self.handle)))
         n = shape.n_q
         ntext = params.n_dense_prefix
         nv = n - ntext
@@ -225,11 +234,15 @@ class SparsePR:
         self.cq_t = self.cq + (ntext > 0)
         self.m = min(params.n_probes, nv)
 
-    def __del__(self):
+    def close(self):
+        """Destroy the plan handle now (a static plan releases its device's array)."""
         h = getattr(self, "handle", None)
         if h is not None and h.value and _lib is not None:
             _lib.sparsepr_plan_destroy(h)
-            self.handle = None
+        self.handle = None
+
+    def __del__(self):
+        self.close()
 
     def plan(self, q, k, stream=None):
         check_tensors(self.shape, q=q, k=k)
