@@ -137,7 +137,7 @@ enum {
   ST_NE_Q = 8,
   ST_NE_K = 9,
   ST_RESCAN = 10,
-  ST_FIT_RANK = 10,
+  ST_FIT_RANK = 11,
 };
 
 // ---- plan kernels -------------------------------------------------------

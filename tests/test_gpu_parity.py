@@ -167,6 +167,17 @@ def test_stats_accounting(orc):
     assert abs(st["rho_exec"] - st["rho_route"] - wl.n_probes / n) < 1e-12
     assert st["rho_exec"] <= wl.density + 1e-9
     assert st["status_flags"] == 0
+    # the attend half (fit rank, probes) leaves the plan's counters alone:
+    # the exact-rescan count read after plan equals the one after attend
+    op = r["op"]
+    op.plan(r["tq"], r["tk"])
+    torch.cuda.synchronize()
+    st_plan = op.stats()
+    out = torch.empty_like(r["tq"])
+    op.attend(r["tq"], r["tk"], r["tv"], out)
+    st_att = op.stats()
+    assert st_plan["kmeans_rescans"] == st_att["kmeans_rescans"]
+    assert st_att["kmeans_rescans"] >= 0
 
 
 def test_import_oracle_plan(orc):
