@@ -635,7 +635,11 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   const int j = jbase + h * 32 + n;
   if (j >= a.n) return;
   const float T1 = h ? t1[1] : t1[0], T2 = h ? t2[1] : t2[0], T3 = h ? t3[1] : t3[0];
-  const int i1 = (int)(__float_as_uint(T1) & imask), i2 = (int)(__float_as_uint(T2) & imask);
+  // the packed indices are below C whenever a real centroid has a finite
+  // score; non-finite coordinates (flagged by k_project) could leave a
+  // padding index or NaN bits, so the indices are clamped into range
+  const int i1 = min((int)(__float_as_uint(T1) & imask), a.C - 1);
+  const int i2 = min((int)(__float_as_uint(T2) & imask), a.C - 1);
   const float xn = a.xn[(size_t)bh * a.n + j];
   const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
   const float ek = ldexpf(1.f, ib - 22);
@@ -730,6 +734,7 @@ __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
           best = rs[w2];
           bi = ri[w2];
         }
+      if (bi >= a.C) bi = 0;  // no finite score (non-finite input, flagged): keep labels in range
       const int old = lab[j];
       lab[j] = bi;
       if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
