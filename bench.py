@@ -118,6 +118,8 @@ def cpu_baseline(wl, host, density, n_heads=1):
                              n_probes=wl.n_probes, r=wl.resid_rank, lam=float(np.float32(wl.ridge)))
         dt += time.perf_counter() - t0
         exec_pairs += int(pl["stats"][0]) + len(pl["probes"]) * n
+        if n_heads > 1:
+            log(f"CPU oracle: head {bh + 1}/{n_heads} done, {dt:.1f}s so far")
     flops = 4.0 * wl.d * exec_pairs
     per_call = dt / n_heads * total
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
