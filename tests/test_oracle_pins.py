@@ -864,3 +864,75 @@ def test_semantic_partition_clusters_the_raw_rows(orc):
     kr = orc.plan(q, k, partition=2, **kw)
     assert np.array_equal(kr["labels_kv"], resp["labels_kv"])
     assert np.array_equal(kr["labels_q"], sem["labels_q"])
+
+
+# --- the oracle's composite entry points against their pinned steps --------
+# plan() and attend() chain the steps pinned above; these tests rebuild each
+# composite from those steps in the paper's order (Sec. 4.1 / App. B.1-B.2,
+# Sec. 4.3, App. A.2 / A.3), so a wiring slip in the composite (a wrong count
+# into M_Q, the wrong centroids for the probes, the budget without the probe
+# reservation, the text group) fails here even though every step passes.
+
+def _composed_plan(orc, q, k, nt, m_s, rk, rq, ck, cq, iters, density, m):
+    n, d = q.shape
+    qv, kv = q[nt:], k[nt:]
+    nv = n - nt
+    fk, _ = orc.response_basis(orc.key_metric(qv, m_s), rk)
+    phik = orc.project(kv, fk)
+    labk, _, cntk, _ = orc.kmeans(phik, ck, iters)
+    kbar, cnt2 = orc.group_mean(kv, labk, ck)
+    assert np.array_equal(cnt2, cntk)
+    fq, _ = orc.response_basis(orc.query_metric(kbar, cntk), rq)
+    phiq = orc.project(qv, fq, rms=True, eps=1e-6)
+    labq, centq, cntq, _ = orc.kmeans(phiq, cq, iters)
+    qbar, _ = orc.group_mean(qv, labq, cq)
+    prio = orc.route_priorities(qbar, cntq, kbar, cntk)
+    mm = min(m, nv)
+    budget = int(np.floor(density * nv * nv)) - mm * n
+    zv, _ = orc.route_select(prio, cntq, cntk, budget)
+    probes, w = orc.probe_select(phiq, labq, centq, m)
+    cq_t, ck_t = cq + (nt > 0), ck + (nt > 0)
+    z = np.zeros((cq_t, ck_t), np.uint8)
+    z[:cq, :ck] = zv
+    if nt:
+        z[:, ck] = 1
+        z[cq, :] = 1
+    lq = np.concatenate([np.full(nt, cq, np.int32), labq])
+    lk = np.concatenate([np.full(nt, ck, np.int32), labk])
+    return dict(labels_q=lq, labels_kv=lk, z=z, probes=probes + nt, w=w, fk=fk, fq=fq,
+                phik=phik, phiq=phiq, kbar=kbar, qbar=qbar, prio=prio, cqphi=centq)
+
+
+@pytest.mark.parametrize("nt", [0, 40])
+def test_plan_composite_equals_its_steps(orc, nt):
+    q, k, _ = tiny_head(seed=3)
+    if nt:
+        rng = np.random.default_rng(7)
+        q[:nt] = rng.standard_normal((nt, q.shape[1])).astype(np.float32)
+        k[:nt] = rng.standard_normal((nt, q.shape[1])).astype(np.float32)
+    kw = dict(n_sampled=64, r_k=48, r_q=64, c_k=16, c_q=16, iters=8, density=0.25, n_probes=24)
+    pl = orc.plan(q, k, n_text=nt, **kw)
+    ref = _composed_plan(orc, q, k, nt, 64, 48, 64, 16, 16, 8, 0.25, 24)
+    for key in ("labels_q", "labels_kv", "z", "probes", "w", "fk", "fq", "phik", "phiq", "kbar",
+                "qbar", "prio", "cqphi"):
+        assert np.array_equal(np.asarray(pl[key]), np.asarray(ref[key])), key
+
+
+def test_attend_composite_equals_its_steps(orc):
+    q, k, v = tiny_head(seed=5)
+    nt = 32
+    n = q.shape[0]
+    kw = dict(n_sampled=64, r_k=48, r_q=64, c_k=16, c_q=16, iters=8, density=0.25, n_probes=24)
+    pl = orc.plan(q, k, n_text=nt, **kw)
+    out, ft = orc.attend(q, k, v, pl["labels_q"], pl["labels_kv"], pl["z"], pl["probes"], pl["w"],
+                         n_text=nt, r=6, lam=1e-3)
+    osp = orc.sparse_rows(q, k, v, pl["labels_q"], pl["labels_kv"], pl["z"])
+    pr = np.asarray(pl["probes"], np.int64)
+    od = orc.dense_rows(q, k, v, pr)
+    f2 = orc.fit(osp[pr], od, pl["w"], 6, 1e-3)
+    ref = orc.correct_rows(osp, f2)
+    ref[:nt] = osp[:nt]           # the dense prefix is exact and left as it is
+    ref[pr] = od                  # probe rows take their exact values
+    assert np.allclose(ft["mu_r"], f2["mu_r"], rtol=0, atol=0)
+    assert np.allclose(ft["g"], f2["g"], rtol=1e-12, atol=1e-14)
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-14)
