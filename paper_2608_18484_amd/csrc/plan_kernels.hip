@@ -441,14 +441,21 @@ __global__ void k_km_init(KmArgs a) {
 // The assignment is defined by the exact float scores above.  To avoid
 // scanning every centroid on the VALU, the scores are first estimated with
 // bf16 MFMA on a three-term split (x = x_hi + x_lo, c = c_hi + c_lo;
-// t~ = x_hi c_hi + x_hi c_lo + x_lo c_hi) and bounded: the neglected terms
-// are below 3.1 * 2^-16 sum|x_k c_k|, the fp32 accumulation of the 3R exact
-// bf16 products and the exact float chain each below gamma_{3R} and
-// gamma_R times sum|x_k c_k|, so with |sum| <= |x||c| every estimated score
-// is within Delta = 1.6e-4 |x| c_max + 1.2e-7 u_max of the exact one (Delta
-// below carries another factor 2).  When the best estimate beats the
-// runner-up by more than 2 Delta, its centroid is the exact argmin; every
-// other point is rescored exactly by k_km_fallback.
+// t~ = x_hi c_hi + x_hi c_lo + x_lo c_hi) and bounded.  The centroid operands
+// hold -2c (a power-of-two scaling, exact in bf16) and one more K block adds
+// the centroid norm in three bf16 parts against ones, last, so the
+// accumulator ends with the whole score u - 2 x.c and no VALU pass forms it.
+// Bounds: the neglected lo*lo terms are below 3.1 * 2^-16 sum|x_k c_k|, the
+// fp32 accumulation of the 3R exact bf16 products and the exact float chain
+// each below gamma_{3R} and gamma_R times sum|x_k c_k| (both doubled by the
+// factor 2), the norm block below four roundings of at most 2^-23 of
+// u_max + 2|x| c_max plus the 2^-24 u left out of the split, and the exact
+// score's own fma below 2^-24 (u_max + 2|x| c_max); with |sum| <= |x||c|
+// every estimated score is within
+// Delta = 1.61e-4 |x| c_max + 6.0e-7 u_max of the exact one (Delta below
+// carries another factor 2).  When the best estimate beats the runner-up by
+// more than 2 Delta, its centroid is the exact argmin; every other point is
+// rescored exactly by k_km_fallback.
 
 __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
@@ -457,7 +464,7 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
 // Points: the bf16 hi/lo split (padded to RP with zeros) and the norms are
 // written by k_project together with the coordinates.
 
-// Centroids: hi/lo split and exact squared norms (+inf for the padding rows).
+// Centroids: hi/lo split of -2c and exact squared norms (+inf for the padding rows).
 __global__ __launch_bounds__(256) void k_km_prep_cent(KmArgs a, int it) {
   // 64 centroids per block, staged in LDS by coalesced loads; thread t < 64
   // forms the squared norm of centroid b0 + t as one fmaf chain in index
@@ -487,11 +494,26 @@ __global__ __launch_bounds__(256) void k_km_prep_cent(KmArgs a, int it) {
   const int rows = min(64, a.CP - b0);
   for (int e = tid; e < rows * RP; e += 256) {
     const int r = e / RP, k = e - r * RP;
-    const float v = (b0 + r < a.C && k < R) ? cs[r][k] : 0.f;
+    const float v = (b0 + r < a.C && k < R) ? -2.f * cs[r][k] : 0.f;
     const uint16_t h = bf16_rne_bits(v);
     hi[e] = h;
     lo[e] = bf16_rne_bits(v - bf16_bits_to_f32(h));
   }
+}
+
+// The sorted-triple update on packed (score, index) values.  The packed
+// values come from integer bit operations, so the compiler would quiet each
+// one with an extra v_max before a float min or med3 (IEEE mode); the packed
+// scores are finite, so the plain instructions are issued directly.
+__device__ __forceinline__ float med3_packed(float x, float y, float z) {
+  float d;
+  asm("v_med3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(x), "v"(y), "v"(z));
+  return d;
+}
+__device__ __forceinline__ float min_packed(float x, float y) {
+  float d;
+  asm("v_min_f32 %0, %1, %2" : "=v"(d) : "v"(x), "v"(y));
+  return d;
 }
 
 // Screening: a block of 4 waves takes 256 points, 64 per wave as two sets
@@ -499,15 +521,17 @@ __global__ __launch_bounds__(256) void k_km_prep_cent(KmArgs a, int it) {
 // staged in LDS (the M side); every centroid fragment read from LDS feeds
 // both sets.  Lane (n, h) ends with the three best estimates of point n of
 // each set over half of the centroids; the halves are merged with one
-// exchange, and lane h then decides set h's point.
+// exchange, and lane h then decides set h's point.  The second launch bound
+// caps the kernel at 256 registers, so the accumulators stay in VGPRs that
+// the VALU reads directly.
 template <int RP>
-__global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
+__global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int KS = RP / 16;
   constexpr int LD = RP + 8;  // padded LDS row (bf16)
   constexpr int NPS = 2;      // sets of 32 points per wave
   __shared__ __attribute__((aligned(16))) uint16_t shi[32 * LD];
   __shared__ __attribute__((aligned(16))) uint16_t slo[32 * LD];
-  __shared__ __attribute__((aligned(16))) float su[32];
+  __shared__ __attribute__((aligned(8))) uint32_t su3[32][2];  // norm in three bf16 parts
   __shared__ float sred[4];
   const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip_assign(a, bh, it)) return;
@@ -525,6 +549,10 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       blo[ps][ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
     }
   }
+  // the norm block's point operand: ones at k = 0, 1, 2 (held by the h = 0
+  // lanes), zeros elsewhere, so the centroid lanes' k >= 3 entries drop out
+  const bf16x8 ones = __builtin_bit_cast(
+      bf16x8, h ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u));
   // Largest centroid squared norm of the head (for the error bound).
   float umax = 0.f;
   const float* cu = a.cu + (size_t)bh * a.CP;
@@ -537,14 +565,17 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   // below adds to the error bound.  Keeping (value, index) in one float lets
   // min / med3 maintain the sorted triple in three instructions per score.
   const int ib = 32 - __clz(a.CP - 1);
-  const uint32_t imask = (1u << ib) - 1u;
+  const uint32_t keep = ~((1u << ib) - 1u);
   float t1[NPS], t2[NPS], t3[NPS];
 #pragma unroll
   for (int ps = 0; ps < NPS; ++ps) t1[ps] = t2[ps] = t3[ps] = INFINITY;
+  // centroid index of accumulator register i: c0 + (i/4)*8 + h*4 + i%4
+  uint32_t cidx[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) cidx[i] = (uint32_t)((i >> 2) * 8 + h * 4 + (i & 3));
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
-  // Centroid tiles go through registers: the next tile's loads are issued
-  // before the current tile is scored, so their latency overlaps the MFMAs.
+  // Centroid tiles go through registers.
   constexpr int TPT = (32 * RP / 8 + 255) / 256;  // 16-byte pieces per thread and array
   uint4 nh[TPT], nl[TPT];
   float nu = 0.f;
@@ -564,8 +595,10 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
       }
     }
   };
-  fetch(0);
-  for (int c0 = 0; c0 < a.CP; c0 += 32) {
+  // Stage the fetched tile in LDS (every wave has finished reading the
+  // previous one), then start fetching the tile after it, so its latency
+  // overlaps the MFMAs.
+  auto stage = [&](int c0) {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < TPT; ++u) {
@@ -576,45 +609,66 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
         *(uint4*)(slo + r * LD + c8 * 8) = nl[u];
       }
     }
-    if (tid < 32) su[tid] = nu;
+    if (tid < 32) {
+      // u = p0 + p1 + p2 + e with |e| <= 2^-24 u; each subtraction is exact
+      const uint16_t p0 = bf16_rne_bits(nu);
+      const float r1 = nu - bf16_bits_to_f32(p0);
+      const uint16_t p1 = bf16_rne_bits(r1);
+      const uint16_t p2 = bf16_rne_bits(r1 - bf16_bits_to_f32(p1));
+      su3[tid][0] = (uint32_t)p0 | ((uint32_t)p1 << 16);
+      su3[tid][1] = (uint32_t)p2;
+    }
     __syncthreads();
     if (c0 + 32 < a.CP) fetch(c0 + 32);
-    f32x16 S[NPS];
+  };
+  // Scores of the staged tile: S = u - 2 x.c, the norm block last.
+  auto score = [&](f32x16 (&S)[NPS]) {
+    bf16x8 ah[KS], al[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      ah[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(shi + n * LD + ks * 16 + h * 8));
+      al[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
+    }
+    const uint2 w = *(const uint2*)&su3[n][0];
+    const bf16x8 an = __builtin_bit_cast(bf16x8, make_uint4(w.x, w.y, 0u, 0u));
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
 #pragma unroll
       for (int i = 0; i < 16; ++i) S[ps][i] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const uint4*)(shi + n * LD + ks * 16 + h * 8));
-      const bf16x8 al = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int ps = 0; ps < NPS; ++ps) {
-        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bhi[ps][ks], S[ps], 0, 0, 0);
-        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, blo[ps][ks], S[ps], 0, 0, 0);
-        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bhi[ps][ks], S[ps], 0, 0, 0);
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], bhi[ps][ks], S[ps], 0, 0, 0);
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], blo[ps][ks], S[ps], 0, 0, 0);
+        S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[ks], bhi[ps][ks], S[ps], 0, 0, 0);
+      }
+#pragma unroll
+    for (int ps = 0; ps < NPS; ++ps)
+      S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(an, ones, S[ps], 0, 0, 0);
+  };
+  // Fold a scored tile into the sorted triples.
+  auto reduce = [&](const f32x16 (&S)[NPS], int c0) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t idx = cidx[i] + (uint32_t)c0;
+#pragma unroll
+      for (int ps = 0; ps < NPS; ++ps) {
+        const float pk = __uint_as_float((__float_as_uint(S[ps][i]) & keep) | idx);
+        const float n3 = med3_packed(t2[ps], t3[ps], pk);
+        const float n2 = med3_packed(t1[ps], t2[ps], pk);
+        t1[ps] = min_packed(t1[ps], pk);
+        t2[ps] = n2;
+        t3[ps] = n3;
       }
     }
-    // register i holds centroid c0 + (i/4)*8 + h*4 + i%4
-#pragma unroll
-    for (int i4 = 0; i4 < 4; ++i4) {
-      const float4 u4 = *(const float4*)&su[i4 * 8 + h * 4];
-      const float uu[4] = {u4.x, u4.y, u4.z, u4.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t idx = (uint32_t)(c0 + i4 * 8 + h * 4 + e);
-#pragma unroll
-        for (int ps = 0; ps < NPS; ++ps) {
-          const float sh = fmaf(-2.f, S[ps][i4 * 4 + e], uu[e]);
-          const float pk = __uint_as_float((__float_as_uint(sh) & ~imask) | idx);
-          const float n3 = __builtin_amdgcn_fmed3f(t2[ps], t3[ps], pk);
-          const float n2 = __builtin_amdgcn_fmed3f(t1[ps], t2[ps], pk);
-          t1[ps] = fminf(t1[ps], pk);
-          t2[ps] = n2;
-          t3[ps] = n3;
-        }
-      }
-    }
+  };
+  fetch(0);
+  for (int c0 = 0; c0 < a.CP; c0 += 32) {
+    stage(c0);
+    f32x16 S[NPS];
+    score(S);
+    reduce(S, c0);
   }
   // merge with the other half of the centroids (lane l ^ 32, same points)
 #pragma unroll
@@ -622,9 +676,9 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
     const float ov[3] = {__shfl_xor(t1[ps], 32), __shfl_xor(t2[ps], 32), __shfl_xor(t3[ps], 32)};
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
-      const float n3 = __builtin_amdgcn_fmed3f(t2[ps], t3[ps], ov[e]);
-      const float n2 = __builtin_amdgcn_fmed3f(t1[ps], t2[ps], ov[e]);
-      t1[ps] = fminf(t1[ps], ov[e]);
+      const float n3 = med3_packed(t2[ps], t3[ps], ov[e]);
+      const float n2 = med3_packed(t1[ps], t2[ps], ov[e]);
+      t1[ps] = min_packed(t1[ps], ov[e]);
       t2[ps] = n2;
       t3[ps] = n3;
     }
@@ -638,10 +692,10 @@ __global__ __launch_bounds__(256) void k_km_assign_mfma(KmArgs a, int it) {
   // the packed indices are below C whenever a real centroid has a finite
   // score; non-finite coordinates (flagged by k_project) could leave a
   // padding index or NaN bits, so the indices are clamped into range
-  const int i1 = min((int)(__float_as_uint(T1) & imask), a.C - 1);
-  const int i2 = min((int)(__float_as_uint(T2) & imask), a.C - 1);
+  const int i1 = min((int)(__float_as_uint(T1) & ~keep), a.C - 1);
+  const int i2 = min((int)(__float_as_uint(T2) & ~keep), a.C - 1);
   const float xn = a.xn[(size_t)bh * a.n + j];
-  const float delta = 3.2e-4f * xn * sqrtf(umax) * 1.000001f + 2.4e-7f * umax;
+  const float delta = 3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax;
   const float ek = ldexpf(1.f, ib - 22);
   int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   int label;
@@ -2116,7 +2170,6 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
     k_route_topp<<<dim3(g.CQ, BH), 256, (size_t)np2 * 8, s>>>(g, w, np2);
   }
   k_sel_init<<<BH, 256, 0, s>>>(g, w);
-  const int64_t ncell = (int64_t)g.CQ * g.CK;
   const int gsel = std::max(1, std::min(g.CQ, 512));
   for (int p = 0; p < kSelPasses; ++p) {
     k_sel_hist<<<dim3(gsel, BH), 256, 0, s>>>(g, w, p);
