@@ -842,41 +842,71 @@ __global__ __launch_bounds__(1024) void k_sort_scan(KmArgs a, int it) {
   if (tid == 0) off[a.C] = total;
 }
 
-// Counting sort, pass 3: stable scatter.  One wave per block of rows walks its
-// rows in order, 64 at a time: each lane reads its label's next slot, its
-// stable rank among the lanes holding the same label comes from a ballot per
-// distinct label, and the last such lane advances the slot.
-__global__ __launch_bounds__(64) void k_sort_scatter(KmArgs a, int it) {
-  extern __shared__ int pos[];
-  const int bh = blockIdx.y, blk = blockIdx.x, lane = threadIdx.x;
+// Counting sort, pass 3: stable scatter.  A block of 4 waves takes the
+// block's rows; wave w owns rows [j0 + 256 w, j0 + 256 (w + 1)).  Each wave
+// counts its labels, the per-label slots of the waves follow by a prefix over
+// the waves, and every wave then walks its rows in order, 64 at a time: each
+// lane reads its label's next slot; the slice's labels go through LDS, every
+// lane marks the lanes holding its label, its stable rank is the number of
+// them before it, and the lane with the last rank advances the slot.
+constexpr int kScatterWaves = 4;
+constexpr int kScatterRows = kSortBlock / kScatterWaves;  // rows per wave
+
+__host__ __device__ __forceinline__ int sort_scatter_cstride(int C) { return (C + 3) & ~3; }
+
+__global__ __launch_bounds__(256) void k_sort_scatter(KmArgs a, int it) {
+  // [kScatterWaves][cs] per-wave counts, then slots; [kScatterWaves][64] slice labels
+  extern __shared__ __attribute__((aligned(16))) int sm[];
+  const int cs = sort_scatter_cstride(a.C);
+  const int bh = blockIdx.y, blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip(a, bh, it)) return;
+  int* pos = sm + wv * cs;
+  int* sl = sm + kScatterWaves * cs + wv * 64;
+  const int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  const int j0 = blk * kSortBlock + wv * kScatterRows;
+  const int j1 = min(a.n, j0 + kScatterRows);
+  for (int b = lane; b < a.C; b += 64) pos[b] = 0;
+  // the wave's own counts (its LDS accesses complete in program order)
+  for (int j = j0 + lane; j < j1; j += 64) atomicAdd(&pos[lab[j]], 1);
+  __syncthreads();
+  // slots: the block's start of each label plus the counts of earlier waves
   const int32_t* hist = a.blkhist + ((size_t)bh * a.nblk + blk) * a.cmax;
   const int32_t* off = a.off + (size_t)bh * a.offstride;
-  for (int b = lane; b < a.C; b += 64) pos[b] = off[b] + hist[b];
+  for (int b = tid; b < a.C; b += 256) {
+    int run = off[b] + hist[b];
+#pragma unroll
+    for (int w = 0; w < kScatterWaves; ++w) {
+      const int c = sm[w * cs + b];
+      sm[w * cs + b] = run;
+      run += c;
+    }
+  }
   __syncthreads();
-  const int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   int32_t* perm = a.perm + (size_t)bh * a.N;
-  const int j0 = blk * kSortBlock, j1 = min(a.n, j0 + kSortBlock);
-  const uint64_t below = (1ull << lane) - 1ull;
+  const uint32_t below_lo = lane >= 32 ? 0xffffffffu : (1u << lane) - 1u;
+  const uint32_t below_hi = lane <= 32 ? 0u : (1u << (lane - 32)) - 1u;
   for (int s = j0; s < j1; s += 64) {
     const int j = s + lane;
     const bool valid = j < j1;
-    const int L = valid ? lab[j] : -1;
-    // the block is one wave: its LDS accesses complete in program order, so
-    // this read sees the previous slice's updates without a barrier
+    const int L = valid ? lab[j] : -1 - lane;  // invalid lanes match nothing
     const int base = valid ? pos[L] : 0;
-    uint64_t active = __ballot(valid);
-    int rank = 0, cnt = 0;
-    while (active) {
-      const int first = __ffsll((unsigned long long)active) - 1;
-      const int Lf = __builtin_amdgcn_readlane(L, first);
-      const uint64_t m = __ballot(L == Lf) & active;
-      if (L == Lf) {
-        rank = __popcll(m & below);
-        cnt = __popcll(m);
+    sl[lane] = L;
+    uint32_t mlo = 0u, mhi = 0u;  // lanes holding this lane's label
+#pragma unroll
+    for (int k4 = 0; k4 < 16; ++k4) {
+      const int4 q = *(const int4*)&sl[4 * k4];
+      const int qv[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int k = 4 * k4 + e;
+        if (k < 32)
+          mlo |= (qv[e] == L ? 1u : 0u) << k;
+        else
+          mhi |= (qv[e] == L ? 1u : 0u) << (k - 32);
       }
-      active &= ~m;
     }
+    const int rank = __popc(mlo & below_lo) + __popc(mhi & below_hi);
+    const int cnt = __popc(mlo) + __popc(mhi);
     if (valid) {
       perm[base + rank] = a.row0 + j;
       if (rank == cnt - 1) pos[L] = base + cnt;
@@ -2043,7 +2073,8 @@ static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
   const int shm = (a.C + 1 + 17) * (int)sizeof(int);
   k_sort_hist<<<dim3(a.nblk, BH), 256, a.C * sizeof(int), s>>>(a, it);
   k_sort_scan<<<BH, 1024, shm, s>>>(a, it);
-  k_sort_scatter<<<dim3(a.nblk, BH), 64, a.C * sizeof(int), s>>>(a, it);
+  k_sort_scatter<<<dim3(a.nblk, BH), 256,
+                   (size_t)kScatterWaves * (sort_scatter_cstride(a.C) + 64) * sizeof(int), s>>>(a, it);
 }
 
 template <int MAXR>
