@@ -916,10 +916,11 @@ __global__ __launch_bounds__(256) void k_sort_scatter(KmArgs a, int it) {
 
 // Centroid update: per group, double sums of the members' coordinates in
 // ascending row order (the stable permutation order) / count, rounded to
-// float; an empty group keeps its centroid.  One wave per group: the
-// members' rows are fetched 64 at a time (lane i holds member m0 + i) and
-// exchanged by readlane; lane l owns coordinates l and l + 64, whose values
-// are loaded eight members at a time and added in ascending member order.
+// float; an empty group keeps its centroid (and its assignment operands).
+// One wave per group: the members' rows are fetched 64 at a time (lane i
+// holds member m0 + i) and exchanged by readlane; lane l owns coordinates l
+// and l + 64, whose values are loaded eight members at a time and added in
+// ascending member order.
 __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (km_changed(a, bh)[it] == 0) return;
@@ -968,8 +969,34 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
     members(std::false_type{});
   const double inv = (double)(s1 - s0);
   float* c = a.cent + ((size_t)bh * a.C + b) * R;
-  if (lane < R) c[lane] = (float)(sum0 / inv);
-  if (lane + 64 < R) c[lane + 64] = (float)(sum1 / inv);
+  const float v0 = (float)(sum0 / inv), v1 = (float)(sum1 / inv);
+  if (lane < R) c[lane] = v0;
+  if (lane + 64 < R) c[lane + 64] = v1;
+  // The next assignment's operands of this centroid (as k_km_prep_cent
+  // forms them): the hi/lo split of -2c and the squared norm, one fmaf chain
+  // in coordinate order through LDS.
+  __shared__ float cw[4][128];
+  const int RP = a.RP;
+  uint16_t* hi = a.chi + ((size_t)bh * a.CP + b) * RP;
+  uint16_t* lo = a.clo + ((size_t)bh * a.CP + b) * RP;
+  if (lane < R) {
+    cw[wv][lane] = v0;
+    const uint16_t h = bf16_rne_bits(-2.f * v0);
+    hi[lane] = h;
+    lo[lane] = bf16_rne_bits(-2.f * v0 - bf16_bits_to_f32(h));
+  }
+  if (lane + 64 < R) {
+    cw[wv][lane + 64] = v1;
+    const uint16_t h = bf16_rne_bits(-2.f * v1);
+    hi[lane + 64] = h;
+    lo[lane + 64] = bf16_rne_bits(-2.f * v1 - bf16_bits_to_f32(h));
+  }
+  // one wave: its LDS writes land before its reads below
+  if (lane == 0) {
+    float u = 0.f;
+    for (int k = 0; k < R; ++k) u = fmaf(cw[wv][k], cw[wv][k], u);
+    a.cu[(size_t)bh * a.CP + b] = u;
+  }
 }
 
 // The dense-prefix rows (before row0) form the extra last group: label C and
@@ -2080,7 +2107,8 @@ static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
 template <int MAXR>
 static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   const int BH = g.BH;
-  k_km_prep_cent<<<dim3((a.CP + 63) / 64, BH), 256, 0, s>>>(a, it);
+  // the first assignment's operands; later ones come from k_km_update
+  if (it == 0) k_km_prep_cent<<<dim3((a.CP + 63) / 64, BH), 256, 0, s>>>(a, it);
   const dim3 grid((a.n + 255) / 256, BH);
   if (a.RP == 16)
     k_km_assign_mfma<16><<<grid, 256, 0, s>>>(a, it);
