@@ -408,6 +408,7 @@ struct KmArgs {
   uint16_t* chi;      // [BH][CP][RP]
   uint16_t* clo;
   float* cu;          // [BH][CP]
+  uint32_t* cn3;      // [BH][CP][2]: the norm's three bf16 parts (p0 | p1 << 16, p2)
   int32_t* fb;        // [BH][n]
   int32_t* fbcnt;     // [BH][2][T]
   int RP, CP;         // rank padded to 16, groups padded to 32 (strides of the above)
@@ -461,6 +462,17 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
+// u = p0 + p1 + p2 + e with |e| <= 2^-24 |u|: three round-to-nearest bf16
+// parts, each subtraction exact; packed as (p0 | p1 << 16, p2), the operand
+// of the assignment's norm step.
+__device__ __forceinline__ uint2 norm_parts(float u) {
+  const uint16_t p0 = bf16_rne_bits(u);
+  const float r1 = u - bf16_bits_to_f32(p0);
+  const uint16_t p1 = bf16_rne_bits(r1);
+  const uint16_t p2 = bf16_rne_bits(r1 - bf16_bits_to_f32(p1));
+  return make_uint2((uint32_t)p0 | ((uint32_t)p1 << 16), (uint32_t)p2);
+}
+
 // Points: the bf16 hi/lo split (padded to RP with zeros) and the norms are
 // written by k_project together with the coordinates.
 
@@ -488,6 +500,9 @@ __global__ __launch_bounds__(256) void k_km_prep_cent(KmArgs a, int it) {
       for (int k = 0; k < R; ++k) u = fmaf(cs[tid][k], cs[tid][k], u);
     }
     a.cu[(size_t)bh * a.CP + b0 + tid] = u;
+    // padding centroids get a huge finite norm in the MFMA step: their
+    // scores stay finite (an index packed into +inf would make a NaN)
+    ((uint2*)a.cn3)[(size_t)bh * a.CP + b0 + tid] = norm_parts(b0 + tid < a.C ? u : 3.0e38f);
   }
   uint16_t* hi = a.chi + ((size_t)bh * a.CP + b0) * RP;
   uint16_t* lo = a.clo + ((size_t)bh * a.CP + b0) * RP;
@@ -516,22 +531,46 @@ __device__ __forceinline__ float min_packed(float x, float y) {
   return d;
 }
 
+// Direct global -> LDS copies for the centroid tiles: lane l's 16 (or 4)
+// bytes land at lds + 16 l (4 l), with lds the same for the whole wave; the
+// compiler does not see these loads, so the kernel orders them with explicit
+// vmcnt waits.  No other code in this file uses M0.
+__device__ __forceinline__ void km_g2lds16(const void* src, uint32_t lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(m0)
+               : "memory");
+}
+__device__ __forceinline__ void km_g2lds4(const void* src, uint32_t lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(m0)
+               : "memory");
+}
+
 // Screening: a block of 4 waves takes 256 points, 64 per wave as two sets
 // of 32 (the N side of v_mfma_f32_32x32x16_bf16), against 32-centroid tiles
-// staged in LDS (the M side); every centroid fragment read from LDS feeds
-// both sets.  Lane (n, h) ends with the three best estimates of point n of
-// each set over half of the centroids; the halves are merged with one
-// exchange, and lane h then decides set h's point.  The second launch bound
-// caps the kernel at 256 registers, so the accumulators stay in VGPRs that
-// the VALU reads directly.
+// in LDS (the M side); every centroid fragment read from LDS feeds both
+// sets.  The tiles (hi and lo rows, padded, and the norms' bf16 parts) are
+// double-buffered and filled by direct global -> LDS copies issued one tile
+// ahead, one barrier per tile.  Lane (n, h) ends with the three best
+// estimates of point n of each set over half of the centroids; the halves
+// are merged with one exchange, and lane h then decides set h's point.  The
+// second launch bound caps the kernel at 256 registers, so the accumulators
+// stay in VGPRs that the VALU reads directly.
 template <int RP>
 __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int KS = RP / 16;
-  constexpr int LD = RP + 8;  // padded LDS row (bf16)
-  constexpr int NPS = 2;      // sets of 32 points per wave
-  __shared__ __attribute__((aligned(16))) uint16_t shi[32 * LD];
-  __shared__ __attribute__((aligned(16))) uint16_t slo[32 * LD];
-  __shared__ __attribute__((aligned(8))) uint32_t su3[32][2];  // norm in three bf16 parts
+  constexpr int LD = RP + 8;            // padded LDS row (bf16)
+  constexpr int ARR = 32 * LD * 2;      // bytes of one array (hi or lo) of a tile
+  constexpr int PPR = LD / 8;           // 16-byte pieces per padded row
+  constexpr int NPIECE = 2 * ARR / 16;  // pieces of hi + lo
+  constexpr int NINST = (NPIECE + 63) / 64;
+  constexpr int TILE = 2 * ARR + 256;   // + the 32 norms' parts
+  constexpr int NPS = 2;                // sets of 32 points per wave
+  __shared__ __attribute__((aligned(1024))) unsigned char tiles[2][TILE];
   __shared__ float sred[4];
   const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip_assign(a, bh, it)) return;
@@ -575,62 +614,54 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   for (int i = 0; i < 16; ++i) cidx[i] = (uint32_t)((i >> 2) * 8 + h * 4 + (i & 3));
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
-  // Centroid tiles go through registers.
-  constexpr int TPT = (32 * RP / 8 + 255) / 256;  // 16-byte pieces per thread and array
-  uint4 nh[TPT], nl[TPT];
-  float nu = 0.f;
-  auto fetch = [&](int c0) {
-    // padding centroids get a huge finite norm: their scores stay finite
-    // (an index packed into +inf would make a NaN) and never win.  The norm
-    // is loaded first: the wait the compiler places before overwriting `nu`
-    // then covers only loads that have already landed, not the tile's.
-    if (tid < 32) nu = (c0 + tid < a.C) ? cu[c0 + tid] : 3.0e38f;
+  const uint32_t* cn3 = a.cn3 + (size_t)bh * a.CP * 2;
+  const uint32_t lds0 = (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)&tiles[0][0];
+  // the copies of tile c0 into buffer b: piece p = inst * 64 + lane lands at
+  // byte 16 p of the buffer (row p / PPR of hi, then of lo; the padding
+  // pieces of a row fetch its first piece), then the norms' parts
+  auto issue = [&](int c0, int b) {
+    const uint32_t base = lds0 + (uint32_t)(b * TILE);
 #pragma unroll
-    for (int u = 0; u < TPT; ++u) {
-      const int i = tid + 256 * u;
-      if (i < 32 * RP / 8) {
-        const int r = i / (RP / 8), c8 = i % (RP / 8);
-        nh[u] = *(const uint4*)(chi + (size_t)(c0 + r) * RP + c8 * 8);
-        nl[u] = *(const uint4*)(clo + (size_t)(c0 + r) * RP + c8 * 8);
+    for (int i0 = 0; i0 < NINST; i0 += 4) {
+      const int inst = i0 + wv;
+      const int p = inst * 64 + lane;
+      if (inst < NINST && p < NPIECE) {
+        const int arr = p >= NPIECE / 2;
+        const int q = p - arr * (NPIECE / 2);
+        const int r = q / PPR, c8 = q - (q / PPR) * PPR;
+        const uint16_t* src = (arr ? clo : chi) + (size_t)(c0 + r) * RP + (c8 < RP / 8 ? c8 : 0) * 8;
+        km_g2lds16(src, base + (uint32_t)(inst * 1024));
       }
     }
+    if (wv == 0) km_g2lds4(cn3 + (size_t)c0 * 2 + lane, base + (uint32_t)(2 * ARR));
   };
-  // Stage the fetched tile in LDS (every wave has finished reading the
-  // previous one), then start fetching the tile after it, so its latency
-  // overlaps the MFMAs.
-  auto stage = [&](int c0) {
+  // s_waitcnt immediate (gfx9 encoding) waiting for vmcnt(0) only
+  constexpr int kWaitVm0 = 0x3f70;
+  // the point operands and the norms above are ordinary loads: wait for
+  // them once here, so no later wait of the compiler's covers the copies
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  issue(0, 0);
+  int buf = 0;
+  for (int c0 = 0; c0 < a.CP; c0 += 32, buf ^= 1) {
+    // this wave's copies of the tile have landed; after the barrier every
+    // wave's have, and every wave is done with the other buffer
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < TPT; ++u) {
-      const int i = tid + 256 * u;
-      if (i < 32 * RP / 8) {
-        const int r = i / (RP / 8), c8 = i % (RP / 8);
-        *(uint4*)(shi + r * LD + c8 * 8) = nh[u];
-        *(uint4*)(slo + r * LD + c8 * 8) = nl[u];
-      }
-    }
-    if (tid < 32) {
-      // u = p0 + p1 + p2 + e with |e| <= 2^-24 u; each subtraction is exact
-      const uint16_t p0 = bf16_rne_bits(nu);
-      const float r1 = nu - bf16_bits_to_f32(p0);
-      const uint16_t p1 = bf16_rne_bits(r1);
-      const uint16_t p2 = bf16_rne_bits(r1 - bf16_bits_to_f32(p1));
-      su3[tid][0] = (uint32_t)p0 | ((uint32_t)p1 << 16);
-      su3[tid][1] = (uint32_t)p2;
-    }
-    __syncthreads();
-    if (c0 + 32 < a.CP) fetch(c0 + 32);
-  };
-  // Scores of the staged tile: S = u - 2 x.c, the norm block last.
-  auto score = [&](f32x16 (&S)[NPS]) {
+    if (c0 + 32 < a.CP) issue(c0 + 32, buf ^ 1);
+    const unsigned char* tb = &tiles[buf][0];
+    const uint16_t* shi = (const uint16_t*)tb;
+    const uint16_t* slo = (const uint16_t*)(tb + ARR);
+    const uint32_t* su3 = (const uint32_t*)(tb + 2 * ARR);
     bf16x8 ah[KS], al[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       ah[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(shi + n * LD + ks * 16 + h * 8));
       al[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
     }
-    const uint2 w = *(const uint2*)&su3[n][0];
+    const uint2 w = *(const uint2*)&su3[2 * n];
     const bf16x8 an = __builtin_bit_cast(bf16x8, make_uint4(w.x, w.y, 0u, 0u));
+    // scores S = u - 2 x.c, the norm block last
+    f32x16 S[NPS];
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
 #pragma unroll
@@ -646,9 +677,7 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
       S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(an, ones, S[ps], 0, 0, 0);
-  };
-  // Fold a scored tile into the sorted triples.
-  auto reduce = [&](const f32x16 (&S)[NPS], int c0) {
+    // fold the tile into the sorted triples
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const uint32_t idx = cidx[i] + (uint32_t)c0;
@@ -662,13 +691,6 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
         t3[ps] = n3;
       }
     }
-  };
-  fetch(0);
-  for (int c0 = 0; c0 < a.CP; c0 += 32) {
-    stage(c0);
-    f32x16 S[NPS];
-    score(S);
-    reduce(S, c0);
   }
   // merge with the other half of the centroids (lane l ^ 32, same points)
 #pragma unroll
@@ -974,7 +996,7 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   if (lane + 64 < R) c[lane + 64] = v1;
   // The next assignment's operands of this centroid (as k_km_prep_cent
   // forms them): the hi/lo split of -2c and the squared norm, one fmaf chain
-  // in coordinate order through LDS.
+  // in coordinate order through LDS, with its three bf16 parts.
   __shared__ float cw[4][128];
   const int RP = a.RP;
   uint16_t* hi = a.chi + ((size_t)bh * a.CP + b) * RP;
@@ -996,6 +1018,7 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
     float u = 0.f;
     for (int k = 0; k < R; ++k) u = fmaf(cw[wv][k], cw[wv][k], u);
     a.cu[(size_t)bh * a.CP + b] = u;
+    ((uint2*)a.cn3)[(size_t)bh * a.CP + b] = norm_parts(u);
   }
 }
 
@@ -2200,7 +2223,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
-            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fb, w.km_fbcnt, 0, 0};
   run_kmeans(g, ak, s, warm);
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
@@ -2216,7 +2239,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   }
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
-            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_fb, w.km_fbcnt, 0, 0};
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fb, w.km_fbcnt, 0, 0};
   run_kmeans(g, aq, s, warm);
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
                                                          w.qbar, 1);
