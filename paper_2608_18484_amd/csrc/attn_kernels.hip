@@ -13,9 +13,10 @@
 // (A = 32 keys x 16 dims from LDS, B = 16 dims x 32 queries held in
 // registers), so every lane holds scores of ONE query and the online softmax
 // needs a single cross-lane exchange (lanes l and l+32).  The probabilities
-// stay in registers and feed O^T = V^T P^T directly as the B operand; V is
-// stored transposed in LDS with its keys permuted inside each 16-key chunk to
-// match the accumulator layout, so the A operand is one 16-byte LDS read.
+// stay in registers and feed O^T = V^T P^T directly as the B operand; V stays
+// row-major in LDS and its A operand V^T comes from transposing LDS reads
+// (ds_read_b64_tr_b16), the keys of each 16-key chunk taken in the order of
+// the accumulator layout.
 // K/V rows are gathered on load through the group-major permutation, so the
 // routed K/V groups are contiguous key ranges without a physical copy.
 #include <hip/hip_runtime.h>
@@ -194,23 +195,27 @@ __device__ __forceinline__ float pair_sum(float x) {
 //    that share one key list: the routed ranges of their query group in the
 //    group-major K/V copy (MODE_SPARSE), or a contiguous slice of the original
 //    K/V rows (MODE_PROBE, MODE_DENSE).
-//  * 32-key tiles, double-buffered in LDS and filled by direct global->LDS
-//    16-byte loads issued one tile ahead; the key positions of a tile are
-//    computed two tiles ahead into a ring of three slots.
+//  * 32-key tiles in LDS filled by direct global->LDS 16-byte loads: one K
+//    buffer, refilled with the next tile once every wave has read its score
+//    operands, and two V buffers, the next tile's V loading while the current
+//    one is computed; the key positions of a tile are computed two tiles
+//    ahead into a ring of three slots.  The 26 KB of LDS and at most 168
+//    registers per lane leave room for six blocks per CU (three waves per
+//    SIMD), which hide each other's latencies better than four.
 //  * S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_32x32x16_bf16; V^T
 //    fragments come from the row-major V tile through transposing LDS reads.
 //  * Online softmax in base 2 with lazy rescaling: the running maximum only
 //    moves (and O, l are rescaled) when a tile's maximum exceeds it by 2^8.
 template <int D, int MODE>
-__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_mfma(Geom g, AttnArgs A) {
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(3, 3))) void k_attn_mfma(Geom g, AttnArgs A) {
   constexpr int KT = 32;
   constexpr int CH = D / 8;                    // 16-byte chunks per row
   constexpr int NKS = D / 16;                  // k-steps of Q K^T
   constexpr int NDB = D / 32;                  // 32-wide blocks of O^T
   constexpr int LPT = KT * CH / 128;           // 16-byte loads per thread per tensor per tile
-  constexpr int MAXR = 512;                    // routed ranges staged in LDS
-  // K and V tiles, double-buffered: tiles[0..1] = K, tiles[2..3] = V
-  __shared__ __attribute__((aligned(1024))) uint16_t tiles[4][KT * D];
+  constexpr int MAXR = 128;                    // routed ranges of the segment staged in LDS
+  // tiles[0] = K (one buffer), tiles[1..2] = V (double-buffered)
+  __shared__ __attribute__((aligned(1024))) uint16_t tiles[3][KT * D];
   __shared__ int spos[3][KT];
   __shared__ int2 srng[MODE == MODE_SPARSE ? MAXR : 1];
 
@@ -274,12 +279,13 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
   const bool wave_active = wv * 32 < w.nrows;
 
-  // routed ranges of the query group (positions in the group-major K/V),
-  // staged in LDS when they fit; never read through generic pointers (flat
-  // accesses would make the compiler wait for the in-flight tile loads).
-  // Only the ranges meeting the key segment [seg_lo, seg_hi) are walked, each
-  // clipped to it: ranges are sorted and disjoint, so they are the run
-  // [j0, j0 + nseg) and their clipped lengths sum to this launch's keys.
+  // routed ranges of the query group (positions in the group-major K/V);
+  // never read through generic pointers (flat accesses would make the
+  // compiler wait for the in-flight tile loads).  Only the ranges meeting the
+  // key segment [seg_lo, seg_hi) are walked, each clipped to it: ranges are
+  // sorted and disjoint, so they are the run [j0, j0 + nseg) and their
+  // clipped lengths sum to this launch's keys; the first MAXR of the run are
+  // staged in LDS.
   typedef const __attribute__((address_space(1))) int* gptr_int;
   gptr_int grng = nullptr;
   int nr = 0, j0 = 0, nseg = 0;
@@ -287,11 +293,9 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   if (MODE == MODE_SPARSE) {
     grng = (gptr_int)(A.rng + ((size_t)bh * g.CQt + w.a) * g.CKt);
     nr = A.rng_cnt[(size_t)bh * g.CQt + w.a];
-    for (int i = tid; i < min(nr, MAXR); i += 128) srng[i] = make_int2(grng[2 * i], grng[2 * i + 1]);
-    __syncthreads();
     int below = 0, before_end = 0, keys = 0;
     for (int i = tid; i < nr; i += 128) {
-      const int2 r = (i < MAXR) ? srng[i] : make_int2(grng[2 * i], grng[2 * i + 1]);
+      const int2 r = make_int2(grng[2 * i], grng[2 * i + 1]);
       below += (r.x + r.y <= A.seg_lo);
       before_end += (r.x < A.seg_hi);
       keys += max(min(r.x + r.y, A.seg_hi) - max(r.x, A.seg_lo), 0);
@@ -308,10 +312,13 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     j0 = sred[0][0] + sred[1][0];
     nseg = sred[0][1] + sred[1][1] - j0;
     w.nkeys = sred[0][2] + sred[1][2];
+    for (int i = tid; i < min(nseg, MAXR); i += 128)
+      srng[i] = make_int2(grng[2 * (j0 + i)], grng[2 * (j0 + i) + 1]);
+    __syncthreads();
   }
   auto range_at = [&](int j) -> int2 {  // clipped range j of the segment's run
     const int jj = j0 + j;
-    const int2 r = (jj < MAXR) ? srng[jj] : make_int2(grng[2 * jj], grng[2 * jj + 1]);
+    const int2 r = (j < MAXR) ? srng[j] : make_int2(grng[2 * jj], grng[2 * jj + 1]);
     const int lo = max(r.x, A.seg_lo), hi = min(r.x + r.y, A.seg_hi);
     return make_int2(lo, hi - lo);
   };
@@ -347,12 +354,13 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       spos[tt % 3][tid] = pos;
     }
   };
-  // LDS byte address of tiles[0] (uniform); K buffer b is at +b*KT*D*2,
-  // V buffer b at +(2+b)*KT*D*2
+  // LDS byte address of tiles[0] (uniform); the K buffer is there, V
+  // buffer b at +(1+b)*KT*D*2
   const uint32_t lds_tiles = __builtin_amdgcn_readfirstlane(
       (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)&tiles[0][0]);
   const uint32_t row_bytes = (uint32_t)(ksn * 2);
-  auto issue_loads = [&](int tt, int buf) {  // tile tt -> K/V buffer `buf`
+  // the copies of tile tt of one tensor into the buffer at dst
+  auto issue = [&](int tt, const uint16_t* src, uint32_t dst) {
     // all positions first (one LDS wait), then the copies
     uint32_t voff[LPT];
 #pragma unroll
@@ -364,12 +372,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       voff[u] = (uint32_t)spos[tt % 3][key] * row_bytes + (uint32_t)(c8 * 16);
     }
 #pragma unroll
-    for (int u = 0; u < LPT; ++u) {
-      const uint32_t dst = lds_tiles + (uint32_t)((wv * LPT + u) * 1024);
-      g2lds16s(Kp, voff[u], dst + (uint32_t)(buf * KT * D * 2));
-      g2lds16s(Vp, voff[u], dst + (uint32_t)((2 + buf) * KT * D * 2));
-    }
+    for (int u = 0; u < LPT; ++u) g2lds16s(src, voff[u], dst + (uint32_t)((wv * LPT + u) * 1024));
   };
+  const uint32_t kdst = lds_tiles;
+  auto vdst = [&](int b) { return lds_tiles + (uint32_t)((1 + b) * KT * D * 2); };
 
   const float sl2 = 1.4426950408889634f / sqrtf((float)D);
   float m_run = -INFINITY, l_run = 0.f;
@@ -404,54 +410,40 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   __builtin_amdgcn_s_waitcnt(0x3f70);
 
   const int ntile = (w.nkeys + KT - 1) / KT;
-  // One step: compute tile t from (kt, vt) while tile t + 1 loads into (kn, vn).
-  auto step = [&](int t, int cb) {  // compute tile t from buffer cb; tile t+1 loads into 1-cb
-    const uint16_t* kt = tiles[cb];
-    const uint16_t* vt = tiles[2 + cb];
-    // Plain s_barrier (no fence): a fence would also wait for the tile t+1
-    // loads just issued.  Ordering is explicit instead: each wave waits for
-    // its own loads of tile t and for its LDS writes before the barrier.
-    // Positions first: the range walk may read global memory, and the wait
-    // the compiler puts before its use also covers every load issued
-    // earlier; here those are only tile t's, which are awaited next anyway.
+  // One step computes tile t (K in the K buffer, V in V buffer vb).  Barrier
+  // A: every wave's copies of tile t have landed and every wave is done with
+  // tile t-1, so V(t+1) is copied into the other V buffer; the scores read
+  // the K buffer; barrier B: every wave is done with K(t), so K(t+1) is
+  // copied into it while the softmax and PV of tile t run.  Plain s_barrier
+  // (no fence): ordering is explicit, each wave waits for its own copies and
+  // LDS accesses before a barrier.
+  auto step = [&](int t, int vb) {
+    const uint16_t* kt = tiles[0];
+    const uint16_t* vt = tiles[1 + vb];
+    // positions first: the range walk may read global memory, and the wait
+    // the compiler puts before its use also covers the copies issued
+    // earlier, which are awaited next anyway
     if (t + 2 < ntile) fill_pos(t + 2);
-    if (t + 1 < ntile) issue_loads(t + 1, 1 - cb);
-    if (t + 1 < ntile)
-      __builtin_amdgcn_s_waitcnt(0x3f70 | (2 * LPT));  // vmcnt(2*LPT): tile t has landed
-    else
-      __builtin_amdgcn_s_waitcnt(0x3f70);              // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0x3f70);  // vmcnt(0): K(t) and V(t) have landed
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_barrier();
+    if (t + 1 < ntile) issue(t + 1, Vp, vdst(1 - vb));
+    f32x16 S;
     if (wave_active) {
-      // All LDS operand reads of the tile are issued first, so that their
-      // latency overlaps: the K fragments feed the score MFMAs, the V^T
-      // fragments (transposing reads) arrive while the softmax runs.
-      bf16x8 kf[NKS];
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const int c8 = (2 * ks + h) ^ kv_swz<D>(n);
-        kf[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
-      }
-      const int grp = lane >> 4, gl = lane & 15;
-      bf16x8 vf[NDB][2];
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const int dv = db * 32 + 16 * (grp & 1) + 4 * (gl & 3);
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int key0 = 16 * c + 4 * h + (gl >> 2);
-          const int key1 = key0 + 8;
-          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz<D>(key0))) * 8 + (dv & 7));
-          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz<D>(key1))) * 8 + (dv & 7));
-          vf[db][c] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      f32x16 S;
 #pragma unroll
       for (int i = 0; i < 16; ++i) S[i] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qreg[ks], S, 0, 0, 0);
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int c8 = (2 * ks + h) ^ kv_swz<D>(n);
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, *(const uint4*)(kt + (n * CH + c8) * 8));
+        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qreg[ks], S, 0, 0, 0);
+      }
+    }
+    // every wave's K reads are done before K(t+1) overwrites the buffer
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+    if (t + 1 < ntile) issue(t + 1, Kp, kdst);
+    if (wave_active) {
       // register i holds key (i/4)*8 + h*4 + i%4 of the tile
       float mt = -INFINITY;
       if ((t + 1) * KT > w.nkeys) {
@@ -493,6 +485,22 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const bf16x2 pp = {P[c][e], P[c][e + 1]};
           l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run, false);
         }
+      // V^T fragments (transposing reads), after the scores are consumed so
+      // that the two never hold registers together
+      const int grp = lane >> 4, gl = lane & 15;
+      bf16x8 vf[NDB][2];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int dv = db * 32 + 16 * (grp & 1) + 4 * (gl & 3);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int key0 = 16 * c + 4 * h + (gl >> 2);
+          const int key1 = key0 + 8;
+          const v4i16 lo = lds_read_tr16(vt + (key0 * CH + ((dv >> 3) ^ kv_swz<D>(key0))) * 8 + (dv & 7));
+          const v4i16 hi = lds_read_tr16(vt + (key1 * CH + ((dv >> 3) ^ kv_swz<D>(key1))) * 8 + (dv & 7));
+          vf[db][c] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      }
       // O^T += V^T P^T over the two 16-key chunks
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
@@ -500,18 +508,20 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int c = 0; c < 2; ++c)
           O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db][c], P[c], O[db], 0, 0, 0);
     }
-    // every wave is done with this buffer before tile t + 2 is loaded into it
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_s_barrier();
   };
   if (ntile > 0) fill_pos(0);
   if (ntile > 1) fill_pos(1);
   __syncthreads();
-  if (ntile > 0) issue_loads(0, 0);
+  if (ntile > 0) {
+    issue(0, Kp, kdst);
+    issue(0, Vp, vdst(0));
+  }
   for (int t = 0; t < ntile; t += 2) {
     step(t, 0);
     if (t + 1 < ntile) step(t + 1, 1);
   }
+  // every copy has landed before the block can end
+  __builtin_amdgcn_s_waitcnt(0x3f70);
   if (!qvalid) return;
   const float l_tot = pair_sum(l_run);
   if (MODE == MODE_PROBE) {
