@@ -93,7 +93,6 @@ void describe(const Geom& g, Work* w, Layout& L) {
   add(&w->km_clo, (size_t)g.cpad * g.rpad * 2);
   add(&w->km_cu, (size_t)g.cpad * 4);
   add(&w->km_cn3, (size_t)g.cpad * 2 * 4);
-  add(&w->km_fb, NV * 4);
   add(&w->km_fbcnt, (size_t)2 * g.T * 4);
   add(&w->kbar, (size_t)g.CK * d * 4);
   add(&w->qbar, (size_t)g.CQ * d * 4);

@@ -409,8 +409,7 @@ struct KmArgs {
   uint16_t* clo;
   float* cu;          // [BH][CP]
   uint32_t* cn3;      // [BH][CP][2]: the norm's three bf16 parts (p0 | p1 << 16, p2)
-  int32_t* fb;        // [BH][n]
-  int32_t* fbcnt;     // [BH][2][T]
+  int32_t* fbcnt;     // [BH][2][T]: points left to the exact scan per assignment
   int RP, CP;         // rank padded to 16, groups padded to 32 (strides of the above)
 };
 
@@ -455,8 +454,9 @@ __global__ void k_km_init(KmArgs a) {
 // every estimated score is within
 // Delta = 1.61e-4 |x| c_max + 6.0e-7 u_max of the exact one (Delta below
 // carries another factor 2).  When the best estimate beats the runner-up by
-// more than 2 Delta, its centroid is the exact argmin; every other point is
-// rescored exactly by k_km_fallback.
+// more than 2 Delta, its centroid is the exact argmin; when only the third
+// is farther, the two candidates are rescored exactly; every other point is
+// rescored against all centroids by its block at the end of the kernel.
 
 __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
@@ -572,8 +572,14 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int NPS = 2;                // sets of 32 points per wave
   __shared__ __attribute__((aligned(1024))) unsigned char tiles[2][TILE];
   __shared__ float sred[4];
+  __shared__ int sfb[256];  // the block's points left to the exact scan
+  __shared__ int nfb;
+  __shared__ __attribute__((aligned(16))) float xs[RP];
+  __shared__ float rsb[4];
+  __shared__ int rsi[4];
   const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (km_skip_assign(a, bh, it)) return;
+  if (tid == 0) nfb = 0;  // ordered by the tile loop's barriers
   const int n = lane & 31, h = lane >> 5;
   const int jbase = blockIdx.x * (128 * NPS) + wv * (32 * NPS);
   bf16x8 bhi[NPS][KS], blo[NPS][KS];
@@ -707,66 +713,56 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   }
   __syncthreads();
   umax = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
   // lane (n, h) decides point n of set h
   const int j = jbase + h * 32 + n;
-  if (j >= a.n) return;
-  const float T1 = h ? t1[1] : t1[0], T2 = h ? t2[1] : t2[0], T3 = h ? t3[1] : t3[0];
-  // the packed indices are below C whenever a real centroid has a finite
-  // score; non-finite coordinates (flagged by k_project) could leave a
-  // padding index or NaN bits, so the indices are clamped into range
-  const int i1 = min((int)(__float_as_uint(T1) & ~keep), a.C - 1);
-  const int i2 = min((int)(__float_as_uint(T2) & ~keep), a.C - 1);
-  const float xn = a.xn[(size_t)bh * a.n + j];
-  const float delta = 3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax;
-  const float ek = ldexpf(1.f, ib - 22);
-  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-  int label;
-  if (T2 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T2))) {
-    label = i1;  // unique candidate: the exact argmin
-  } else if (T3 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T3))) {
-    // exactly two candidates: rescore both with the defining float score
-    const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
-    const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
-    const float* c2 = a.cent + ((size_t)bh * a.C + i2) * a.R;
-    float d1 = 0.f, d2 = 0.f;
-    for (int k = 0; k < a.R; ++k) {
-      const float xk = xp[k];
-      d1 = fmaf(xk, c1[k], d1);
-      d2 = fmaf(xk, c2[k], d2);
+  if (j < a.n) {
+    const float T1 = h ? t1[1] : t1[0], T2 = h ? t2[1] : t2[0], T3 = h ? t3[1] : t3[0];
+    // the packed indices are below C whenever a real centroid has a finite
+    // score; non-finite coordinates (flagged by k_project) could leave a
+    // padding index or NaN bits, so the indices are clamped into range
+    const int i1 = min((int)(__float_as_uint(T1) & ~keep), a.C - 1);
+    const int i2 = min((int)(__float_as_uint(T2) & ~keep), a.C - 1);
+    const float xn = a.xn[(size_t)bh * a.n + j];
+    const float delta = 3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax;
+    const float ek = ldexpf(1.f, ib - 22);
+    int label = -1;
+    if (T2 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T2))) {
+      label = i1;  // unique candidate: the exact argmin
+    } else if (T3 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T3))) {
+      // exactly two candidates: rescore both with the defining float score
+      const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
+      const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
+      const float* c2 = a.cent + ((size_t)bh * a.C + i2) * a.R;
+      float d1 = 0.f, d2 = 0.f;
+      for (int k = 0; k < a.R; ++k) {
+        const float xk = xp[k];
+        d1 = fmaf(xk, c1[k], d1);
+        d2 = fmaf(xk, c2[k], d2);
+      }
+      const float s1 = fmaf(-2.f, d1, cu[i1]), s2 = fmaf(-2.f, d2, cu[i2]);
+      label = (s2 < s1 || (s2 == s1 && i2 < i1)) ? i2 : i1;
+    } else {
+      // more than two candidates: the block's exact scan below
+      sfb[atomicAdd(&nfb, 1)] = j;
+      atomicAdd(a.fbcnt + (size_t)bh * 2 * a.T + a.sel * a.T + it, 1);
     }
-    const float s1 = fmaf(-2.f, d1, cu[i1]), s2 = fmaf(-2.f, d2, cu[i2]);
-    label = (s2 < s1 || (s2 == s1 && i2 < i1)) ? i2 : i1;
-  } else {
-    int32_t* cnt = a.fbcnt + (size_t)bh * 2 * a.T + a.sel * a.T + it;
-    const int slot = atomicAdd(cnt, 1);
-    a.fb[(size_t)bh * a.n + slot] = j;
-    return;
+    if (label >= 0) {
+      const int old = lab[j];
+      lab[j] = label;
+      if (it > 0 && old != label) atomicAdd(&km_changed(a, bh)[it], 1);
+    }
   }
-  const int old = lab[j];
-  lab[j] = label;
-  if (it > 0 && old != label) atomicAdd(&km_changed(a, bh)[it], 1);
-}
-
-// Exact scan (the defining float score) for the points the screen could not
-// decide; there are few of them, so each gets a block: the point sits in
-// LDS, every thread scores a strided subset of the centroids with the float
-// chain, and the block keeps the smallest score, lowest index among equal
-// scores.
-template <int RP>
-__global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
-  __shared__ __attribute__((aligned(16))) float xs[RP];
-  __shared__ float rs[4];
-  __shared__ int ri[4];
-  const int bh = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  if (km_skip_assign(a, bh, it)) return;
-  const int cnt = a.fbcnt[(size_t)bh * 2 * a.T + a.sel * a.T + it];
-  const float* cu = a.cu + (size_t)bh * a.CP;
-  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  __syncthreads();
+  // Exact scan (the defining float score) of the block's undecided points:
+  // the point sits in LDS, every thread scores a strided subset of the
+  // centroids with the float chain, and the block keeps the smallest score,
+  // lowest index among equal scores.
+  const int nundecided = nfb;
   const int R = a.R;
-  for (int e = blockIdx.x; e < cnt; e += gridDim.x) {
-    const int j = a.fb[(size_t)bh * a.n + e];
-    __syncthreads();
-    if (tid < RP) xs[tid] = tid < R ? a.pts[((size_t)bh * a.n + j) * R + tid] : 0.f;
+  for (int e = 0; e < nundecided; ++e) {
+    const int jj = sfb[e];
+    if (tid < RP) xs[tid] = tid < R ? a.pts[((size_t)bh * a.n + jj) * R + tid] : 0.f;
     __syncthreads();
     float best = INFINITY;
     int bi = 0x7fffffff;
@@ -800,21 +796,22 @@ __global__ __launch_bounds__(256) void k_km_fallback(KmArgs a, int it) {
       }
     }
     if (lane == 0) {
-      rs[wv] = best;
-      ri[wv] = bi;
+      rsb[wv] = best;
+      rsi[wv] = bi;
     }
     __syncthreads();
     if (tid == 0) {
       for (int w2 = 1; w2 < 4; ++w2)
-        if (rs[w2] < best || (rs[w2] == best && ri[w2] < bi)) {
-          best = rs[w2];
-          bi = ri[w2];
+        if (rsb[w2] < best || (rsb[w2] == best && rsi[w2] < bi)) {
+          best = rsb[w2];
+          bi = rsi[w2];
         }
       if (bi >= a.C) bi = 0;  // no finite score (non-finite input, flagged): keep labels in range
-      const int old = lab[j];
-      lab[j] = bi;
+      const int old = lab[jj];
+      lab[jj] = bi;
       if (it > 0 && old != bi) atomicAdd(&km_changed(a, bh)[it], 1);
     }
+    __syncthreads();  // xs and the reduction slots are reused by the next point
   }
 }
 
@@ -2127,7 +2124,6 @@ static void run_sort(const KmArgs& a, int BH, int it, hipStream_t s) {
                    (size_t)kScatterWaves * (sort_scatter_cstride(a.C) + 64) * sizeof(int), s>>>(a, it);
 }
 
-template <int MAXR>
 static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
   const int BH = g.BH;
   // the first assignment's operands; later ones come from k_km_update
@@ -2149,8 +2145,6 @@ static void assign_step(const Geom& g, const KmArgs& a, int it, hipStream_t s) {
     k_km_assign_mfma<112><<<grid, 256, 0, s>>>(a, it);
   else
     k_km_assign_mfma<128><<<grid, 256, 0, s>>>(a, it);
-  // few points per head need the exact scan: a handful of blocks per head
-  k_km_fallback<MAXR><<<dim3(16, BH), 256, 0, s>>>(a, it);
 }
 
 static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm) {
@@ -2162,12 +2156,7 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm
   if (!warm) k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
   const int iters = warm ? g.T_warm : g.T;
   for (int it = 0; it < iters; ++it) {
-    if (a.R <= 32)
-      assign_step<32>(g, a, it, s);
-    else if (a.R <= 64)
-      assign_step<64>(g, a, it, s);
-    else
-      assign_step<128>(g, a, it, s);
+    assign_step(g, a, it, s);
     run_sort(a, BH, it, s);
     k_km_update<<<dim3((a.C + 3) / 4, BH), 256, 0, s>>>(a, it);
   }
@@ -2223,7 +2212,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   project<D>(g, w, k, w.fk, g.rk, 0, 0, 0.f, w.phik, s);
   KmArgs ak{w.phik, w.centk, w.labk, w.permk, w.offk, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rk, g.CK, g.CKt + 1, g.nsort_blk, g.cmax, 0, g.T,
-            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fb, w.km_fbcnt, 0, 0};
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fbcnt, 0, 0};
   run_kmeans(g, ak, s, warm);
   // Query-response coordinates from the K/V groups (App. B.2)
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
@@ -2239,7 +2228,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   }
   KmArgs aq{w.phiq, w.centq, w.labq, w.permq, w.offq, w.blkhist, w.kmstate, g.NV, g.ntext, g.N,
             g.rq, g.CQ, g.CQt + 1, g.nsort_blk, g.cmax, 1, g.T,
-            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fb, w.km_fbcnt, 0, 0};
+            w.km_xhi, w.km_xlo, w.km_xn, w.km_chi, w.km_clo, w.km_cu, w.km_cn3, w.km_fbcnt, 0, 0};
   run_kmeans(g, aq, s, warm);
   k_group_mean<<<dim3((g.CQ + 3) / 4, BH), 256, 0, s>>>(q, g, w.permq, w.offq, g.CQ, g.CQt + 1,
                                                          w.qbar, 1);

@@ -89,7 +89,6 @@ struct Work {
   uint16_t* km_clo; // [BH][cpad][rpad]
   float* km_cu;     // [BH][cpad] exact squared centroid norms (+inf for padding)
   uint32_t* km_cn3; // [BH][cpad][2] the norms as three bf16 parts (operand of the MFMA norm step)
-  int32_t* km_fb;   // [BH][NV] points whose assignment needs the exact scan
   int32_t* km_fbcnt;// [BH][2][T] number of such points per assignment
   float* kbar;      // [BH][CK][d]
   float* qbar;      // [BH][CQ][d]
