@@ -231,10 +231,12 @@ __global__ __launch_bounds__(1024) void k_fit_solve(Geom g, Work w) {
       __syncthreads();
       jacobi_eig_lds<D, T, 1024>(Am, Vm, rot, &flag, sizeof(T) == 8 ? T(1e-12) : T(1e-4));
       if (tid < D) {
-        const T li = Am[tid * LD + tid];
+        // a NaN diagonal (non-finite input) ranks as -inf, so the ranks stay
+        // a permutation and every order[] entry is written
+        const T li = eig_rank_key(Am[tid * LD + tid]);
         int rank = 0;
         for (int j = 0; j < D; ++j) {
-          const T lj = Am[j * LD + j];
+          const T lj = eig_rank_key(Am[j * LD + j]);
           rank += (lj > li) || (lj == li && j < tid);
         }
         order[rank] = tid;

@@ -26,6 +26,13 @@ struct alignas(16) JacobiRot {
   int p, q;
 };
 
+// Eigenvalue sort key: NaN (from non-finite inputs) as -inf, so that ranks
+// by (key descending, index ascending) are a permutation.
+template <typename T>
+__device__ __forceinline__ T eig_rank_key(T v) {
+  return v == v ? v : -(T)INFINITY;
+}
+
 template <int D>
 constexpr int jacobi_vt_ld() {
   return D + 4;

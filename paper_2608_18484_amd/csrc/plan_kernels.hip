@@ -89,10 +89,12 @@ __device__ void eig_order(const T* A, int* order) {
   constexpr int LD = D + 1;
   const int i = threadIdx.x;
   if (i < D) {
-    const T li = A[i * LD + i];
+    // a NaN diagonal (non-finite input) ranks as -inf, so the ranks stay a
+    // permutation and every order[] entry is written
+    const T li = eig_rank_key(A[i * LD + i]);
     int rank = 0;
     for (int j = 0; j < D; ++j) {
-      const T lj = A[j * LD + j];
+      const T lj = eig_rank_key(A[j * LD + j]);
       rank += (lj > li) || (lj == li && j < i);
     }
     order[rank] = i;

@@ -655,3 +655,44 @@ def test_imported_plan_with_many_ranges(orc):
     assert rel_l2(ex["o_sparse"], osp) < 1e-2
     err = rel_l2(out.float().cpu().numpy()[0, 0], ref)
     assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("where", ["nan_sampled_query", "inf_key"])
+def test_nonfinite_inputs_flagged_indices_in_range(where):
+    # A non-finite input reaches the partition features (a NaN in a sampled
+    # query spreads through the key metric of App. B.1 to every coordinate;
+    # an Inf key to its own coordinates and group): the projection raises
+    # the flag, the call completes, every label, permutation, range and probe
+    # index stays in range, and the same operator afterwards plans clean
+    # inputs exactly as a fresh one does.
+    from paper_2608_18484_amd import sparsepr as S
+    import torch
+    wl = medium(heads=1)
+    q, k, v = W.make_inputs(wl)[:3]
+    qb, kb = q.copy(), k.copy()
+    if where == "nan_sampled_query":
+        qb[0, 0, 0, 3] = np.nan
+    else:
+        kb[0, 0, 37, 5] = np.inf
+    r = _run(wl, inputs=(qb, kb, v))
+    op, n = r["op"], wl.n
+    st = op.stats()
+    assert st["status_flags"] & S.FLAG_NONFINITE_INPUT
+    ex = op.export(0)
+    for lab, c in ((ex["labels_q"], op.cq_t), (ex["labels_kv"], op.ck_t)):
+        assert lab.min() >= 0 and lab.max() < c
+    for perm in (ex["perm_q"], ex["perm_kv"]):
+        assert np.array_equal(np.sort(perm), np.arange(n))
+    for off, c in ((ex["off_q"], op.cq_t), (ex["off_kv"], op.ck_t)):
+        assert off[0] == 0 and off[c] == n and np.all(np.diff(off[:c + 1]) >= 0)
+    pr = ex["probes"][:ex["n_probes"]]
+    assert len(pr) > 0 and pr.min() >= 0 and pr.max() < n
+    # clean inputs through the same operator, against a fresh operator
+    tq, tk, tv = to_device(q, k, v, wl.dtype)
+    out = torch.empty_like(tq)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    torch.cuda.synchronize()
+    assert op.stats()["status_flags"] & S.FLAG_NONFINITE_INPUT == 0
+    fresh = _run(wl, inputs=(q, k, v))
+    assert np.array_equal(out.float().cpu().numpy(), fresh["out"])
