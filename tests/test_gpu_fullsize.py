@@ -4,9 +4,11 @@ configuration bench.py times (every head of the layer in one plan + attend).
 The oracle cannot replay a whole full-size call in test time, so for two
 heads of each workload it checks, on the GPU's own float inputs to each
 decision: the K/V and query k-means labels and final centroids (bit-exact),
-the route set (bit-exact), the probe set (bit-exact); then, on sampled rows, the hard-drop output, the exact
-probe rows and the corrected output (the oracle's fit on its own sparse and
-dense probe rows, applied to the sampled rows).
+the route set (bit-exact), the probe set (bit-exact); then, on sampled rows,
+the hard-drop output, the exact probe rows and the corrected output (the
+oracle's fit on its own sparse and dense probe rows, applied to the sampled
+rows).  The warm-started and grouped-query configurations of the long-video
+workload are checked the same way.
 """
 import numpy as np
 import pytest
@@ -21,6 +23,57 @@ torch = pytest.importorskip("torch")
 
 def _heads(wl):
     return [(0, 0), (wl.batch - 1, wl.heads - 1)]
+
+
+def _check_head(orc, tag, p, ex, qhs, kh, vh, outs, iters, init=None):
+    """One K/V head of a full-size plan against the oracle, on the GPU's own
+    float inputs to each decision.  qhs / outs: the query heads that share
+    the plan (one, or g under grouped-query attention) and their outputs."""
+    nt = p.n_dense_prefix
+    ck, cq = p.n_kv_groups, p.n_q_groups
+    kw = oracle_kwargs(p)
+    n = kh.shape[0]
+    # K/V and query k-means on the GPU's coordinates: bit-exact labels and
+    # final centroids (the query centroids are the probe-selection means)
+    lab_k, cent_k, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, iters,
+                                         init=None if init is None else init["cent_k"])
+    assert np.array_equal(ex["labels_kv"][nt:], lab_k)
+    assert np.array_equal(ex["cent_k"], cent_k)
+    lab_q, cent_q, _, _ = orc.kmeans(ex["phi_q"], cq, iters,
+                                     init=None if init is None else init["cent_q"])
+    assert np.array_equal(ex["labels_q"][nt:], lab_q)
+    assert np.array_equal(ex["cent_q"], cent_q)
+    # routes given the GPU's priorities, bit-exact
+    cnt_q = np.bincount(ex["labels_q"][nt:], minlength=cq)
+    nv = n - nt
+    m = min(p.n_probes, nv)
+    budget = int(np.floor(float(np.float32(p.target_exec_density)) * nv * nv)) - m * n
+    z, _ = orc.route_select(ex["route_prio"], cnt_q, cnt_k, budget)
+    assert np.array_equal(ex["routes"][:cq, :ck], z)
+    # probes on the GPU's query coordinates and centroids, bit-exact
+    probes, wts = orc.probe_select(ex["phi_q"], ex["labels_q"][nt:], ex["cent_q"], p.n_probes)
+    assert np.array_equal(ex["probes"], probes + nt)
+    rows = W.strided_rows(n, 384)
+    pr = ex["probes"].astype(np.int64)
+    for j, (qh, outh) in enumerate(zip(qhs, outs)):
+        # sampled rows: hard-drop output and exact probe rows
+        osp = orc.sparse_rows(qh, kh, vh, ex["labels_q"], ex["labels_kv"], ex["routes"], rows)
+        if j == 0:
+            assert rel_l2(ex["o_sparse"][rows], osp) < 1e-2
+        od = orc.dense_rows(qh, kh, vh, pr)
+        if j == 0:
+            assert rel_l2(ex["o_dense_probes"], od) < 1e-2
+        # corrected output on the sampled rows (eq. final_reconstructed_output)
+        xp = orc.sparse_rows(qh, kh, vh, ex["labels_q"], ex["labels_kv"], ex["routes"], pr)
+        ft = orc.fit(xp, od, ex["probe_weights"].astype(np.float64), kw["r"], kw["lam"],
+                     eps=float(np.float32(p.eps_x)))
+        ref = orc.correct_rows(osp, ft)
+        ref[rows < nt] = osp[rows < nt]
+        isprobe = np.isin(rows, pr)
+        ref[isprobe] = orc.dense_rows(qh, kh, vh, rows[isprobe])
+        err = rel_l2(outh[rows], ref)
+        print(f"[{tag}] query head {j}: sampled-row rel-L2 vs oracle {err:.3e}", flush=True)
+        assert err < 2e-2
 
 
 @pytest.mark.parametrize("name", ["video_dit", "long_video", "text_video", "world_model"])
@@ -41,48 +94,80 @@ def test_full_size_sampled_parity(orc, name):
     # realised density never exceeds the target (Sec. 4.3 budget incl. probes)
     assert st["rho_exec"] <= float(np.float32(p.target_exec_density)) + 1e-6 or wl.n_text
     outn = out.float().cpu().numpy()
-    kw = oracle_kwargs(p)
-    nt = wl.n_text
-    ck, cq = p.n_kv_groups, p.n_q_groups
     for b, h in _heads(wl):
-        bh = b * wl.heads + h
         print(f"[{name}] head ({b},{h}): oracle checks", flush=True)
-        ex = op.export(bh)
-        qh, kh, vh = q[b, h], k[b, h], v[b, h]
-        n = qh.shape[0]
-        # K/V and query k-means on the GPU's coordinates: bit-exact labels and
-        # final centroids (the query centroids are the probe-selection means)
-        lab_k, cent_k, cnt_k, _ = orc.kmeans(ex["phi_k"], ck, p.kmeans_iters)
-        assert np.array_equal(ex["labels_kv"][nt:], lab_k)
-        assert np.array_equal(ex["cent_k"], cent_k)
-        lab_q, cent_q, _, _ = orc.kmeans(ex["phi_q"], cq, p.kmeans_iters)
-        assert np.array_equal(ex["labels_q"][nt:], lab_q)
-        assert np.array_equal(ex["cent_q"], cent_q)
-        # routes given the GPU's priorities, bit-exact
-        _, cnt_q = orc.group_mean(qh[nt:], ex["labels_q"][nt:], cq)
-        nv = n - nt
-        m = min(p.n_probes, nv)
-        budget = int(np.floor(float(np.float32(p.target_exec_density)) * nv * nv)) - m * n
-        z, _ = orc.route_select(ex["route_prio"], cnt_q, cnt_k, budget)
-        assert np.array_equal(ex["routes"][:cq, :ck], z)
-        # probes on the GPU's query coordinates and centroids, bit-exact
-        probes, wts = orc.probe_select(ex["phi_q"], ex["labels_q"][nt:], ex["cent_q"], p.n_probes)
-        assert np.array_equal(ex["probes"], probes + nt)
-        # sampled rows: hard-drop output and exact probe rows
-        rows = W.strided_rows(n, 384)
-        osp = orc.sparse_rows(qh, kh, vh, ex["labels_q"], ex["labels_kv"], ex["routes"], rows)
-        assert rel_l2(ex["o_sparse"][rows], osp) < 1e-2
-        pr = ex["probes"].astype(np.int64)
-        od = orc.dense_rows(qh, kh, vh, pr)
-        assert rel_l2(ex["o_dense_probes"], od) < 1e-2
-        # corrected output on the sampled rows (eq. final_reconstructed_output)
-        xp = orc.sparse_rows(qh, kh, vh, ex["labels_q"], ex["labels_kv"], ex["routes"], pr)
-        ft = orc.fit(xp, od, ex["probe_weights"].astype(np.float64), kw["r"], kw["lam"],
-                     eps=float(np.float32(p.eps_x)))
-        ref = orc.correct_rows(osp, ft)
-        ref[rows < nt] = osp[rows < nt]
-        isprobe = np.isin(rows, pr)
-        ref[isprobe] = orc.dense_rows(qh, kh, vh, rows[isprobe])
-        err = rel_l2(outn[b, h][rows], ref)
-        print(f"[{name}] head ({b},{h}): sampled-row rel-L2 vs oracle {err:.3e}", flush=True)
-        assert err < 2e-2
+        _check_head(orc, f"{name} ({b},{h})", p, op.export(b * wl.heads + h), [q[b, h]], k[b, h],
+                    v[b, h], [outn[b, h]], p.kmeans_iters)
+
+
+def test_full_size_warm_start(orc):
+    # Warm start (App. C.1) in the configuration bench.py --warm-start times:
+    # a cold call, then a call on inputs nudged by 5% noise (as between
+    # denoising steps) whose k-means start from the first call's centroids
+    # and run two assignments.
+    from paper_2608_18484_amd import sparsepr as S
+    wl = W.CONFIGS["long_video"]
+    print(f"\n[warm] generating {wl.batch}x{wl.heads} heads, N={wl.n}", flush=True)
+    q, k, v, _ = W.make_inputs(wl, workers=16)
+    p = params_for(wl, warm_start=1, warm_iters=2)
+    tq, tk, tv = to_device(q, k, v, wl.dtype)
+    op = S.SparsePR(S.shape_of(tq), p)
+    out = torch.empty_like(tq)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    heads = _heads(wl)
+    first = {bh: op.export(bh, fields=["cent_k", "cent_q"])
+             for bh in (b * wl.heads + h for b, h in heads)}
+    rng = np.random.default_rng(11)
+    q2, k2, v2 = (W.bf16_round(x + 0.05 * np.std(x) * rng.standard_normal(x.shape, np.float32))
+                  for x in (q, k, v))
+    del tq, tk, tv
+    tq, tk, tv = to_device(q2, k2, v2, wl.dtype)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    torch.cuda.synchronize()
+    st = op.stats()
+    assert st["status_flags"] == 0
+    assert st["kmeans_iters_kv"] <= 2 and st["kmeans_iters_q"] <= 2
+    outn = out.float().cpu().numpy()
+    for b, h in heads:
+        bh = b * wl.heads + h
+        print(f"[warm] head ({b},{h}): oracle checks", flush=True)
+        _check_head(orc, f"warm ({b},{h})", p, op.export(bh), [q2[b, h]], k2[b, h], v2[b, h],
+                    [outn[b, h]], 2, init=first[bh])
+
+
+def test_full_size_grouped_query(orc):
+    # Grouped-query attention in the configuration bench.py --kv-heads 8
+    # times: 24 query heads on 8 K/V heads (K/V are every third generated
+    # head); one plan per K/V head pools its three query heads.
+    from paper_2608_18484_amd import sparsepr as S
+    wl = W.CONFIGS["long_video"]
+    g = 3
+    print(f"\n[gqa] generating {wl.batch}x{wl.heads} heads, N={wl.n}", flush=True)
+    q, k, v, _ = W.make_inputs(wl, workers=16)
+    k, v = np.ascontiguousarray(k[:, ::g]), np.ascontiguousarray(v[:, ::g])
+    tq, tk, tv = to_device(q, k, v, wl.dtype)
+    p = params_for(wl)
+    op = S.SparsePR(S.shape_of(tq, kv=tk), p)
+    out = torch.empty_like(tq)
+    op.plan(tq, tk)
+    op.attend(tq, tk, tv, out)
+    torch.cuda.synchronize()
+    st = op.stats()
+    assert st["status_flags"] == 0
+    outn = out.float().cpu().numpy()
+    hkv = wl.heads // g
+    for hk in (0, hkv - 1):
+        print(f"[gqa] K/V head {hk}: oracle checks", flush=True)
+        ex = op.export(hk * g)
+        qg = q[0, hk * g:(hk + 1) * g]
+        # the pooled key metric over the group's sampled query rows (App. B.1)
+        assert rel_l2(ex["m_k"], orc.key_metric_pooled(qg, p.n_sampled_queries)) < 1e-5
+        for j in range(1, g):
+            exj = op.export(hk * g + j, fields=["labels_q", "routes", "probes"])
+            assert np.array_equal(exj["labels_q"], ex["labels_q"])
+            assert np.array_equal(exj["routes"], ex["routes"])
+            assert np.array_equal(exj["probes"], ex["probes"])
+        _check_head(orc, f"gqa {hk}", p, ex, list(qg), k[0, hk], v[0, hk],
+                    [outn[0, hk * g + j] for j in range(g)], p.kmeans_iters)
