@@ -413,6 +413,7 @@ struct KmArgs {
   uint32_t* cn3;      // [BH][CP][2]: the norm's three bf16 parts (p0 | p1 << 16, p2)
   int32_t* fbcnt;     // [BH][2][T]: points left to the exact scan per assignment
   int RP, CP;         // rank padded to 16, groups padded to 32 (strides of the above)
+  int warm;           // the first assignment starts from an earlier call's centroids
 };
 
 __device__ __forceinline__ int32_t* km_changed(const KmArgs& a, int bh) {
@@ -560,10 +561,11 @@ __device__ __forceinline__ void km_g2lds4(const void* src, uint32_t lds) {
 // ahead, one barrier per tile.  Lane (n, h) ends with the three best
 // estimates of point n of each set over half of the centroids; the halves
 // are merged with one exchange, and lane h then decides set h's point.  The
-// second launch bound caps the kernel at 256 registers, so the accumulators
-// stay in VGPRs that the VALU reads directly.
+// second launch bound (three blocks per CU up to rank 64, two above) caps
+// the registers at 168 / 256, so the accumulators stay in VGPRs that the
+// VALU reads directly.
 template <int RP>
-__global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
+__global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int KS = RP / 16;
   constexpr int LD = RP + 8;            // padded LDS row (bf16)
   constexpr int ARR = 32 * LD * 2;      // bytes of one array (hi or lo) of a tile
@@ -573,7 +575,6 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int TILE = 2 * ARR + 256;   // + the 32 norms' parts
   constexpr int NPS = 2;                // sets of 32 points per wave
   __shared__ __attribute__((aligned(1024))) unsigned char tiles[2][TILE];
-  __shared__ float sred[4];
   __shared__ int sfb[256];  // the block's points left to the exact scan
   __shared__ int nfb;
   __shared__ __attribute__((aligned(16))) float xs[RP];
@@ -584,10 +585,16 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   if (tid == 0) nfb = 0;  // ordered by the tile loop's barriers
   const int n = lane & 31, h = lane >> 5;
   const int jbase = blockIdx.x * (128 * NPS) + wv * (32 * NPS);
+  // Points are taken in the order of the previous assignment's counting
+  // sort (group-major, so a wave's points mostly share a centroid); the
+  // first assignment takes them in row order.  Slot s holds row
+  // perm[s] - row0 of this k-means.
+  const int32_t* prm = it > 0 ? a.perm + (size_t)bh * a.N : nullptr;
+  auto row_of = [&](int s) { return prm ? prm[s] - a.row0 : s; };
   bf16x8 bhi[NPS][KS], blo[NPS][KS];
 #pragma unroll
   for (int ps = 0; ps < NPS; ++ps) {
-    const int jc = min(jbase + ps * 32 + n, a.n - 1);
+    const int jc = row_of(min(jbase + ps * 32 + n, a.n - 1));
     const uint16_t* xh = a.xhi + ((size_t)bh * a.n + jc) * RP;
     const uint16_t* xl = a.xlo + ((size_t)bh * a.n + jc) * RP;
 #pragma unroll
@@ -600,22 +607,51 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   // lanes), zeros elsewhere, so the centroid lanes' k >= 3 entries drop out
   const bf16x8 ones = __builtin_bit_cast(
       bf16x8, h ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u));
-  // Largest centroid squared norm of the head (for the error bound).
+  // Largest centroid squared norm of the head (for the error bound), the
+  // same value in every wave.
   float umax = 0.f;
   const float* cu = a.cu + (size_t)bh * a.CP;
-  for (int b = tid; b < a.C; b += 256) umax = fmaxf(umax, cu[b]);
+  for (int b = lane; b < a.C; b += 64) umax = fmaxf(umax, cu[b]);
   umax = wave_max(umax);
-  if (lane == 0) sred[wv] = umax;
   // Three smallest estimates per point, ascending, each with its centroid
   // index in the low IB mantissa bits (C <= 2^IB).  Replacing those bits
   // moves a value by at most 2^(IB-23) of its magnitude, which the decision
   // below adds to the error bound.  Keeping (value, index) in one float lets
   // min / med3 maintain the sorted triple in three instructions per score.
+  // The start value is finite and above every score.
   const int ib = 32 - __clz(a.CP - 1);
   const uint32_t keep = ~((1u << ib) - 1u);
+  const float ek = ldexpf(1.f, ib - 22);
   float t1[NPS], t2[NPS], t3[NPS];
 #pragma unroll
-  for (int ps = 0; ps < NPS; ++ps) t1[ps] = t2[ps] = t3[ps] = INFINITY;
+  for (int ps = 0; ps < NPS; ++ps) t1[ps] = t2[ps] = t3[ps] = 3.4e38f;
+  // Skipping tiles.  Let e be a point's smallest packed estimate and M twice
+  // the error bound of its scores (mrg below).  The decision only looks at
+  // estimates p with p - e <= M + ek (|e| + |p|); a larger one can stay out
+  // of the triple without changing it (p - ek |p| grows with p, and an entry
+  // left at the start value passes the same test).  For any U >= e every such
+  // p has a raw score at most
+  //   L(U) = U + M + 2 ek |U| + ek |U|          when U + M + 2 ek |U| <= 0
+  //   L(U) = U + M + 5 ek (|U| + M) + 2^-20 ... otherwise,
+  // both growing with U (the packing moves a raw score by at most ek/2 of
+  // it, and the small absolute terms cover the rounding of L).  U is the
+  // smallest estimate folded so far over both halves of the centroids, so a
+  // wave folds a tile into set ps's triples only when some lane has a raw
+  // score at or below L(U) (or a NaN); until the first fold U is infinite.
+  float mrg[NPS], thr[NPS];
+#pragma unroll
+  for (int ps = 0; ps < NPS; ++ps) {
+    const float xn = a.xn[(size_t)bh * a.n + row_of(min(jbase + ps * 32 + n, a.n - 1))];
+    mrg[ps] = 2.f * (3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax);
+    thr[ps] = INFINITY;
+  }
+  auto bound = [&](int ps) {
+    const float u = fminf(t1[ps], __shfl_xor(t1[ps], 32));
+    const float au = fabsf(u), m = mrg[ps];
+    const float lp = u + fmaf(2.f * ek, au, m);
+    const float slack = 0x1p-20f * (au + m);
+    return lp <= 0.f ? lp + fmaf(ek, au, slack) : u + m + fmaf(5.f * ek, au + m, slack);
+  };
   // centroid index of accumulator register i: c0 + (i/4)*8 + h*4 + i%4
   uint32_t cidx[16];
 #pragma unroll
@@ -647,15 +683,24 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
   constexpr int kWaitVm0 = 0x3f70;
   // the point operands and the norms above are ordinary loads: wait for
   // them once here, so no later wait of the compiler's covers the copies
+  // The block sweeps the tiles from the one holding its first point's
+  // previous label (that of the earlier call in a warm first assignment; in
+  // a cold one, the start centroid of a nearby row), wrapping around: the
+  // running minima are tight early.  Any start gives the same result.
+  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
+  const int jb0 = blockIdx.x * (128 * NPS);
+  int cst = (it > 0 || a.warm) ? lab[row_of(jb0)] : (int)(((int64_t)jb0 * a.C) / a.n);
+  cst = __builtin_amdgcn_readfirstlane(min(max(cst, 0), a.C - 1) & ~31);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
-  issue(0, 0);
-  int buf = 0;
-  for (int c0 = 0; c0 < a.CP; c0 += 32, buf ^= 1) {
+  issue(cst, 0);
+  int buf = 0, c0 = cst;
+  for (int t = 0; t < a.CP; t += 32, buf ^= 1) {
     // this wave's copies of the tile have landed; after the barrier every
     // wave's have, and every wave is done with the other buffer
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
-    if (c0 + 32 < a.CP) issue(c0 + 32, buf ^ 1);
+    const int cnext = c0 + 32 < a.CP ? c0 + 32 : 0;
+    if (t + 32 < a.CP) issue(cnext, buf ^ 1);
     const unsigned char* tb = &tiles[buf][0];
     const uint16_t* shi = (const uint16_t*)tb;
     const uint16_t* slo = (const uint16_t*)(tb + ARR);
@@ -685,12 +730,20 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
       S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(an, ones, S[ps], 0, 0, 0);
-    // fold the tile into the sorted triples
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t idx = cidx[i] + (uint32_t)c0;
+    for (int ps = 0; ps < NPS; ++ps) {
+      // the lane's smallest raw score of the tile (NaN only if all are);
+      // plain code, so the compiler keeps the wait states an MFMA result
+      // needs before a VALU instruction reads it
+      float m = fminf(fminf(S[ps][0], S[ps][1]), S[ps][2]);
 #pragma unroll
-      for (int ps = 0; ps < NPS; ++ps) {
+      for (int i = 3; i < 15; i += 2) m = fminf(fminf(m, S[ps][i]), S[ps][i + 1]);
+      m = fminf(m, S[ps][15]);
+      if (__builtin_amdgcn_ballot_w64(!(m > thr[ps])) == 0) continue;
+      // fold the tile into set ps's sorted triples
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t idx = cidx[i] + (uint32_t)c0;
         const float pk = __uint_as_float((__float_as_uint(S[ps][i]) & keep) | idx);
         const float n3 = med3_packed(t2[ps], t3[ps], pk);
         const float n2 = med3_packed(t1[ps], t2[ps], pk);
@@ -698,7 +751,9 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
         t2[ps] = n2;
         t3[ps] = n3;
       }
+      thr[ps] = bound(ps);
     }
+    c0 = cnext;
   }
   // merge with the other half of the centroids (lane l ^ 32, same points)
 #pragma unroll
@@ -713,27 +768,23 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
       t3[ps] = n3;
     }
   }
-  __syncthreads();
-  umax = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
-  int32_t* lab = a.labels + (size_t)bh * a.N + a.row0;
-  // lane (n, h) decides point n of set h
+  // lane (n, h) decides point n of set h (slot j, row jr)
   const int j = jbase + h * 32 + n;
   if (j < a.n) {
+    const int jr = row_of(j);
     const float T1 = h ? t1[1] : t1[0], T2 = h ? t2[1] : t2[0], T3 = h ? t3[1] : t3[0];
     // the packed indices are below C whenever a real centroid has a finite
     // score; non-finite coordinates (flagged by k_project) could leave a
     // padding index or NaN bits, so the indices are clamped into range
     const int i1 = min((int)(__float_as_uint(T1) & ~keep), a.C - 1);
     const int i2 = min((int)(__float_as_uint(T2) & ~keep), a.C - 1);
-    const float xn = a.xn[(size_t)bh * a.n + j];
-    const float delta = 3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax;
-    const float ek = ldexpf(1.f, ib - 22);
+    const float delta = 0.5f * (h ? mrg[1] : mrg[0]);
     int label = -1;
     if (T2 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T2))) {
       label = i1;  // unique candidate: the exact argmin
     } else if (T3 - T1 > 2.f * delta + ek * (fabsf(T1) + fabsf(T3))) {
       // exactly two candidates: rescore both with the defining float score
-      const float* xp = a.pts + ((size_t)bh * a.n + j) * a.R;
+      const float* xp = a.pts + ((size_t)bh * a.n + jr) * a.R;
       const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
       const float* c2 = a.cent + ((size_t)bh * a.C + i2) * a.R;
       float d1 = 0.f, d2 = 0.f;
@@ -746,12 +797,12 @@ __global__ __launch_bounds__(256, 2) void k_km_assign_mfma(KmArgs a, int it) {
       label = (s2 < s1 || (s2 == s1 && i2 < i1)) ? i2 : i1;
     } else {
       // more than two candidates: the block's exact scan below
-      sfb[atomicAdd(&nfb, 1)] = j;
+      sfb[atomicAdd(&nfb, 1)] = jr;
       atomicAdd(a.fbcnt + (size_t)bh * 2 * a.T + a.sel * a.T + it, 1);
     }
     if (label >= 0) {
-      const int old = lab[j];
-      lab[j] = label;
+      const int old = lab[jr];
+      lab[jr] = label;
       if (it > 0 && old != label) atomicAdd(&km_changed(a, bh)[it], 1);
     }
   }
@@ -2156,6 +2207,7 @@ static void run_kmeans(const Geom& g, const KmArgs& a0, hipStream_t s, bool warm
   a.CP = (a.C + 31) / 32 * 32;
   // warm start: the centroids left by the previous call are the initial ones
   if (!warm) k_km_init<<<dim3((a.C * a.R + 255) / 256, BH), 256, 0, s>>>(a);
+  a.warm = warm;
   const int iters = warm ? g.T_warm : g.T;
   for (int it = 0; it < iters; ++it) {
     assign_step(g, a, it, s);
