@@ -446,20 +446,25 @@ __global__ void k_km_init(KmArgs a) {
 // bf16 MFMA on a three-term split (x = x_hi + x_lo, c = c_hi + c_lo;
 // t~ = x_hi c_hi + x_hi c_lo + x_lo c_hi) and bounded.  The centroid operands
 // hold -2c (a power-of-two scaling, exact in bf16) and one more K block adds
-// the centroid norm in three bf16 parts against ones, last, so the
-// accumulator ends with the whole score u - 2 x.c and no VALU pass forms it.
+// the centroid norm in three bf16 parts against ones and, against a one,
+// the point's shift s = bf16(|x|^2), last, so the accumulator ends with the
+// whole score u - 2 x.c plus s and no VALU pass forms it.  The shift is the
+// same for every centroid of a point, so it cancels in every comparison; it
+// makes the smallest scores about |x - c|^2 instead of about -|x|^2, ten
+// times smaller here, and with them the index packing's perturbation below.
 // Bounds: the neglected lo*lo terms are below 3.1 * 2^-16 sum|x_k c_k|, the
 // fp32 accumulation of the 3R exact bf16 products and the exact float chain
 // each below gamma_{3R} and gamma_R times sum|x_k c_k| (both doubled by the
-// factor 2), the norm block below four roundings of at most 2^-23 of
-// u_max + 2|x| c_max plus the 2^-24 u left out of the split, and the exact
-// score's own fma below 2^-24 (u_max + 2|x| c_max); with |sum| <= |x||c|
-// every estimated score is within
-// Delta = 1.61e-4 |x| c_max + 6.0e-7 u_max of the exact one (Delta below
-// carries another factor 2).  When the best estimate beats the runner-up by
-// more than 2 Delta, its centroid is the exact argmin; when only the third
-// is farther, the two candidates are rescored exactly; every other point is
-// rescored against all centroids by its block at the end of the kernel.
+// factor 2), the norm block below five roundings of at most 2^-23 of
+// u_max + 2|x| c_max + s plus the 2^-24 u left out of the split, and the
+// exact score's own fma below 2^-24 (u_max + 2|x| c_max); with
+// |sum| <= |x||c| every estimated score is within
+// Delta = 1.62e-4 |x| c_max + 8.0e-7 (u_max + |x|^2) of the exact one plus s
+// (Delta below carries another factor 2).  When the best estimate beats the
+// runner-up by more than 2 Delta, its centroid is the exact argmin; when only
+// the third is farther, the two candidates are rescored exactly; every other
+// point is rescored against all centroids by its block at the end of the
+// kernel.
 
 __device__ __forceinline__ uint16_t bf16_rne_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
@@ -603,10 +608,6 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       blo[ps][ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(xl + ks * 16 + h * 8));
     }
   }
-  // the norm block's point operand: ones at k = 0, 1, 2 (held by the h = 0
-  // lanes), zeros elsewhere, so the centroid lanes' k >= 3 entries drop out
-  const bf16x8 ones = __builtin_bit_cast(
-      bf16x8, h ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u));
   // Largest centroid squared norm of the head (for the error bound), the
   // same value in every wave.
   float umax = 0.f;
@@ -639,11 +640,18 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
   // wave folds a tile into set ps's triples only when some lane has a raw
   // score at or below L(U) (or a NaN); until the first fold U is infinite.
   float mrg[NPS], thr[NPS];
+  // the norm block's point operand: ones at k = 0, 1, 2 and the shift at
+  // k = 3 (held by the h = 0 lanes), zeros elsewhere, so the centroid lanes'
+  // k >= 4 entries drop out
+  bf16x8 bnorm[NPS];
 #pragma unroll
   for (int ps = 0; ps < NPS; ++ps) {
     const float xn = a.xn[(size_t)bh * a.n + row_of(min(jbase + ps * 32 + n, a.n - 1))];
-    mrg[ps] = 2.f * (3.22e-4f * xn * sqrtf(umax) * 1.000001f + 1.2e-6f * umax);
+    mrg[ps] = 2.f * (3.24e-4f * xn * sqrtf(umax) * 1.000001f + 8.0e-7f * (umax + xn * xn));
     thr[ps] = INFINITY;
+    const uint32_t sh = bf16_rne_bits(xn * xn);
+    bnorm[ps] = __builtin_bit_cast(
+        bf16x8, h ? make_uint4(0u, 0u, 0u, 0u) : make_uint4(0x3F803F80u, 0x3F80u | (sh << 16), 0u, 0u));
   }
   auto bound = [&](int ps) {
     const float u = fminf(t1[ps], __shfl_xor(t1[ps], 32));
@@ -652,10 +660,6 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
     const float slack = 0x1p-20f * (au + m);
     return lp <= 0.f ? lp + fmaf(ek, au, slack) : u + m + fmaf(5.f * ek, au + m, slack);
   };
-  // centroid index of accumulator register i: c0 + (i/4)*8 + h*4 + i%4
-  uint32_t cidx[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) cidx[i] = (uint32_t)((i >> 2) * 8 + h * 4 + (i & 3));
   const uint16_t* chi = a.chi + (size_t)bh * a.CP * RP;
   const uint16_t* clo = a.clo + (size_t)bh * a.CP * RP;
   const uint32_t* cn3 = a.cn3 + (size_t)bh * a.CP * 2;
@@ -712,7 +716,7 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       al[ks] = __builtin_bit_cast(bf16x8, *(const uint4*)(slo + n * LD + ks * 16 + h * 8));
     }
     const uint2 w = *(const uint2*)&su3[2 * n];
-    const bf16x8 an = __builtin_bit_cast(bf16x8, make_uint4(w.x, w.y, 0u, 0u));
+    const bf16x8 an = __builtin_bit_cast(bf16x8, make_uint4(w.x, w.y | 0x3F800000u, 0u, 0u));
     // scores S = u - 2 x.c, the norm block last
     f32x16 S[NPS];
 #pragma unroll
@@ -729,7 +733,7 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       }
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps)
-      S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(an, ones, S[ps], 0, 0, 0);
+      S[ps] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(an, bnorm[ps], S[ps], 0, 0, 0);
 #pragma unroll
     for (int ps = 0; ps < NPS; ++ps) {
       // the lane's smallest raw score of the tile (NaN only if all are);
@@ -743,7 +747,8 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       // fold the tile into set ps's sorted triples
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const uint32_t idx = cidx[i] + (uint32_t)c0;
+        // centroid index of accumulator register i: c0 + (i/4)*8 + h*4 + i%4
+        const uint32_t idx = (uint32_t)(c0 + h * 4) + (uint32_t)((i >> 2) * 8 + (i & 3));
         const float pk = __uint_as_float((__float_as_uint(S[ps][i]) & keep) | idx);
         const float n3 = med3_packed(t2[ps], t3[ps], pk);
         const float n2 = med3_packed(t1[ps], t2[ps], pk);
@@ -788,10 +793,25 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       const float* c1 = a.cent + ((size_t)bh * a.C + i1) * a.R;
       const float* c2 = a.cent + ((size_t)bh * a.C + i2) * a.R;
       float d1 = 0.f, d2 = 0.f;
-      for (int k = 0; k < a.R; ++k) {
-        const float xk = xp[k];
-        d1 = fmaf(xk, c1[k], d1);
-        d2 = fmaf(xk, c2[k], d2);
+      if ((a.R & 3) == 0) {
+        for (int k = 0; k < a.R; k += 4) {
+          const float4 x4 = *(const float4*)(xp + k);
+          const float4 p4 = *(const float4*)(c1 + k), q4 = *(const float4*)(c2 + k);
+          d1 = fmaf(x4.x, p4.x, d1);
+          d2 = fmaf(x4.x, q4.x, d2);
+          d1 = fmaf(x4.y, p4.y, d1);
+          d2 = fmaf(x4.y, q4.y, d2);
+          d1 = fmaf(x4.z, p4.z, d1);
+          d2 = fmaf(x4.z, q4.z, d2);
+          d1 = fmaf(x4.w, p4.w, d1);
+          d2 = fmaf(x4.w, q4.w, d2);
+        }
+      } else {
+        for (int k = 0; k < a.R; ++k) {
+          const float xk = xp[k];
+          d1 = fmaf(xk, c1[k], d1);
+          d2 = fmaf(xk, c2[k], d2);
+        }
       }
       const float s1 = fmaf(-2.f, d1, cu[i1]), s2 = fmaf(-2.f, d2, cu[i2]);
       label = (s2 < s1 || (s2 == s1 && i2 < i1)) ? i2 : i1;
