@@ -539,6 +539,20 @@ __device__ __forceinline__ float min_packed(float x, float y) {
   return d;
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n below 7 (gfx9 encoding: vmcnt in
+// bits 3:0, expcnt and lgkmcnt left at their maxima); larger n waits for all
+__device__ __forceinline__ void km_wait_vm(int n) {
+  switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(0x3f70); break;
+    case 1: __builtin_amdgcn_s_waitcnt(0x3f71); break;
+    case 2: __builtin_amdgcn_s_waitcnt(0x3f72); break;
+    case 3: __builtin_amdgcn_s_waitcnt(0x3f73); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x3f74); break;
+    case 5: __builtin_amdgcn_s_waitcnt(0x3f75); break;
+    case 6: __builtin_amdgcn_s_waitcnt(0x3f76); break;
+    default: __builtin_amdgcn_s_waitcnt(0x3f70); break;
+  }
+}
 // Direct global -> LDS copies for the centroid tiles: lane l's 16 (or 4)
 // bytes land at lds + 16 l (4 l), with lds the same for the whole wave; the
 // compiler does not see these loads, so the kernel orders them with explicit
@@ -562,9 +576,9 @@ __device__ __forceinline__ void km_g2lds4(const void* src, uint32_t lds) {
 // of 32 (the N side of v_mfma_f32_32x32x16_bf16), against 32-centroid tiles
 // in LDS (the M side); every centroid fragment read from LDS feeds both
 // sets.  The tiles (hi and lo rows, padded, and the norms' bf16 parts) are
-// double-buffered and filled by direct global -> LDS copies issued one tile
-// ahead, one barrier per tile.  Lane (n, h) ends with the three best
-// estimates of point n of each set over half of the centroids; the halves
+// in a ring of three LDS buffers filled by direct global -> LDS copies
+// issued two tiles ahead, one barrier per tile.  Lane (n, h) ends with the
+// three best estimates of point n of each set over half of the centroids; the halves
 // are merged with one exchange, and lane h then decides set h's point.  The
 // second launch bound (three blocks per CU up to rank 64, two above) caps
 // the registers at 168 / 256, so the accumulators stay in VGPRs that the
@@ -579,7 +593,7 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
   constexpr int NINST = (NPIECE + 63) / 64;
   constexpr int TILE = 2 * ARR + 256;   // + the 32 norms' parts
   constexpr int NPS = 2;                // sets of 32 points per wave
-  __shared__ __attribute__((aligned(1024))) unsigned char tiles[2][TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char tiles[3][TILE];
   __shared__ int sfb[256];  // the block's points left to the exact scan
   __shared__ int nfb;
   __shared__ __attribute__((aligned(16))) float xs[RP];
@@ -695,16 +709,26 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
   const int jb0 = blockIdx.x * (128 * NPS);
   int cst = (it > 0 || a.warm) ? lab[row_of(jb0)] : (int)(((int64_t)jb0 * a.C) / a.n);
   cst = __builtin_amdgcn_readfirstlane(min(max(cst, 0), a.C - 1) & ~31);
+  // copy instructions this wave issues per tile (vmcnt counts them in order)
+  const int ncopy = (NINST - wv + 3) / 4 + (wv == 0);
+  // three buffers: the copies run two tiles ahead of the MFMAs
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   issue(cst, 0);
+  const int cnx0 = cst + 32 < a.CP ? cst + 32 : 0;
+  if (32 < a.CP) issue(cnx0, 1);
   int buf = 0, c0 = cst;
-  for (int t = 0; t < a.CP; t += 32, buf ^= 1) {
-    // this wave's copies of the tile have landed; after the barrier every
-    // wave's have, and every wave is done with the other buffer
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  for (int t = 0; t < a.CP; t += 32, buf = buf == 2 ? 0 : buf + 1) {
+    // this wave's copies of the tile have landed (only the next tile's may
+    // still be in flight); after the barrier every wave's have, and every
+    // wave is done with the previous tile's buffer, which takes tile t + 2
+    if (t + 32 < a.CP)
+      km_wait_vm(ncopy);
+    else
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
     const int cnext = c0 + 32 < a.CP ? c0 + 32 : 0;
-    if (t + 32 < a.CP) issue(cnext, buf ^ 1);
+    const int cn2 = cnext + 32 < a.CP ? cnext + 32 : 0;
+    if (t + 64 < a.CP) issue(cn2, buf == 0 ? 2 : buf - 1);
     const unsigned char* tb = &tiles[buf][0];
     const uint16_t* shi = (const uint16_t*)tb;
     const uint16_t* slo = (const uint16_t*)(tb + ARR);
