@@ -214,16 +214,29 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
   const int bh = blockIdx.y, tid = threadIdx.x;
   const float* Fh = F + (size_t)bh * D * R;
   if constexpr (MF) {
-    for (int i = tid; i < D * MAXR; i += 256) {
-      const int k = i / MAXR, c = i % MAXR;
-      const float f = c < R ? Fh[k * R + c] : 0.f;
-      const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f);
-      const float r1 = f - bf16_bits_to_f32(hi);
-      const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
-      const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
-      fsp[(0 * MAXR + c) * FLD + k] = hi;
-      fsp[(1 * MAXR + c) * FLD + k] = mid;
-      fsp[(2 * MAXR + c) * FLD + k] = lo;
+    // eight loads in flight per thread, then their splits
+    constexpr int PER = D * MAXR / 256, BATCH = 8;
+    static_assert(PER % BATCH == 0, "F split batches");
+    for (int i0 = 0; i0 < PER; i0 += BATCH) {
+      float f[BATCH];
+#pragma unroll
+      for (int e = 0; e < BATCH; ++e) {
+        const int i = (i0 + e) * 256 + tid;
+        const int k = i / MAXR, c = i % MAXR;
+        f[e] = c < R ? Fh[k * R + c] : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < BATCH; ++e) {
+        const int i = (i0 + e) * 256 + tid;
+        const int k = i / MAXR, c = i % MAXR;
+        const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f[e]);
+        const float r1 = f[e] - bf16_bits_to_f32(hi);
+        const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
+        const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
+        fsp[(0 * MAXR + c) * FLD + k] = hi;
+        fsp[(1 * MAXR + c) * FLD + k] = mid;
+        fsp[(2 * MAXR + c) * FLD + k] = lo;
+      }
     }
   } else if (R == MAXR) {
     for (int i = tid; i < D * MAXR / 4; i += 256) ((float4*)fs)[i] = ((const float4*)Fh)[i];
