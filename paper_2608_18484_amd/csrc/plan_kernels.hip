@@ -639,7 +639,13 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
   // same value in every wave.
   float umax = 0.f;
   const float* cu = a.cu + (size_t)bh * a.CP;
-  for (int b = lane; b < a.C; b += 64) umax = fmaxf(umax, cu[b]);
+  for (int b0 = 0; b0 < a.C; b0 += 64 * 8) {  // eight loads in flight per lane
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = b0 + e * 64 + lane < a.C ? cu[b0 + e * 64 + lane] : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) umax = fmaxf(umax, v[e]);
+  }
   umax = wave_max(umax);
   // Three smallest estimates per point, ascending, each with its centroid
   // index in the low IB mantissa bits (C <= 2^IB).  Replacing those bits
