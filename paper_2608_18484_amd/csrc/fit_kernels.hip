@@ -393,7 +393,7 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
   constexpr int CW = D / 4, RS = 16;
   __shared__ __attribute__((aligned(16))) float fy[D][RS];
   __shared__ __attribute__((aligned(16))) float fp[D][RS];
-  __shared__ __attribute__((aligned(16))) float fvs[3][D];  // mu_x, s_x, mu_R
+  __shared__ __attribute__((aligned(16))) float fvs[3][D];  // mu_x, 1 / s_x, mu_R
   const int bq = blockIdx.y, bh = bq % g.BH, tid = threadIdx.x;
   const int r = g.r;
   const int rw = tid >> 2, qtr = tid & 3;
@@ -412,7 +412,8 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
       fp[c][sl] = t < tn ? Psi[c * r + t0 + t] : 0.f;
     }
   };
-  for (int i = tid; i < 3 * D; i += 256) fvs[i / D][i % D] = fv[i];
+  // mu_x, 1 / s_x (one division per column and block, not per row), mu_R
+  for (int i = tid; i < 3 * D; i += 256) fvs[i / D][i % D] = i / D == 1 ? 1.f / fv[i] : fv[i];
   if (one_slice) stage(0);
   __syncthreads();
   for (int chunk = 0; chunk < CORR_CHUNKS; ++chunk) {
@@ -445,7 +446,7 @@ __global__ __launch_bounds__(256) void k_correct(Geom g, Work w, void* out) {
 #pragma unroll
       for (int c = 0; c < CW; ++c) {
         const int col = qtr * CW + c;
-        const float xb = (x[c] - fvs[0][col]) / fvs[1][col];
+        const float xb = (x[c] - fvs[0][col]) * fvs[1][col];
 #pragma unroll
         for (int t4 = 0; t4 < RS / 4; ++t4) {
           const float4 y4 = *(const float4*)&fy[col][(t4 ^ qtr) * 4];
