@@ -355,8 +355,9 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
           for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o);
           den = fmaxf(sqrtf(ss / (float)R), eps);
         }
+        const float inv = 1.f / den;  // one division per row, not per element
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) pooled[u][c] += acc[u][c] / den;
+        for (int c = 0; c < CPT; ++c) pooled[u][c] = fmaf(acc[u][c], inv, pooled[u][c]);
       }
     }
 #pragma unroll
