@@ -325,8 +325,20 @@ def main():
     dense = None
     if not args.no_dense:
         ql, kl, vl = inputs[(ncall[0] - 1) % len(inputs)]  # the inputs of the last call
-        dense = S.dense_attention(ql, kl, vl)
+        dense = S.dense_attention(ql, kl, vl, stream=stream)
+        # the same inputs through the library's dense attention (every key,
+        # the block-sparse kernel's MFMA layout), timed over three calls for
+        # the attention-level speedup of the whole SparsePR call
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(3):
+            S.dense_attention(ql, kl, vl, out=dense, stream=stream)
+        ev1.record(stream)
         torch.cuda.synchronize()
+        result["dense_ms"] = round(ev0.elapsed_time(ev1) / 3, 4)
+        result["speedup_vs_dense"] = round(result["dense_ms"] / result["ms_per_call"], 3)
+        log(f"dense attention {result['dense_ms']:.3f} ms per call; SparsePR call speedup "
+            f"{result['speedup_vs_dense']:.2f}x")
         o = out.float()
         dn = dense.float()
         diff = (o - dn).reshape(-1, d)
