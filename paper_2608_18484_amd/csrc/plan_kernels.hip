@@ -1896,20 +1896,49 @@ __global__ __launch_bounds__(256) void k_ranges(Geom g, Work w) {
 
 // Attention work items: each query group split into tiles of kQTile rows.
 __global__ __launch_bounds__(1024) void k_chunks(Geom g, Work w) {
-  extern __shared__ int nch[];  // CQt + 1 + 17
+  // A head's chunks in decreasing order of their group's routed key count
+  // (64 buckets of similar counts, heaviest first; any order inside a
+  // bucket): the attention launches dispatch chunks in list order, so the
+  // blocks left at the end of each launch are the short ones.  Every chunk's
+  // rows and arithmetic are the same in any order.
+  constexpr int NB = 64;
+  __shared__ int bcnt[NB];
+  __shared__ int wmax_s, total_s;
+  extern __shared__ int nch[];  // CQt
   const int bh = blockIdx.x, tid = threadIdx.x;
   const int32_t* oq = w.offq + (size_t)bh * (g.CQt + 1);
-  for (int a = tid; a < g.CQt; a += 1024) nch[a] = (oq[a + 1] - oq[a] + kQTile - 1) / kQTile;
-  __syncthreads();
-  const int total = block_exclusive_scan(nch, g.CQt, nch + g.CQt + 1);
-  int4* ch = w.chunks + (size_t)bh * g.nchunk_max;
   const int32_t* kt = w.keytot + (size_t)bh * g.CQt;
+  if (tid < NB) bcnt[tid] = 0;
+  if (tid == 0) wmax_s = 0;
+  __syncthreads();
   for (int a = tid; a < g.CQt; a += 1024) {
+    nch[a] = (oq[a + 1] - oq[a] + kQTile - 1) / kQTile;
+    if (nch[a] > 0) atomicMax(&wmax_s, kt[a]);
+  }
+  __syncthreads();
+  const int64_t wmax = wmax_s;
+  auto bucket = [&](int a) { return (int)(((wmax - kt[a]) * NB) / (wmax + 1)); };
+  for (int a = tid; a < g.CQt; a += 1024)
+    if (nch[a] > 0) atomicAdd(&bcnt[bucket(a)], nch[a]);
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int b = 0; b < NB; ++b) {
+      const int c = bcnt[b];
+      bcnt[b] = run;
+      run += c;
+    }
+    total_s = run;
+  }
+  __syncthreads();
+  int4* ch = w.chunks + (size_t)bh * g.nchunk_max;
+  for (int a = tid; a < g.CQt; a += 1024) {
+    if (nch[a] == 0) continue;
     const int na = oq[a + 1] - oq[a];
-    int c = nch[a];
+    int c = atomicAdd(&bcnt[bucket(a)], nch[a]);
     for (int r0 = 0; r0 < na; r0 += kQTile) ch[c++] = make_int4(a, r0, min(kQTile, na - r0), kt[a]);
   }
-  if (tid == 0) w.nchunks[bh] = total;
+  if (tid == 0) w.nchunks[bh] = total_s;
 }
 
 // ---------------------------------------------------------------------------
