@@ -28,20 +28,26 @@ sys.path.insert(0, ROOT)
 from paper_2608_18484_amd import workloads as W  # noqa: E402
 
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
-ATTN_SRC = os.path.join(ROOT, "paper_2608_18484_amd", "csrc", "attn_kernels.hip")
+# the attention kernel, and the planner that orders its chunks (dispatch
+# order changes how much K/V is read again from beyond L2)
+ATTN_SRCS = [os.path.join(ROOT, "paper_2608_18484_amd", "csrc", f)
+             for f in ("attn_kernels.hip", "plan_kernels.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_attn_mfma_long_video_traffic.json")
 
 
 def attn_traffic(workload):
     """HBM bytes of one call's sparse-attention launches, from the committed
     FETCH_SIZE / WRITE_SIZE counter runs (scaled by the copy calibration), or
-    None when they were taken on another workload or on a different kernel
-    source than the one built now."""
+    None when they were taken on another workload or on different kernel
+    sources (attention and planner) than the ones built now."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-        with open(ATTN_SRC, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        h = hashlib.sha256()
+        for src in ATTN_SRCS:
+            with open(src, "rb") as f:
+                h.update(f.read())
+        sha = h.hexdigest()
     except (OSError, ValueError):
         return None
     if rec.get("source_sha256") != sha or rec.get("workload") != workload:
