@@ -213,6 +213,9 @@ def main():
     if args.n_probes >= 0:
         p.n_probes = args.n_probes
     gqa = args.kv_heads > 0 and args.kv_heads != wl.heads
+    default_cfg = (args.density == 0.25 and not gqa and not args.warm_start
+                   and args.partition == "response" and args.probe_rule == "stratified"
+                   and args.routing == "priority" and not args.ridge_only and args.n_probes < 0)
     if gqa:
         if wl.heads % args.kv_heads:
             print("--kv-heads must divide the query heads", file=sys.stderr)
@@ -324,7 +327,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "k_attn_mfma<128, MODE_SPARSE>",
                      "achieved": round(attn_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-                     "kernel_ms": round(attn_ms, 4), "traffic": attn_traffic(wl.name),
+                     "kernel_ms": round(attn_ms, 4),
+                     # counters were taken on the default configuration only
+                     "traffic": attn_traffic(wl.name) if default_cfg else None,
                      "unit_of_work": f"one call's sparse-attention launches ({nseg} key segments)"},
     }
 
