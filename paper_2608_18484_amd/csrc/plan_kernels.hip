@@ -1055,7 +1055,7 @@ __global__ __launch_bounds__(256) void k_sort_scatter(KmArgs a, int it) {
 // float; an empty group keeps its centroid (and its assignment operands).
 // One wave per group: the members' rows are fetched 64 at a time (lane i
 // holds member m0 + i) and exchanged by readlane; lane l owns coordinates l
-// and l + 64, whose values are loaded eight members at a time and added in
+// and l + 64, whose values are loaded sixteen members at a time and added in
 // ascending member order.
 __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
   const int bh = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -1077,25 +1077,22 @@ __global__ __launch_bounds__(256) void k_km_update(KmArgs a, int it) {
     for (int m0 = s0; m0 < s1; m0 += 64) {
       const int cnt = min(64, s1 - m0);
       const int myrow = lane < cnt ? perm[m0 + lane] - a.row0 : 0;
-      int u = 0;
-      for (; u + 8 <= cnt; u += 8) {
-        float v0[8], v1[8];
+      // 16 members' loads in flight; past the last member the loads read a
+      // member row again and their values are not added
+      for (int u = 0; u < cnt; u += 16) {
+        float v0[16], v1[16];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float* pr = pts + (size_t)__builtin_amdgcn_readlane(myrow, u + e) * R;
+        for (int e = 0; e < 16; ++e) {
+          const float* pr = pts + (size_t)__builtin_amdgcn_readlane(myrow, (u + e) & 63) * R;
           v0[e] = pr[k0];
           if constexpr (TWO) v1[e] = pr[k1];
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          sum0 += (double)v0[e];
-          if constexpr (TWO) sum1 += (double)v1[e];
-        }
-      }
-      for (; u < cnt; ++u) {
-        const float* pr = pts + (size_t)__builtin_amdgcn_readlane(myrow, u) * R;
-        sum0 += (double)pr[k0];
-        if constexpr (TWO) sum1 += (double)pr[k1];
+        for (int e = 0; e < 16; ++e)
+          if (u + e < cnt) {
+            sum0 += (double)v0[e];
+            if constexpr (TWO) sum1 += (double)v1[e];
+          }
       }
     }
   };
@@ -1224,96 +1221,135 @@ __global__ __launch_bounds__(256) void k_group_mean(const void* x, Geom g, const
 
 // Query-response metric M_Q = Kt^T Kt / (C_k^+ d) from the nonempty key-space
 // group means centred by their uniform mean, equal weights
-// (App. B.2 eq. app_query_metric).
+// (App. B.2 eq. app_query_metric).  One sweep over the groups: with d_b the
+// nonempty means shifted by the first nonempty one (s) and S = sum_b d_b,
+//   sum_b (x_b - mu)(x_b - mu)^T = sum_b d_b d_b^T - S S^T / C_k^+,
+// since mu - s = S / C_k^+; the shift keeps both terms of the size of the
+// spread, so the fp64 difference loses no digits to a large common mean.
 template <int D>
 __global__ __launch_bounds__(256) void k_query_metric(const float* kbar, const int32_t* offk,
                                                       Geom g, double* gram) {
-  // block (x, bh) computes output rows [8x, 8x + 8); every entry is summed
-  // over the groups in ascending order.  Group means are staged in LDS 32
-  // groups at a time; the next chunk's loads are issued into registers
-  // before the current chunk is used.
-  constexpr int RB = 8, GB = 32;
-  constexpr int TPR = 256 / RB;       // threads per output row
-  constexpr int ENT = D / TPR;        // entries per thread
-  constexpr int P = 256 / D;          // threads per column of the mean
-  constexpr int LPT = GB * D / 4 / 256;  // float4 loads per thread per chunk
-  static_assert(LPT >= 1 && 256 % D == 0, "thread mapping");
-  __shared__ double mu[D];
-  __shared__ double part[P][D];
-  __shared__ double ks[GB][D + 1];
+  // Block (x, bh) computes output rows [RB x, RB x + RB).  Thread (tr, tc)
+  // holds rows RB x + 2 tr, +1 and columns 4 tc .. 4 tc + 3; every entry is
+  // one fp64 chain over the groups in ascending order.  Shifted means are
+  // staged in LDS GB groups at a time; the next chunk's loads are issued
+  // into registers before the current chunk is used.
+  constexpr int CQD = D / 4;               // column quads
+  constexpr int TRN = 256 / CQD;           // row pairs per block
+  constexpr int RB = 2 * TRN;              // rows per block
+  constexpr int GB = 32;
+  constexpr int LPT = GB * D / 4 / 256;    // float4 loads per thread per chunk
+  static_assert(LPT >= 1 && 256 % CQD == 0 && D % RB == 0, "thread mapping");
+  __shared__ __attribute__((aligned(32))) double ks[GB][D];
+  __shared__ double sh[D];
+  __shared__ __attribute__((aligned(32))) double ssum[256 / CQD][D];
   __shared__ int fl[GB];
-  __shared__ int cplus_part[P], cplus;
+  __shared__ int first_s, cnt_s;
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int C = g.CK;
   const int32_t* o = offk + (size_t)bh * (g.CKt + 1);
   const float* kb = kbar + (size_t)bh * C * D;
-  {
-    // uniform mean over the nonempty groups: column c, groups b = q, q+P, ...
-    const int c = tid % D, q = tid / D;
-    double sacc = 0.0;
-    int cp = 0;
-#pragma unroll 8
-    for (int bb = q; bb < C; bb += P) {
-      const bool ne = o[bb + 1] > o[bb];
-      const float x = kb[(size_t)bb * D + c];
-      sacc += ne ? (double)x : 0.0;
-      cp += ne;
-    }
-    part[q][c] = sacc;
-    if (c == 0) cplus_part[q] = cp;
+  if (tid == 0) {
+    first_s = C;
+    cnt_s = 0;
   }
   __syncthreads();
-  if (tid < D) {
-    double sacc = 0.0;
-    int cp = 0;
-#pragma unroll
-    for (int q = 0; q < P; ++q) {
-      sacc += part[q][tid];
-      cp += cplus_part[q];
+  // the first nonempty group (its mean is the shift) and the nonempty count
+  {
+    int first = C, cnt = 0;
+    for (int b = tid; b < C; b += 256) {
+      const bool ne = o[b + 1] > o[b];
+      cnt += ne;
+      if (ne && first == C) first = b;
     }
-    mu[tid] = cp ? sacc / cp : 0.0;
-    if (tid == 0) cplus = cp;
+    if (first < C) atomicMin(&first_s, first);
+    atomicAdd(&cnt_s, cnt);
   }
-  const int ra = blockIdx.x * RB + tid / TPR, cb = (tid % TPR) * ENT;
-  double acc[ENT];
+  __syncthreads();
+  const int first = first_s, cplus = cnt_s;
+  if (tid < D) sh[tid] = first < C ? (double)kb[(size_t)first * D + tid] : 0.0;
+  const int tc = tid % CQD, tr = tid / CQD;
+  const int r0 = blockIdx.x * RB + 2 * tr, c0 = 4 * tc;
+  // acc: the thread's entries of sum_b d_b d_b^T; sp: its staging columns'
+  // sums over the groups it stages (b = tid / CQD + k * 256 / CQD)
+  double acc[2][4], sp[4];
 #pragma unroll
-  for (int e = 0; e < ENT; ++e) acc[e] = 0.0;
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[a][e] = 0.0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) sp[e] = 0.0;
   float4 pre[LPT];
   int pfl = 0;
   auto load_chunk = [&](int b0) {
 #pragma unroll
     for (int l = 0; l < LPT; ++l) {
-      const int e4 = tid + 256 * l, bb = b0 + e4 / (D / 4);
-      pre[l] = bb < C ? ((const float4*)(kb + (size_t)bb * D))[e4 % (D / 4)] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int e4 = tid + 256 * l, bb = b0 + e4 / CQD;
+      pre[l] = bb < C ? ((const float4*)(kb + (size_t)bb * D))[e4 % CQD] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (tid < GB) pfl = (b0 + tid < C) && (o[b0 + tid + 1] > o[b0 + tid]);
   };
   load_chunk(0);
   for (int b0 = 0; b0 < C; b0 += GB) {
     if (tid < GB) fl[tid] = pfl;
-    __syncthreads();  // flags and mu visible; the previous chunk is consumed
+    __syncthreads();  // flags and the shift visible; the previous chunk is consumed
 #pragma unroll
     for (int l = 0; l < LPT; ++l) {
-      const int e4 = tid + 256 * l, i = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
+      const int e4 = tid + 256 * l, i = e4 / CQD, c = (e4 % CQD) * 4;
       const bool ne = fl[i] != 0;
-      ks[i][c + 0] = ne ? (double)pre[l].x - mu[c + 0] : 0.0;
-      ks[i][c + 1] = ne ? (double)pre[l].y - mu[c + 1] : 0.0;
-      ks[i][c + 2] = ne ? (double)pre[l].z - mu[c + 2] : 0.0;
-      ks[i][c + 3] = ne ? (double)pre[l].w - mu[c + 3] : 0.0;
+      double4 v;
+      v.x = ne ? (double)pre[l].x - sh[c + 0] : 0.0;
+      v.y = ne ? (double)pre[l].y - sh[c + 1] : 0.0;
+      v.z = ne ? (double)pre[l].z - sh[c + 2] : 0.0;
+      v.w = ne ? (double)pre[l].w - sh[c + 3] : 0.0;
+      *(double4*)&ks[i][c] = v;
+      sp[0] += v.x;
+      sp[1] += v.y;
+      sp[2] += v.z;
+      sp[3] += v.w;
     }
     if (b0 + GB < C) load_chunk(b0 + GB);
     __syncthreads();
-    const int cnt = min(GB, C - b0);
-    for (int i = 0; i < cnt; ++i) {
-      const double av = ks[i][ra];
+    // groups past the end were staged as zeros, so whole chunks are summed
+    // (four groups' operands loaded together)
+#pragma unroll 4
+    for (int i = 0; i < GB; ++i) {
+      const double2 rv = *(const double2*)&ks[i][r0];
+      const double4 cv = *(const double4*)&ks[i][c0];
+      const double r[2] = {rv.x, rv.y};
+      const double c[4] = {cv.x, cv.y, cv.z, cv.w};
 #pragma unroll
-      for (int e = 0; e < ENT; ++e) acc[e] += av * ks[i][cb + e];
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[a][e] = fma(r[a], c[e], acc[a][e]);
     }
   }
-  const double den = (double)max(cplus, 1) * (double)D;
-  double* out = gram + (size_t)bh * D * D + (size_t)ra * D + cb;
+  // S = sum_b d_b from the staging threads' partial sums
+  *(double4*)&ssum[tr][4 * tc] = make_double4(sp[0], sp[1], sp[2], sp[3]);
+  __syncthreads();
+  double rs[2], cs[4];
 #pragma unroll
-  for (int e = 0; e < ENT; ++e) out[e] = acc[e] / den;
+  for (int a = 0; a < 2; ++a) {
+    rs[a] = 0.0;
+    for (int q = 0; q < 256 / CQD; ++q) rs[a] += ssum[q][r0 + a];
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    cs[e] = 0.0;
+    for (int q = 0; q < 256 / CQD; ++q) cs[e] += ssum[q][c0 + e];
+  }
+  const double np = (double)max(cplus, 1);
+  const double den = np * (double)D;
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    double* out = gram + (size_t)bh * D * D + (size_t)(r0 + a) * D + c0;
+    double4 v;
+    v.x = (acc[a][0] - rs[a] * cs[0] / np) / den;
+    v.y = (acc[a][1] - rs[a] * cs[1] / np) / den;
+    v.z = (acc[a][2] - rs[a] * cs[2] / np) / den;
+    v.w = (acc[a][3] - rs[a] * cs[3] / np) / den;
+    *(double4*)out = v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1710,7 +1746,13 @@ __global__ __launch_bounds__(256) void k_sel_init(Geom g, Work w) {
 
 // Weighted radix select, one 8-bit digit of the 64-bit cell key per pass:
 // histogram of pair cost per digit over the cells still in the bucket.
+// Blocks take rows of the route matrix (two at a time), threads up to KB
+// columns each; the columns' sizes stay in registers across the rows.  The
+// leading digits are shared by most cells (the priorities span a few
+// binades), so each thread sums the cost of the first two digits it meets in
+// registers and adds only its other cells to LDS one by one.
 __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
+  constexpr int KB = 8, RR = 2;
   __shared__ unsigned long long hs[kSelBins];
   const int bh = blockIdx.y, tid = threadIdx.x;
   const int64_t* st = w.selstate + (size_t)bh * 8;
@@ -1724,21 +1766,65 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
   const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
   const unsigned long long cunit = sel_count_unit(g);
-  // rows a of the route matrix per block, columns b per thread: the row's
-  // size and forced cell are block-uniform and its scores are contiguous
-  for (int a = blockIdx.x; a < g.CQ; a += gridDim.x) {
-    const int na = oq[a + 1] - oq[a];
-    if (na == 0) continue;
-    const int fa = fo[a];
-    const int64_t row = (int64_t)a * g.CK;
-    for (int b = tid; b < g.CK; b += 256) {
-      const int nb = ok[b + 1] - ok[b];
-      if (nb == 0 || fa == b) continue;
-      const uint64_t key = cell_key(pr[row + b], row + b);
-      if (p > 0 && (key >> (shift + 8)) != (prefix >> (shift + 8))) continue;
-      atomicAdd(&hs[(key >> shift) & 255], (unsigned long long)na * (unsigned long long)nb + cunit);
+  // two digits per thread are summed in registers, the others added to LDS
+  int dA = -1, dB = -1;
+  unsigned long long sA = 0ull, sB = 0ull;
+  auto hist_add = [&](bool act, int dig, unsigned long long wgt) {
+    if (!act) return;
+    if (dig == dA) {
+      sA += wgt;
+    } else if (dig == dB) {
+      sB += wgt;
+    } else if (dA < 0) {
+      dA = dig;
+      sA = wgt;
+    } else if (dB < 0) {
+      dB = dig;
+      sB = wgt;
+    } else {
+      atomicAdd(&hs[dig], wgt);
+    }
+  };
+  for (int cb = 0; cb < g.CK; cb += 256 * KB) {
+    int nb[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int b = cb + tid + 256 * k;
+      nb[k] = b < g.CK ? ok[b + 1] - ok[b] : 0;
+    }
+    for (int a0 = blockIdx.x; a0 < g.CQ; a0 += RR * gridDim.x) {
+      int na[RR], fa[RR];
+      float pv[RR][KB];
+#pragma unroll
+      for (int r = 0; r < RR; ++r) {
+        const int a = a0 + r * gridDim.x;
+        na[r] = a < g.CQ ? oq[a + 1] - oq[a] : 0;
+        fa[r] = na[r] ? fo[a] : -1;
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+          const int b = cb + tid + 256 * k;
+          pv[r][k] = (na[r] && b < g.CK && nb[k]) ? pr[(int64_t)a * g.CK + b] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < RR; ++r) {
+        if (na[r] == 0) continue;  // uniform
+        const int64_t row = (int64_t)(a0 + r * gridDim.x) * g.CK;
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+          if (cb + 256 * k >= g.CK) break;  // uniform
+          const int b = cb + tid + 256 * k;
+          const uint64_t key = cell_key(pv[r][k], row + b);
+          bool act = b < g.CK && nb[k] != 0 && b != fa[r];
+          if (p > 0) act = act && (key >> (shift + 8)) == (prefix >> (shift + 8));
+          hist_add(act, (int)((key >> shift) & 255),
+                   (unsigned long long)na[r] * (unsigned long long)nb[k] + cunit);
+        }
+      }
     }
   }
+  if (dA >= 0) atomicAdd(&hs[dA], sA);
+  if (dB >= 0) atomicAdd(&hs[dB], sB);
   __syncthreads();
   uint64_t* gh = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
   for (int i = tid; i < kSelBins; i += 256)
@@ -2365,7 +2451,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   k_group_mean<<<dim3((g.CK + 3) / 4, BH), 256, 0, s>>>(k, g, w.permk, w.offk, g.CK, g.CKt + 1,
                                                          w.kbar, 0);
   if (g.partition == SPARSEPR_PARTITION_RESPONSE) {
-    k_query_metric<D><<<dim3(D / 8, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
+    k_query_metric<D><<<dim3(D * D / 2048, BH), 256, 0, s>>>(w.kbar, w.offk, g, w.gram_q);
     k_eig_basis<D><<<BH, 1024, 0, s>>>(w.gram_q, g.rq, 1e-6f, w.fq, w.evals_q, w.eigscr, w.stats);
     project<D>(g, w, q, w.fq, g.rq, 1, 1, g.eps_q, w.phiq, s);
   } else {
@@ -2388,7 +2474,8 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
     k_route_topp<<<dim3(g.CQ, BH), 256, (size_t)np2 * 8, s>>>(g, w, np2);
   }
   k_sel_init<<<BH, 256, 0, s>>>(g, w);
-  const int gsel = std::max(1, std::min(g.CQ, 512));
+  // about 2048 blocks over all heads, each taking rows of one head
+  const int gsel = std::max(1, std::min(g.CQ, (2048 + BH - 1) / BH));
   for (int p = 0; p < kSelPasses; ++p) {
     k_sel_hist<<<dim3(gsel, BH), 256, 0, s>>>(g, w, p);
     k_sel_choose<<<BH, 256, 0, s>>>(g, w, p);
