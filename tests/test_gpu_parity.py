@@ -549,13 +549,20 @@ def test_top_p_routing(orc, ntext):
     assert err < 2e-2, err
 
 
-@pytest.mark.parametrize("case", ["one_group", "no_probes", "singleton_groups"])
+@pytest.mark.parametrize("case", ["one_group", "no_probes", "singleton_groups", "half_probes",
+                                  "many_probes"])
 def test_degenerate_plans(orc, case):
     """One group per side (every row routes everything), no probe rows (the
-    output is the hard-drop output), and one group per token (singleton
-    groups, many short routed ranges): every plan stage against the oracle,
-    the output against its replay."""
-    if case == "one_group":
+    output is the hard-drop output), one group per token (singleton groups,
+    many short routed ranges), and 1024 / 1100 probe rows over 2048 rows (many
+    probes per query group, several in one 64-row tile): every plan stage
+    against the oracle, the output against its replay."""
+    if case.endswith("_probes") and case != "no_probes":
+        # density 1 keeps the pair budget above the probes' reserved cost
+        wl = medium(grid=(4, 16, 32), heads=1, density=1.0,
+                    n_probes=1024 if case == "half_probes" else 1100)
+        over = {}
+    elif case == "one_group":
         wl = medium(grid=(2, 16, 32), heads=1)
         over = dict(n_kv_groups=1, n_q_groups=1)
     elif case == "no_probes":
