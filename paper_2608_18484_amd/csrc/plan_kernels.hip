@@ -379,17 +379,31 @@ __global__ __launch_bounds__(256) void k_project(const void* x, Geom g, const fl
       float* out = phi + ((size_t)bh * g.NV + row) * R;
       uint16_t* oh = xhi + ((size_t)bh * g.NV + row) * RP;
       uint16_t* ol = xlo + ((size_t)bh * g.NV + row) * RP;
+      uint16_t hbs[CPT], lbs[CPT];
 #pragma unroll
       for (int c = 0; c < CPT; ++c) {
-        const int col = tx * CPT + c;
-        if (col < R) {
-          bad |= !isfinite(vv[c]);
-          out[col] = vv[c];
-        }
+        hbs[c] = __builtin_bit_cast(uint16_t, (__bf16)vv[c]);
+        lbs[c] = __builtin_bit_cast(uint16_t, (__bf16)(vv[c] - bf16_bits_to_f32(hbs[c])));
+        if (tx * CPT + c < R) bad |= !isfinite(vv[c]);
+      }
+      if (CPT == 4 && R % 4 == 0 && RP % 4 == 0) {
+        // a thread's four columns as one 16-byte and two 8-byte stores (row
+        // pitches of R floats and RP halves keep them aligned)
+        const int col = tx * 4;
+        if (col < R) *(float4*)(out + col) = make_float4(vv[0], vv[1], vv[2], vv[3]);
         if (col < RP) {
-          const uint16_t hb = __builtin_bit_cast(uint16_t, (__bf16)vv[c]);
-          oh[col] = hb;
-          ol[col] = __builtin_bit_cast(uint16_t, (__bf16)(vv[c] - bf16_bits_to_f32(hb)));
+          *(uint2*)(oh + col) = make_uint2(hbs[0] | ((uint32_t)hbs[1] << 16), hbs[2] | ((uint32_t)hbs[3] << 16));
+          *(uint2*)(ol + col) = make_uint2(lbs[0] | ((uint32_t)lbs[1] << 16), lbs[2] | ((uint32_t)lbs[3] << 16));
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+          const int col = tx * CPT + c;
+          if (col < R) out[col] = vv[c];
+          if (col < RP) {
+            oh[col] = hbs[c];
+            ol[col] = lbs[c];
+          }
         }
       }
       if (tx == 0) xn[(size_t)bh * g.NV + row] = sqrtf(ssq) * 1.000001f;
@@ -1834,40 +1848,52 @@ __global__ __launch_bounds__(256) void k_sel_hist(Geom g, Work w, int p) {
 // Pick the digit bucket where the cumulative cost (from the largest keys
 // down) first exceeds the remaining budget.
 __global__ __launch_bounds__(256) void k_sel_choose(Geom g, Work w, int p) {
-  __shared__ uint64_t gh[kSelBins];
-  const int bh = blockIdx.x;
+  // Thread t takes digit 255 - t: an inclusive scan of the pair costs from
+  // the largest digit down gives, per digit, the cost of it and every digit
+  // above, and the first digit where that exceeds the budget is the bucket.
+  static_assert(kSelBins == 256, "one digit per thread");
+  __shared__ long long wsum[4];
+  __shared__ int hit;
+  const int bh = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int64_t* st = w.selstate + (size_t)bh * 8;
   if (st[SS_DONE] != 0) return;  // uniform over the block
-  // the bins are read by all threads at once; thread 0 then walks them
   const uint64_t* ghg = w.selhist + ((size_t)bh * kSelPasses + p) * kSelBins;
-  for (int i = threadIdx.x; i < kSelBins; i += blockDim.x) gh[i] = ghg[i];
-  __syncthreads();
-  if (threadIdx.x != 0) return;
-  const int shift = 56 - 8 * p;
-  const long long rem = st[SS_REM];
-  long long run = st[SS_ABOVE];
-  for (int dg = kSelBins - 1; dg >= 0; --dg) {
-    const unsigned long long cunit = sel_count_unit(g);
-    const long long h = (long long)(cunit ? (gh[dg] & (cunit - 1ull)) : gh[dg]);
-    if (run + h > rem) {
-      const uint64_t prefix = (uint64_t)st[SS_PREFIX] | ((uint64_t)dg << shift);
-      st[SS_PREFIX] = (int64_t)prefix;
-      st[SS_ABOVE] = run;
-      if (shift == 0) {
-        st[SS_BOUND] = (int64_t)prefix;
-        st[SS_DONE] = 2;
-      } else if (cunit && (gh[dg] >> g.sel_cshift) == 1) {
-        // the boundary cell is the only one with this prefix: every cell of
-        // a higher bucket is taken and it is not, which is what comparing
-        // keys with the largest key of the prefix selects
-        st[SS_BOUND] = (int64_t)(prefix | ((1ull << shift) - 1ull));
-        st[SS_DONE] = 2;
-      }
-      return;
-    }
-    run += h;
+  const int dg = kSelBins - 1 - tid;
+  const uint64_t raw = ghg[dg];
+  const unsigned long long cunit = sel_count_unit(g);
+  const long long h = (long long)(cunit ? (raw & (cunit - 1ull)) : raw);
+  long long x = h;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const long long y = __shfl_up(x, o);
+    if (lane >= o) x += y;
   }
-  st[SS_DONE] = 1;
+  if (lane == 63) wsum[wv] = x;
+  if (tid == 0) hit = kSelBins;
+  __syncthreads();
+  long long cum = st[SS_ABOVE] + x;
+  for (int k = 0; k < wv; ++k) cum += wsum[k];
+  if (cum > (long long)st[SS_REM]) atomicMin(&hit, tid);
+  __syncthreads();  // every thread has read the state before it changes
+  if (hit == kSelBins) {
+    if (tid == 0) st[SS_DONE] = 1;
+    return;
+  }
+  if (tid != hit) return;
+  const int shift = 56 - 8 * p;
+  const uint64_t prefix = (uint64_t)st[SS_PREFIX] | ((uint64_t)dg << shift);
+  st[SS_PREFIX] = (int64_t)prefix;
+  st[SS_ABOVE] = cum - h;
+  if (shift == 0) {
+    st[SS_BOUND] = (int64_t)prefix;
+    st[SS_DONE] = 2;
+  } else if (cunit && (raw >> g.sel_cshift) == 1) {
+    // the boundary cell is the only one with this prefix: every cell of
+    // a higher bucket is taken and it is not, which is what comparing
+    // keys with the largest key of the prefix selects
+    st[SS_BOUND] = (int64_t)(prefix | ((1ull << shift) - 1ull));
+    st[SS_DONE] = 2;
+  }
 }
 
 // Route matrix over all cells (dense-prefix group included): forced cells,
