@@ -1427,18 +1427,36 @@ __global__ __launch_bounds__(256) void k_route_prio(const float* qbar, const flo
         qp[2][ks][e] = (__bf16)(r1 - (float)mid);
       }
     }
+    // a chunk's key means: every 16-byte load issued before the splits
+    constexpr int LPT4 = TR * D / 4 / 256;
     for (int b0 = 0; b0 < CK; b0 += TR) {
       __syncthreads();  // the previous chunk is consumed
-#pragma unroll 8
-      for (int i = tid; i < TR * D; i += 256) {
-        const int r = i / D, c = i % D;
-        const float f = b0 + r < CK ? kb[(size_t)(b0 + r) * D + c] : 0.f;
-        const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f);
-        const float r1 = f - bf16_bits_to_f32(hi);
-        const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
-        ks3[0][r][c] = hi;
-        ks3[1][r][c] = mid;
-        ks3[2][r][c] = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
+      float4 pre[LPT4];
+#pragma unroll
+      for (int j = 0; j < LPT4; ++j) {
+        const int i4 = tid + 256 * j, r = i4 * 4 / D, c = i4 * 4 % D;
+        pre[j] = b0 + r < CK ? *(const float4*)(kb + (size_t)(b0 + r) * D + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int j = 0; j < LPT4; ++j) {
+        const int i4 = tid + 256 * j, r = i4 * 4 / D, c = i4 * 4 % D;
+        const float fv[4] = {pre[j].x, pre[j].y, pre[j].z, pre[j].w};
+        uint32_t pw[3][2];  // the four values' parts, two per word (8-byte stores)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float f = fv[e];
+          const uint16_t hi = __builtin_bit_cast(uint16_t, (__bf16)f);
+          const float r1 = f - bf16_bits_to_f32(hi);
+          const uint16_t mid = __builtin_bit_cast(uint16_t, (__bf16)r1);
+          const uint16_t lo = __builtin_bit_cast(uint16_t, (__bf16)(r1 - bf16_bits_to_f32(mid)));
+          const int sh = 16 * (e & 1);
+          if ((e & 1) == 0) pw[0][e >> 1] = pw[1][e >> 1] = pw[2][e >> 1] = 0u;
+          pw[0][e >> 1] |= (uint32_t)hi << sh;
+          pw[1][e >> 1] |= (uint32_t)mid << sh;
+          pw[2][e >> 1] |= (uint32_t)lo << sh;
+        }
+#pragma unroll
+        for (int part = 0; part < 3; ++part) *(uint2*)&ks3[part][r][c] = make_uint2(pw[part][0], pw[part][1]);
       }
       __syncthreads();
       f32x16 Sb, Ss;
