@@ -2133,8 +2133,8 @@ __device__ __forceinline__ uint64_t probe_key(float d2, int row) {
 // id when there are at most M nonempty groups, otherwise the stride-s
 // interleave (rank mod s, rank), s = ceil(G / M)); each visit takes the
 // group's next row by (distance, row index).
-__global__ __launch_bounds__(256) void k_probe_select(Geom g, Work w) {
-  extern __shared__ int sh[];  // cnt[CQ] | ne[CQ] | mcount[CQ] | base[CQ + 1 + 5]
+__global__ __launch_bounds__(1024) void k_probe_select(Geom g, Work w) {
+  extern __shared__ int sh[];  // cnt[CQ] | ne[CQ] | mcount[CQ] | base[CQ + 1 + 17]
   int* cnt = sh;
   int* ne = cnt + g.CQ;
   int* mcount = ne + g.CQ;
@@ -2148,21 +2148,21 @@ __global__ __launch_bounds__(256) void k_probe_select(Geom g, Work w) {
   int32_t* picks = w.picks + (size_t)bh * M;
   float* pw = w.pw + (size_t)bh * M;
   const float* d2 = w.d2 + (size_t)bh * g.NV;
-  for (int a = tid; a < g.CQ; a += 256) {
+  for (int a = tid; a < g.CQ; a += 1024) {
     cnt[a] = oq[a + 1] - oq[a];
     mcount[a] = 0;
     base[a] = (cnt[a] > 0);
   }
   __syncthreads();
   const int ng = block_exclusive_scan(base, g.CQ, base + g.CQ + 1);
-  for (int a = tid; a < g.CQ; a += 256)
+  for (int a = tid; a < g.CQ; a += 1024)
     if (cnt[a] > 0) ne[base[a]] = a;
   if (tid == 0) G = ng;
   __syncthreads();
   // probes per group
   if (G > M) {
     const int s = (G + M - 1) / M, qs = G / s, rem = G % s;
-    for (int k = tid; k < G; k += 256) {
+    for (int k = tid; k < G; k += 1024) {
       const int res = k % s;
       const int pos = res * qs + min(res, rem) + k / s;
       if (pos < M) mcount[ne[k]] = 1;
@@ -2177,11 +2177,11 @@ __global__ __launch_bounds__(256) void k_probe_select(Geom g, Work w) {
         }
   }
   __syncthreads();
-  for (int a = tid; a < g.CQ; a += 256) base[a] = mcount[a];
+  for (int a = tid; a < g.CQ; a += 1024) base[a] = mcount[a];
   __syncthreads();
   block_exclusive_scan(base, g.CQ, base + g.CQ + 1);
   // each wave selects the mcount smallest (d2, row) rows of its groups
-  for (int a = wv; a < g.CQ; a += 4) {
+  for (int a = wv; a < g.CQ; a += 16) {
     const int m = mcount[a];
     if (m == 0) continue;
     const int s0 = oq[a], s1 = oq[a + 1];
@@ -2533,7 +2533,7 @@ static void plan_d(const Geom& g, const Work& w, const void* q, const void* k, h
   if (g.M > 0) {
     if (g.probe_rule == SPARSEPR_PROBES_STRATIFIED) {
       k_probe_d2<<<dim3((g.NV + 127) / 128, BH), 128, (g.rq % 4 == 0) ? (size_t)128 * (g.rq + 4) * 4 : 0, s>>>(g, w);
-      k_probe_select<<<BH, 256, (4 * g.CQ + 1 + 5) * sizeof(int), s>>>(g, w);
+      k_probe_select<<<BH, 1024, (4 * g.CQ + 1 + 17) * sizeof(int), s>>>(g, w);
     } else if (g.probe_rule == SPARSEPR_PROBES_UNIFORM) {
       k_probe_uniform<<<BH, 256, 0, s>>>(g, w);
     } else {
