@@ -57,18 +57,37 @@ __global__ __launch_bounds__(256) void k_key_metric(const void* q, Geom g, doubl
   for (int j = 0; j < g.G; ++j) {
     const int64_t base = q_base(g, bh, j);
     for (int s0 = 0; s0 < g.Ms; s0 += SB) {
-#pragma unroll 8
-      for (int t = tid; t < SB * D; t += 256) {
-        const int i = s0 + t / D, c = t % D;
-        float v = 0.f;
+      // eight consecutive elements per load (16 bytes of bf16, two float4)
+#pragma unroll
+      for (int t8 = tid; t8 < SB * D / 8; t8 += 256) {
+        const int i = s0 + t8 / (D / 8), c = (t8 % (D / 8)) * 8;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
         if (i < g.Ms) {
           const int64_t row = g.ntext + ((int64_t)i * g.NV) / g.Ms;
-          v = load_x(q, g.bf16, base + row * g.sn + c);
+          const int64_t off = base + row * g.sn + c;
+          if (g.bf16) {
+            const uint4 u = *(const uint4*)((const uint16_t*)q + off);
+            const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] = __uint_as_float(wds[e] << 16);
+              v[2 * e + 1] = __uint_as_float(wds[e] & 0xffff0000u);
+            }
+          } else {
+            const float4 u0 = *(const float4*)((const float*)q + off);
+            const float4 u1 = *(const float4*)((const float*)q + off + 4);
+            v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w;
+            v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
+          }
         }
-        qs[t / D][c] = v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qs[t8 / (D / 8)][c + e] = v[e];
       }
       __syncthreads();
       const int cnt = min(SB, g.Ms - s0);
+#pragma unroll 4
       for (int i = 0; i < cnt; ++i) {
         const double a = qs[i][ra];
 #pragma unroll
