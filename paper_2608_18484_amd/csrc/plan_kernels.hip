@@ -1946,28 +1946,51 @@ __global__ __launch_bounds__(256) void k_sel_mark(Geom g, Work w) {
   const int32_t* fo = w.forced + (size_t)bh * g.CQ;
   const float* pr = (g.routing == SPARSEPR_ROUTING_TOP_P ? w.skey : w.prio) + (size_t)bh * g.CQ * g.CK;
   uint8_t* z = w.z + (size_t)bh * g.CQt * g.CKt;
-  const int64_t ncell = (int64_t)g.CQt * g.CKt;
   int cnt = 0;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + tid; idx < ncell; idx += (int64_t)gridDim.x * 256) {
-    const int a = (int)(idx / g.CKt), b = (int)(idx - (int64_t)a * g.CKt);
-    uint8_t sel = 0;
-    if (a < g.CQ && b < g.CK) {
-      const int na = oq[a + 1] - oq[a], nb = ok[b + 1] - ok[b];
-      if (na > 0 && nb > 0) {
-        if (fo[a] == b) {
-          sel = 1;
-        } else if (done == 1) {
-          sel = 1;
-        } else if (done == 2) {
-          const int64_t vidx = (int64_t)a * g.CK + b;
-          sel = cell_key(pr[vidx], vidx) > bound;
-        }
-        cnt += sel;
-      }
-    } else {
-      sel = 1;  // dense-prefix query group or K/V group
+  // rows of the route matrix per block, up to KB columns per thread (their
+  // group sizes held in registers across the rows)
+  constexpr int KB = 8;
+  for (int cb = 0; cb < g.CKt; cb += 256 * KB) {
+    int nb[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int b = cb + tid + 256 * k;
+      nb[k] = b < g.CK ? ok[b + 1] - ok[b] : 0;
     }
-    z[idx] = sel;
+    for (int a = blockIdx.x; a < g.CQt; a += gridDim.x) {
+      uint8_t* zr = z + (size_t)a * g.CKt;
+      const bool arow = a < g.CQ;
+      const int na = arow ? oq[a + 1] - oq[a] : 0;
+      const int fa = na > 0 ? fo[a] : -1;
+      const int64_t row = (int64_t)a * g.CK;
+      float pv[KB];
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        const int b = cb + tid + 256 * k;
+        pv[k] = (done == 2 && na > 0 && b < g.CK && nb[k] > 0) ? pr[row + b] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        const int b = cb + tid + 256 * k;
+        if (b >= g.CKt) break;
+        uint8_t sel = 0;
+        if (arow && b < g.CK) {
+          if (na > 0 && nb[k] > 0) {
+            if (fa == b) {
+              sel = 1;
+            } else if (done == 1) {
+              sel = 1;
+            } else if (done == 2) {
+              sel = cell_key(pv[k], row + b) > bound;
+            }
+            cnt += sel;
+          }
+        } else {
+          sel = 1;  // dense-prefix query group or K/V group
+        }
+        zr[b] = sel;
+      }
+    }
   }
   cnt = wave_sum_i(cnt);
   if (lane == 0) red[wv] = cnt;
@@ -2001,12 +2024,24 @@ __global__ __launch_bounds__(256) void k_ranges(Geom g, Work w) {
   if (na > 0) {
     int prev_rt = 0;    // routing of the last nonempty group so far
     int start_key = 0;  // key of the last switch so far (a range start when prev_rt)
+    // the next 64 groups' offsets and routes are loaded before this slice
+    // is processed
+    int nks = lane < g.CKt ? ok[lane] : 0, nke = lane < g.CKt ? ok[lane + 1] : 0;
+    uint8_t nz = lane < g.CKt ? z[lane] : 0;
     for (int b0 = 0; b0 < g.CKt; b0 += 64) {
       const int b = b0 + lane;
       const bool in = b < g.CKt;
-      const int ks = in ? ok[b] : 0, ke = in ? ok[b + 1] : 0;
+      const int ks = nks, ke = nke;
+      const uint8_t zb = nz;
+      if (b0 + 64 < g.CKt) {
+        const int bn = b + 64;
+        const bool inn = bn < g.CKt;
+        nks = inn ? ok[bn] : 0;
+        nke = inn ? ok[bn + 1] : 0;
+        nz = inn ? z[bn] : 0;
+      }
       const bool ne = in && ke > ks;
-      const bool rt = ne && z[b] != 0;
+      const bool rt = ne && zb != 0;
       const uint64_t NE = __ballot(ne), RT = __ballot(rt);
       const uint64_t nb = NE & below;
       const int pr = nb ? (int)((RT >> (63 - __clzll((long long)nb))) & 1ull) : prev_rt;
