@@ -697,9 +697,12 @@ __global__ __launch_bounds__(128) void k_probe_merge(Geom g, const float* part,
   if (p >= nprobes[bh] || c >= g.dv) return;
   const int D = g.dv;
   const float* src = part + ((size_t)bq * g.M + p) * g.nsplit * (D + 2);
+  // both sweeps keep the split order; unrolled so that their loads overlap
   float m = -INFINITY;
+#pragma unroll 8
   for (int s = 0; s < g.nsplit; ++s) m = fmaxf(m, src[(size_t)s * (D + 2) + D]);
   float l = 0.f, o = 0.f;
+#pragma unroll 8
   for (int s = 0; s < g.nsplit; ++s) {
     const float* e = src + (size_t)s * (D + 2);
     const float f = exp2f(e[D] - m);

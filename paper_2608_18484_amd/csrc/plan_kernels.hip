@@ -2145,6 +2145,7 @@ __global__ __launch_bounds__(128) void k_probe_d2(Geom g, Work w) {
   const bool vec = (R & 3) == 0;
   const int LDP = R + 4;
   if (vec) {
+#pragma unroll 8
     for (int e = tid; e < rows * (R / 4); e += 128) {
       const int r = e / (R / 4), k4 = e - r * (R / 4);
       *(float4*)&ps[r * LDP + 4 * k4] = ((const float4*)phb)[e];
