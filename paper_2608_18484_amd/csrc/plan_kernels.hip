@@ -920,6 +920,8 @@ __global__ __launch_bounds__(256, RP <= 64 ? 3 : 2) void k_km_assign_mfma(KmArgs
       const float* cb = a.cent + ((size_t)bh * a.C + b) * R;
       float t = 0.f;
       if ((R & 3) == 0) {
+        // sixteen of the centroid's 16-byte loads in flight ahead of the chain
+#pragma unroll 16
         for (int k = 0; k < R; k += 4) {
           const float4 c4 = *(const float4*)(cb + k);
           t = fmaf(xs[k], c4.x, t);
