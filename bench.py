@@ -192,7 +192,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: every SparsePR head is an independent call, and "
-              "this build runs no multi-GPU path (heads would shard across GPUs without any "
+              "the library has no multi-GPU path (heads would shard across GPUs without any "
               "collective). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
